@@ -1,0 +1,343 @@
+"""CPU oracle for multi-component floating point (MCF) arithmetic.
+
+TEST INFRASTRUCTURE ONLY: imported by tests/, by the smoke check and by the
+CPU-baseline leg of bench.py.  The product library never imports, links or calls it,
+and it shares no code with the HIP implementation.
+
+The arithmetic lives in ``mcf_oracle.c`` (plain C, one rounding per printed step,
+see its header for the number model).  This module only marshals numpy arrays.
+
+Array conventions (component-major, "planar"):
+  * an MC array with nc components and logical shape S is an ndarray of shape
+    ``(nc, *S)``; a plain tensor has shape ``(1, *S)`` or ``S``;
+  * dtype is ``np.float16`` or ``np.float32`` (the component format).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+F16, F32 = 0, 1
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_SRC = os.path.join(_HERE, "mcf_oracle.c")
+
+OP_ADD, OP_MUL, OP_DIV, OP_EXP, OP_RENORM, OP_SIMPLE_RENORM, OP_SCALING_EXPAND = range(7)
+
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (no contraction, no fast-math, OpenMP)."""
+    if force or not os.path.exists(_LIB_PATH):
+        cmd = ["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-fopenmp",
+               "-fPIC", "-shared", "-Wall", "-o", _LIB_PATH + ".tmp", _SRC, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(_LIB_PATH + ".tmp", _LIB_PATH)
+    return _LIB_PATH
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
+            build()
+        L = ctypes.CDLL(_LIB_PATH)
+        vp, i64, ci, dbl = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_double
+        L.mcf_oracle_check_env.restype = ci
+        L.mcf_oracle_max_threads.restype = ci
+        for name in ("mcf_oracle_round", "mcf_oracle_fl_exp"):
+            getattr(L, name).restype = dbl
+            getattr(L, name).argtypes = [ci, dbl]
+        for name in ("mcf_oracle_fl_add", "mcf_oracle_fl_sub", "mcf_oracle_fl_mul", "mcf_oracle_fl_div"):
+            getattr(L, name).restype = dbl
+            getattr(L, name).argtypes = [ci, dbl, dbl]
+        L.mcf_oracle_fl_fma.restype = dbl
+        L.mcf_oracle_fl_fma.argtypes = [ci, dbl, dbl, dbl]
+        L.mcf_oracle_f16_decode.restype = dbl
+        L.mcf_oracle_f16_decode.argtypes = [ctypes.c_uint16]
+        L.mcf_oracle_f16_encode.restype = ctypes.c_uint16
+        L.mcf_oracle_f16_encode.argtypes = [dbl]
+        L.mcf_oracle_binop_array.restype = None
+        L.mcf_oracle_binop_array.argtypes = [ci, ci, i64, vp, vp, vp]
+        L.mcf_oracle_eft_array.restype = None
+        L.mcf_oracle_eft_array.argtypes = [ci, ci, i64, vp, vp, vp, vp]
+        L.mcf_oracle_elementwise.restype = ci
+        L.mcf_oracle_elementwise.argtypes = [ci, ci, ci, ci, i64, vp, ci, vp, ci, vp]
+        L.mcf_oracle_matmul.restype = ci
+        L.mcf_oracle_matmul.argtypes = [ci, ci, i64, i64, i64, vp, ci, vp, ci, vp, vp, i64, vp]
+        L.mcf_oracle_linear.restype = ci
+        L.mcf_oracle_linear.argtypes = [ci, ci, i64, i64, i64, vp, vp, vp, vp, vp, i64, vp]
+        L.mcf_oracle_matmul_exact_err.restype = ci
+        L.mcf_oracle_matmul_exact_err.argtypes = [ci, ci, i64, i64, i64, vp, ci, vp, ci, vp, ci,
+                                                  vp, vp, i64, vp, vp, vp, vp]
+        L.mcf_oracle_exact_diff.restype = None
+        L.mcf_oracle_exact_diff.argtypes = [ci, i64, vp, ci, vp, ci, vp]
+        if L.mcf_oracle_check_env() != 0:
+            raise RuntimeError("oracle: SSE flush-to-zero or denormals-are-zero is set")
+        _lib = L
+    return _lib
+
+
+def fmt_of(dtype) -> int:
+    dt = np.dtype(dtype)
+    if dt == np.float16:
+        return F16
+    if dt == np.float32:
+        return F32
+    raise TypeError(f"component dtype must be float16 or float32, got {dt}")
+
+
+def _ptr(a: np.ndarray | None):
+    return None if a is None else ctypes.c_void_p(a.ctypes.data)
+
+
+def _planar(a: np.ndarray, dtype) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def threads() -> int:
+    return int(lib().mcf_oracle_max_threads())
+
+
+# ---------------------------------------------------------------------------------
+# scalar primitives on float64 arrays (values exactly representable in the format)
+# ---------------------------------------------------------------------------------
+
+def _binop(fmt: int, op: int, a, b=None) -> np.ndarray:
+    a = np.ascontiguousarray(a, dtype=np.float64).ravel()
+    b = a if b is None else np.ascontiguousarray(b, dtype=np.float64).ravel()
+    out = np.empty_like(a)
+    lib().mcf_oracle_binop_array(fmt, op, a.size, _ptr(a), _ptr(b), _ptr(out))
+    return out
+
+
+def fl_round(fmt, x):
+    """fl(x): round float64 values to the component format (returned as float64)."""
+    return _binop(fmt, 6, x)
+
+
+def fl_add(fmt, a, b):
+    return _binop(fmt, 0, a, b)
+
+
+def fl_sub(fmt, a, b):
+    return _binop(fmt, 1, a, b)
+
+
+def fl_mul(fmt, a, b):
+    return _binop(fmt, 2, a, b)
+
+
+def fl_div(fmt, a, b):
+    return _binop(fmt, 3, a, b)
+
+
+def two_prod_err(fmt, a, b):
+    """fma(a, b, -fl(a*b)) rounded once."""
+    return _binop(fmt, 4, a, b)
+
+
+def fl_exp(fmt, a):
+    """Correctly rounded component exponential."""
+    return _binop(fmt, 5, a)
+
+
+def two_sum(fmt, a, b):
+    a = np.ascontiguousarray(a, dtype=np.float64).ravel()
+    b = np.ascontiguousarray(b, dtype=np.float64).ravel()
+    s, e = np.empty_like(a), np.empty_like(a)
+    lib().mcf_oracle_eft_array(fmt, 0, a.size, _ptr(a), _ptr(b), _ptr(s), _ptr(e))
+    return s, e
+
+
+def two_prod(fmt, a, b):
+    a = np.ascontiguousarray(a, dtype=np.float64).ravel()
+    b = np.ascontiguousarray(b, dtype=np.float64).ravel()
+    s, e = np.empty_like(a), np.empty_like(a)
+    lib().mcf_oracle_eft_array(fmt, 1, a.size, _ptr(a), _ptr(b), _ptr(s), _ptr(e))
+    return s, e
+
+
+# ---------------------------------------------------------------------------------
+# elementwise MC operations on planar arrays
+# ---------------------------------------------------------------------------------
+
+def _as_operand(a, nc, is_mc, dtype):
+    a = _planar(a, dtype)
+    planes = nc if is_mc else 1
+    if a.shape[0] != planes:
+        a = a.reshape((1,) + a.shape) if not is_mc else a
+    if a.shape[0] != planes:
+        raise ValueError(f"operand has {a.shape[0]} planes, expected {planes}")
+    return a
+
+
+def elementwise(op: int, x, y=None, *, nc: int, x_mc=True, y_mc=True, nc_out=None, dtype=None):
+    dtype = np.dtype(dtype or np.asarray(x).dtype)
+    fmt = fmt_of(dtype)
+    x = _as_operand(x, nc, x_mc, dtype)
+    shape = x.shape[1:]
+    n = int(np.prod(shape)) if shape else 1
+    if y is not None:
+        y = _as_operand(y, nc, y_mc, dtype)
+        if y.shape[1:] != shape:
+            raise ValueError("shape mismatch")
+    if op in (OP_RENORM, OP_SIMPLE_RENORM):
+        planes_out = nc_out
+    elif op == OP_SCALING_EXPAND:
+        planes_out = nc + 1
+    else:
+        planes_out = nc
+    out = np.empty((planes_out,) + shape, dtype=dtype)
+    rc = lib().mcf_oracle_elementwise(fmt, op, nc, nc_out or nc, n, _ptr(x), int(bool(x_mc)), _ptr(y),
+                                      int(bool(y_mc)), _ptr(out))
+    if rc != 0:
+        raise ValueError("oracle: bad arguments")
+    return out
+
+
+def add(x, y, *, nc, x_mc=True, y_mc=True):
+    """Add-MCN (MC,MC) or Grow-ExpN (MC,T)/(T,MC)."""
+    return elementwise(OP_ADD, x, y, nc=nc, x_mc=x_mc, y_mc=y_mc)
+
+
+def mul(x, y, *, nc, x_mc=True, y_mc=True):
+    """Mult-MCN (MC,MC) or ScalingN (MC,T)/(T,MC)."""
+    return elementwise(OP_MUL, x, y, nc=nc, x_mc=x_mc, y_mc=y_mc)
+
+
+def div(x, y, *, nc, x_mc=True, y_mc=True):
+    """Div-MCN (MC,MC), DivN (T,MC), Div-MCN with a zero-padded divisor (MC,T)."""
+    return elementwise(OP_DIV, x, y, nc=nc, x_mc=x_mc, y_mc=y_mc)
+
+
+def exp(x, *, nc):
+    """Exp-MCN."""
+    return elementwise(OP_EXP, x, nc=nc)
+
+
+def renorm(x, *, nc, nc_out=None, mode=0):
+    """mode 0: Renormalize; mode 1: Simple-Renorm."""
+    return elementwise(OP_RENORM if mode == 0 else OP_SIMPLE_RENORM, x, nc=nc, nc_out=nc_out or nc)
+
+
+def scaling_expand(x, v, *, nc):
+    """ScalingN with expand: nc+1 output components."""
+    return elementwise(OP_SCALING_EXPAND, x, v, nc=nc, x_mc=True, y_mc=False)
+
+
+# ---------------------------------------------------------------------------------
+# matrix products
+# ---------------------------------------------------------------------------------
+
+def _positions(M, N, rows, cols):
+    if rows is None:
+        return None, None, M * N
+    rows = np.ascontiguousarray(rows, dtype=np.int64).ravel()
+    cols = np.ascontiguousarray(cols, dtype=np.int64).ravel()
+    if rows.shape != cols.shape:
+        raise ValueError("rows/cols mismatch")
+    if rows.size and (rows.min() < 0 or rows.max() >= M or cols.min() < 0 or cols.max() >= N):
+        raise ValueError("position out of range")
+    return rows, cols, rows.size
+
+
+def matmul(A, B, *, nc, a_mc=True, b_mc=True, rows=None, cols=None):
+    """C = A x B (MM-MCN order; MC x MC by linearity over B's components).
+
+    A: (nc|1, M, K), B: (nc|1, K, N).  Returns (nc, M, N), or (nc, count) at the
+    given positions.
+    """
+    dtype = np.dtype(A.dtype)
+    fmt = fmt_of(dtype)
+    A = _planar(A, dtype)
+    B = _planar(B, dtype)
+    if A.ndim == 2:
+        A = A[None]
+    if B.ndim == 2:
+        B = B[None]
+    M, K = A.shape[1:]
+    K2, N = B.shape[1:]
+    if K2 != K or A.shape[0] != (nc if a_mc else 1) or B.shape[0] != (nc if b_mc else 1):
+        raise ValueError("matmul: shape mismatch")
+    r, c, count = _positions(M, N, rows, cols)
+    out = np.empty((nc, count), dtype=dtype)
+    rc = lib().mcf_oracle_matmul(fmt, nc, M, N, K, _ptr(A), int(a_mc), _ptr(B), int(b_mc), _ptr(r), _ptr(c),
+                                 count, _ptr(out))
+    if rc != 0:
+        raise ValueError("oracle: bad arguments")
+    return out.reshape(nc, M, N) if rows is None else out
+
+
+def linear(X, W, bias=None, *, nc, rows=None, cols=None):
+    """MC-Linear forward: X plain (T, I), W (nc, O, I), bias (nc, O) or None."""
+    dtype = np.dtype(W.dtype)
+    fmt = fmt_of(dtype)
+    X = _planar(X, dtype)
+    W = _planar(W, dtype)
+    T, I = X.shape[-2:]
+    O = W.shape[1]
+    if W.shape != (nc, O, I):
+        raise ValueError("linear: shape mismatch")
+    if bias is not None:
+        bias = _planar(bias, dtype)
+        if bias.shape != (nc, O):
+            raise ValueError("linear: bias shape mismatch")
+    r, c, count = _positions(T, O, rows, cols)
+    out = np.empty((nc, count), dtype=dtype)
+    rc = lib().mcf_oracle_linear(fmt, nc, T, I, O, _ptr(X), _ptr(W), _ptr(bias), _ptr(r), _ptr(c), count,
+                                 _ptr(out))
+    if rc != 0:
+        raise ValueError("oracle: bad arguments")
+    return out.reshape(nc, T, O) if rows is None else out
+
+
+def matmul_exact_err(A, B, C, *, bias=None, rows=None, cols=None):
+    """Exact error of a computed product C (nc, M, N) -- or (nc, count) at positions --
+    against the exact product of the MC inputs A (planes, M, K), B (planes, K, N),
+    plus an optional bias (planes, N).
+
+    Returns (err, absab, exact) as float64 arrays: err = sum(C) - exact (computed
+    exactly, then rounded), absab = sum_k |A^_ik||B^_kj| (+|bias^_j|).
+    """
+    dtype = np.dtype(A.dtype)
+    fmt = fmt_of(dtype)
+    A = _planar(A, dtype)
+    B = _planar(B, dtype)
+    if A.ndim == 2:
+        A = A[None]
+    if B.ndim == 2:
+        B = B[None]
+    M, K = A.shape[1:]
+    N = B.shape[2]
+    nc = C.shape[0]
+    r, c, count = _positions(M, N, rows, cols)
+    Cf = _planar(C, dtype).reshape(nc, count)
+    if bias is not None:
+        bias = _planar(bias, dtype)
+        if bias.ndim == 1:
+            bias = bias[None]
+    err = np.empty(count)
+    absab = np.empty(count)
+    exact = np.empty(count)
+    lib().mcf_oracle_matmul_exact_err(fmt, nc, M, N, K, _ptr(A), A.shape[0], _ptr(B), B.shape[0], _ptr(bias),
+                                      0 if bias is None else bias.shape[0], _ptr(r), _ptr(c), count, _ptr(Cf),
+                                      _ptr(err), _ptr(absab), _ptr(exact))
+    return err, absab, exact
+
+
+def exact_diff(x, y=None):
+    """Exact (x - y) per element, rounded to double; x, y planar with any plane count."""
+    dtype = np.dtype(x.dtype)
+    fmt = fmt_of(dtype)
+    x = _planar(x, dtype)
+    n = int(np.prod(x.shape[1:]))
+    if y is not None:
+        y = _planar(y, dtype)
+    out = np.empty(n)
+    lib().mcf_oracle_exact_diff(fmt, n, _ptr(x), x.shape[0], _ptr(y), 0 if y is None else y.shape[0], _ptr(out))
+    return out.reshape(x.shape[1:])

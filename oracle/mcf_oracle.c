@@ -1,0 +1,710 @@
+/*
+ * mcf_oracle.c -- plain, slow CPU oracle for multi-component floating point (MCF)
+ * arithmetic as defined in "MCTensor: A High-Precision Deep Learning Library with
+ * Multi-Component Floating-Point" (Yu, Guo, Li, Yuan, De Sa; arXiv 2207.08867).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product library calls, links or
+ * includes this file; only the test-suite, the smoke check and the CPU-baseline leg
+ * of the benchmark load it.  It shares no code, header, table or constant with the
+ * HIP implementation.
+ *
+ * Number model (Section 2.1 and Appendix A.2.1 write every step as fl(.), one
+ * rounding in the component format):
+ *   - A component value is held in a C double.  Every double handled here is
+ *     exactly representable in the component format (binary16 or binary32).
+ *   - fl(.) is IEEE-754 round-to-nearest-even into the component format, with
+ *     gradual underflow and overflow to infinity.  It is implemented from the IEEE
+ *     definition in round_to() below, on top of an exact or correctly-rounded double.
+ *   - + - : the double sum of two binary16 values is exact; for binary32 the double
+ *     sum is one extra rounding that is innocuous because 53 >= 2*24+2 (Figueroa,
+ *     "When is double rounding innocuous?", SIGNUM 1995).
+ *   - *   : the double product of two binary16/binary32 values is exact.
+ *   - /   : correctly-rounded double quotient, then fl(.); innocuous by the same
+ *     theorem (53 >= 2p+2 for p = 11 and p = 24).
+ *   - fma : exact product, double sum with its exact remainder, then fl(.) with the
+ *     remainder's sign used to break a tie (see fl_fma).
+ *   - exp : the component exponential is taken to be correctly rounded (the paper
+ *     calls torch.exp and fixes no accuracy); computed as fl(.) of a double
+ *     (binary16) or long double (binary32) exponential.  Exhaustive pinning for
+ *     binary16 lives in the tests.
+ * Build with -ffp-contract=off and without fast-math; mcf_oracle_check_env()
+ * verifies that the SSE flush-to-zero / denormals-are-zero bits are clear.
+ *
+ * Layout of array arguments: component-major ("planar") -- component c of element i
+ * is at index c*n + i.  binary16 data are passed as raw uint16 bit patterns,
+ * binary32 data as float.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <xmmintrin.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define FMT_F16 0
+#define FMT_F32 1
+#define MAXC 8 /* largest component count handled by the fixed-size scratch arrays */
+
+/* ------------------------------------------------------------------------------ */
+/* Component formats and rounding                                                   */
+/* ------------------------------------------------------------------------------ */
+
+typedef struct {
+  int p;    /* significand bits, hidden bit included */
+  int emin; /* exponent of the smallest normal number */
+  int emax; /* exponent of the largest finite number */
+} fmt_desc;
+
+static const fmt_desc FMTS[2] = {{11, -14, 15}, {24, -126, 127}};
+
+/* Round the real number x + r to the format, where x is a double and r is an
+ * infinitesimal remainder whose sign is dir (-1, 0 or +1).  IEEE round to nearest,
+ * ties to even, gradual underflow, overflow to infinity. */
+static double round_to(int f, double x, int dir) {
+  const fmt_desc *d = &FMTS[f];
+  if (isnan(x) || isinf(x)) return x;
+  if (x == 0.0) {
+    if (dir == 0) return x;
+    return dir > 0 ? 0.0 : -0.0; /* |x + r| is far below half the smallest subnormal */
+  }
+  int neg = signbit(x) ? 1 : 0;
+  double ax = fabs(x);
+  int mdir = neg ? -dir : dir; /* direction of the remainder for the magnitude */
+  int e2;
+  frexp(ax, &e2);          /* ax = m * 2^e2 with m in [0.5, 1): leading bit at 2^(e2-1) */
+  int lead = e2 - 1;
+  int q = lead - (d->p - 1); /* exponent of the last significand bit */
+  int qmin = d->emin - (d->p - 1);
+  if (q < qmin) q = qmin;    /* subnormal range: fixed quantum 2^qmin */
+  double scaled = ldexp(ax, -q); /* exact: power-of-two scaling, scaled < 2^p */
+  double n = floor(scaled);
+  double frac = scaled - n;      /* exact: scaled < 2^53 */
+  if (frac > 0.5) {
+    n += 1.0;
+  } else if (frac == 0.5) {
+    if (mdir > 0)
+      n += 1.0;
+    else if (mdir == 0 && fmod(n, 2.0) != 0.0)
+      n += 1.0;
+  }
+  double r = ldexp(n, q);
+  if (r >= ldexp(1.0, d->emax + 1)) r = INFINITY;
+  return neg ? -r : r;
+}
+
+static double fl(int f, double x) { return round_to(f, x, 0); }
+
+static double fl_add(int f, double a, double b) { return fl(f, a + b); }
+static double fl_sub(int f, double a, double b) { return fl(f, a - b); }
+static double fl_mul(int f, double a, double b) { return fl(f, a * b); }
+static double fl_div(int f, double a, double b) { return fl(f, a / b); }
+
+/* fma(a, b, c) rounded once.  a*b is exact in double; s = a*b + c is rounded in
+ * double and t is its exact remainder (Knuth's six-operation sum in double, used here
+ * only as exact double-precision bookkeeping).  fl(s) is the correctly rounded result
+ * unless s sits exactly on a tie of the component format, where t decides. */
+static double fl_fma(int f, double a, double b, double c) {
+  double pr = a * b;
+  double s = pr + c;
+  double bv = s - pr;
+  double av = s - bv;
+  double t = (pr - av) + (c - bv);
+  if (isnan(t) || isinf(s)) return fl(f, s);
+  return round_to(f, s, t > 0 ? 1 : (t < 0 ? -1 : 0));
+}
+
+/* Correctly rounded component exponential (a reading: the paper calls torch.exp). */
+static double fl_exp(int f, double a) {
+  if (f == FMT_F16) return fl(f, exp(a));
+  long double e = expl((long double)a);
+  double hi = (double)e;
+  long double lo = e - (long double)hi;
+  return round_to(f, hi, lo > 0 ? 1 : (lo < 0 ? -1 : 0));
+}
+
+/* binary16 bit pattern <-> double, from the IEEE-754 definition. */
+static double f16_decode(uint16_t h) {
+  int s = h >> 15, e = (h >> 10) & 0x1f, m = h & 0x3ff;
+  double v;
+  if (e == 0x1f)
+    v = m ? NAN : INFINITY;
+  else if (e == 0)
+    v = ldexp((double)m, -24);
+  else
+    v = ldexp((double)(m + 1024), e - 25);
+  return s ? -v : v;
+}
+
+static uint16_t f16_encode(double v) { /* v must be exactly representable */
+  uint16_t s = signbit(v) ? 0x8000 : 0;
+  double a = fabs(v);
+  if (isnan(v)) return 0x7e00;
+  if (isinf(v)) return s | 0x7c00;
+  if (a == 0.0) return s;
+  if (a < ldexp(1.0, -14)) return s | (uint16_t)(a * ldexp(1.0, 24));
+  int e2;
+  double m = frexp(a, &e2); /* a = m 2^e2, m in [0.5,1) */
+  int e = e2 - 1;           /* a = (1.f) 2^e */
+  uint16_t mant = (uint16_t)((m * 2.0 - 1.0) * 1024.0);
+  return s | (uint16_t)((e + 15) << 10) | mant;
+}
+
+static double load_c(int f, const void *base, int64_t idx) {
+  if (f == FMT_F16) return f16_decode(((const uint16_t *)base)[idx]);
+  return (double)((const float *)base)[idx];
+}
+
+static void store_c(int f, void *base, int64_t idx, double v) {
+  if (f == FMT_F16)
+    ((uint16_t *)base)[idx] = f16_encode(v);
+  else
+    ((float *)base)[idx] = (float)v;
+}
+
+/* ------------------------------------------------------------------------------ */
+/* Error-free transformations (Appendix A.2.1)                                      */
+/* ------------------------------------------------------------------------------ */
+
+/* Two-Sum: s = fl(a+b) and its exact error, six operations in the printed order. */
+static void two_sum(int f, double a, double b, double *s, double *e) {
+  double x = fl_add(f, a, b);
+  double b_virtual = fl_sub(f, x, a);
+  double a_virtual = fl_sub(f, x, b_virtual);
+  double b_roundoff = fl_sub(f, b, b_virtual);
+  double a_roundoff = fl_sub(f, a, a_virtual);
+  *s = x;
+  *e = fl_add(f, a_roundoff, b_roundoff);
+}
+
+/* Two-Prod, FMA variant: p = fl(a*b), e = fl(a*b - p) in one rounding. */
+static void two_prod(int f, double a, double b, double *p, double *e) {
+  *p = fl_mul(f, a, b);
+  *e = fl_fma(f, a, b, -*p);
+}
+
+/* Simple-Renorm: move the zero components back.  Reading used throughout: every one
+ * of the m inputs is scanned (the prose says all non-zero values are extracted) and
+ * the first r non-zero ones are kept in order; empty slots are +0. */
+static void simple_renorm(const double *h, int m, int r, double *b) {
+  int k = 0;
+  for (int i = 0; i < r; ++i) b[i] = 0.0;
+  for (int i = 0; i < m; ++i) {
+    if (h[i] != 0.0 && k < r) {
+      b[k] = h[i];
+      k += 1;
+    }
+  }
+}
+
+/* Renormalize (Priest variant, Appendix A.2.1).  Readings: the first sweep runs over
+ * the components that exist (i = 1..n-1); t_0 = 0 is kept; the value left in s after
+ * the second sweep is emitted if a slot is free, so no part of the sum is dropped. */
+static void renormalize(int f, const double *x, int n, int r, double *b) {
+  double t[MAXC + 1];
+  double s = x[0];
+  t[0] = 0.0;
+  for (int i = 1; i < n; ++i) two_sum(f, x[i], s, &s, &t[i]);
+  int k = 0;
+  for (int i = 0; i < r; ++i) b[i] = 0.0;
+  for (int i = 0; i < n; ++i) {
+    double e;
+    two_sum(f, s, t[i], &s, &e);
+    if (e != 0.0) {
+      if (k < r) b[k] = s;
+      s = e;
+      k += 1;
+    }
+  }
+  if (k < r) b[k] = s;
+}
+
+/* Grow-ExpN (Section 2.1): an n-component value plus a plain value v. */
+static void grow_expn(int f, const double *x, int n, double v, double *out) {
+  double h[MAXC + 1];
+  double Q = v;
+  for (int i = 1; i <= n; ++i) {
+    int k = n + 1 - i;
+    two_sum(f, x[k - 1], Q, &Q, &h[k]);
+  }
+  h[0] = Q;
+  simple_renorm(h, n + 1, n, out);
+}
+
+/* ScalingN (Appendix A.2.1): an m-component value times a plain value v.  With
+ * expand the m+1 terms are all kept, otherwise m. */
+static void scaling_n(int f, const double *x, int m, double v, int expand, double *out) {
+  double h[MAXC + 1];
+  double e = 0.0;
+  for (int i = 0; i < m; ++i) {
+    double hp, e1, e2;
+    two_prod(f, x[i], v, &hp, &e1);
+    two_sum(f, hp, e, &h[i], &e2);
+    e = fl_add(f, e1, e2);
+  }
+  h[m] = e;
+  simple_renorm(h, m + 1, expand ? m + 1 : m, out);
+}
+
+/* Add-MCN (Appendix A.2.1): sum of two n-component values. */
+static void add_mcn(int f, const double *x, const double *y, int n, double *out) {
+  double h[MAXC + 1];
+  double e = 0.0;
+  for (int i = 0; i < n; ++i) {
+    double hp, e1, e2;
+    two_sum(f, x[i], y[i], &hp, &e1);
+    two_sum(f, hp, e, &h[i], &e2);
+    e = fl_add(f, e1, e2);
+  }
+  h[n] = e;
+  simple_renorm(h, n + 1, n, out);
+}
+
+/* Div-MCN (Appendix A.2.1): long division, n+1 quotient digits, n corrections. */
+static void div_mcn(int f, const double *x_in, const double *y, int n, double *out) {
+  double h[MAXC + 1], x[MAXC] = {0.0}, s[MAXC], neg[MAXC];
+  for (int i = 0; i < n; ++i) x[i] = x_in[i];
+  double q = fl_div(f, x[0], y[0]);
+  h[0] = q;
+  for (int i = 1; i <= n; ++i) {
+    scaling_n(f, y, n, q, 0, s);
+    for (int c = 0; c < n; ++c) neg[c] = -s[c]; /* negation is exact */
+    double r[MAXC];
+    add_mcn(f, x, neg, n, r);
+    for (int c = 0; c < n; ++c) x[c] = r[c];
+    q = fl_div(f, x[0], y[0]);
+    h[i] = q;
+  }
+  simple_renorm(h, n + 1, n, out);
+}
+
+/* DivN (Appendix A.2.1): plain value over an n-component value, by padding the
+ * plain value with zero components. */
+static void div_n(int f, double v, const double *y, int n, double *out) {
+  double x[MAXC];
+  x[0] = v;
+  for (int i = 1; i < n; ++i) x[i] = 0.0;
+  div_mcn(f, x, y, n, out);
+}
+
+/* Mult-MCN, fast version (Appendix A.2.1): x / (1/y), each quotient renormalized. */
+static void mult_mcn(int f, const double *x, const double *y, int n, double *out) {
+  double one[MAXC], q[MAXC], yinv[MAXC];
+  one[0] = 1.0;
+  for (int i = 1; i < n; ++i) one[i] = 0.0;
+  div_mcn(f, one, y, n, q);
+  renormalize(f, q, n, n, yinv);
+  div_mcn(f, x, yinv, n, q);
+  renormalize(f, q, n, n, out);
+}
+
+/* Exp-MCN (Appendix A.2.1).  Reading: the factor of step i is exp(x_i) (the printed
+ * exp(h_i) is taken as a typo); h starts with one component and ScalingN with expand
+ * grows it by one per step, to n components. */
+static void exp_mcn(int f, const double *x, int n, double *out) {
+  double h[MAXC + 1], t[MAXC + 1];
+  int m = 1;
+  h[0] = fl_exp(f, x[0]);
+  for (int i = 1; i < n; ++i) {
+    scaling_n(f, h, m, fl_exp(f, x[i]), 1, t);
+    m += 1;
+    for (int c = 0; c < m; ++c) h[c] = t[c];
+  }
+  for (int c = 0; c < n; ++c) out[c] = h[c];
+}
+
+/* ------------------------------------------------------------------------------ */
+/* Environment check                                                                */
+/* ------------------------------------------------------------------------------ */
+
+/* Returns 0 when the SSE control word has flush-to-zero and denormals-are-zero clear
+ * (gradual underflow is part of the number model). */
+int mcf_oracle_check_env(void) {
+  unsigned int csr = _mm_getcsr();
+  return (csr & 0x8040u) ? -1 : 0;
+}
+
+int mcf_oracle_max_threads(void) {
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
+}
+
+/* ------------------------------------------------------------------------------ */
+/* Scalar primitives exported for pinning tests (values as doubles)                  */
+/* ------------------------------------------------------------------------------ */
+
+double mcf_oracle_round(int f, double x) { return fl(f, x); }
+double mcf_oracle_fl_add(int f, double a, double b) { return fl_add(f, a, b); }
+double mcf_oracle_fl_sub(int f, double a, double b) { return fl_sub(f, a, b); }
+double mcf_oracle_fl_mul(int f, double a, double b) { return fl_mul(f, a, b); }
+double mcf_oracle_fl_div(int f, double a, double b) { return fl_div(f, a, b); }
+double mcf_oracle_fl_fma(int f, double a, double b, double c) { return fl_fma(f, a, b, c); }
+double mcf_oracle_fl_exp(int f, double a) { return fl_exp(f, a); }
+double mcf_oracle_f16_decode(uint16_t h) { return f16_decode(h); }
+uint16_t mcf_oracle_f16_encode(double v) { return f16_encode(v); }
+
+/* Vectorised versions over arrays of doubles (for exhaustive pins). op: 0 add, 1 sub,
+ * 2 mul, 3 div, 4 fma(a,b,-fl(a*b)) i.e. the Two-Prod error, 5 exp(a), 6 round(a). */
+void mcf_oracle_binop_array(int f, int op, int64_t n, const double *a, const double *b, double *out) {
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < n; ++i) {
+    double r;
+    switch (op) {
+      case 0: r = fl_add(f, a[i], b[i]); break;
+      case 1: r = fl_sub(f, a[i], b[i]); break;
+      case 2: r = fl_mul(f, a[i], b[i]); break;
+      case 3: r = fl_div(f, a[i], b[i]); break;
+      case 4: r = fl_fma(f, a[i], b[i], -fl_mul(f, a[i], b[i])); break;
+      case 5: r = fl_exp(f, a[i]); break;
+      default: r = fl(f, a[i]); break;
+    }
+    out[i] = r;
+  }
+}
+
+/* Two-Sum / Two-Prod on arrays of doubles: outputs s (or p) and e. */
+void mcf_oracle_eft_array(int f, int prod, int64_t n, const double *a, const double *b, double *s, double *e) {
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < n; ++i) {
+    if (prod)
+      two_prod(f, a[i], b[i], &s[i], &e[i]);
+    else
+      two_sum(f, a[i], b[i], &s[i], &e[i]);
+  }
+}
+
+/* ------------------------------------------------------------------------------ */
+/* Elementwise MC operations over planar arrays                                     */
+/* ------------------------------------------------------------------------------ */
+
+/* Gather element i of a planar operand with xn planes. */
+static void gather(int f, const void *base, int xn, int64_t n, int64_t i, double *v) {
+  for (int c = 0; c < xn; ++c) v[c] = load_c(f, base, (int64_t)c * n + i);
+}
+
+static void scatter(int f, void *base, int nc, int64_t n, int64_t i, const double *v) {
+  for (int c = 0; c < nc; ++c) store_c(f, base, (int64_t)c * n + i, v[c]);
+}
+
+/* Operation codes for mcf_oracle_elementwise. */
+enum { OP_ADD = 0, OP_MUL = 1, OP_DIV = 2, OP_EXP = 3, OP_RENORM = 4, OP_SIMPLE_RENORM = 5,
+       OP_SCALING_EXPAND = 6 };
+
+/* out = op(x, y) elementwise over n elements.  x_mc / y_mc say whether an operand is
+ * an MC value (nc planes) or a plain tensor (one plane).
+ *   ADD : (MC,MC) Add-MCN; (MC,T) and (T,MC) Grow-ExpN.
+ *   MUL : (MC,MC) Mult-MCN (fast); (MC,T) and (T,MC) ScalingN without expand.
+ *   DIV : (MC,MC) Div-MCN; (T,MC) DivN; (MC,T) Div-MCN with the divisor padded by zeros.
+ *   EXP : Exp-MCN of x (MC).
+ *   RENORM / SIMPLE_RENORM : x (MC) has nc components, out has nc_out.
+ *   SCALING_EXPAND : (MC,T) ScalingN with expand, out has nc+1 components.
+ * Returns 0, or -1 on bad arguments. */
+int mcf_oracle_elementwise(int f, int op, int nc, int nc_out, int64_t n, const void *x, int x_mc,
+                           const void *y, int y_mc, void *out) {
+  if (nc < 1 || nc > MAXC || (f != FMT_F16 && f != FMT_F32)) return -1;
+  int binary = (op == OP_ADD || op == OP_MUL || op == OP_DIV || op == OP_SCALING_EXPAND);
+  if (binary && !x_mc && !y_mc) return -1;
+  if ((op == OP_RENORM || op == OP_SIMPLE_RENORM) && (nc_out < 1 || nc_out > nc)) return -1;
+  int xn = x_mc ? nc : 1, yn = y_mc ? nc : 1;
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < n; ++i) {
+    double a[MAXC + 1], b[MAXC + 1], r[MAXC + 1];
+    for (int c = 0; c < MAXC + 1; ++c) a[c] = b[c] = r[c] = 0.0;
+    gather(f, x, xn, n, i, a);
+    if (binary) gather(f, y, yn, n, i, b);
+    int rn = nc;
+    switch (op) {
+      case OP_ADD:
+        if (x_mc && y_mc)
+          add_mcn(f, a, b, nc, r);
+        else if (x_mc)
+          grow_expn(f, a, nc, b[0], r);
+        else
+          grow_expn(f, b, nc, a[0], r);
+        break;
+      case OP_MUL:
+        if (x_mc && y_mc)
+          mult_mcn(f, a, b, nc, r);
+        else if (x_mc)
+          scaling_n(f, a, nc, b[0], 0, r);
+        else
+          scaling_n(f, b, nc, a[0], 0, r);
+        break;
+      case OP_DIV:
+        if (x_mc && y_mc)
+          div_mcn(f, a, b, nc, r);
+        else if (y_mc)
+          div_n(f, a[0], b, nc, r);
+        else
+          div_mcn(f, a, b, nc, r); /* (MC,T): the divisor is (v, 0, ..., 0) */
+        break;
+      case OP_EXP:
+        exp_mcn(f, a, nc, r);
+        break;
+      case OP_RENORM:
+        renormalize(f, a, nc, nc_out, r);
+        rn = nc_out;
+        break;
+      case OP_SIMPLE_RENORM:
+        simple_renorm(a, nc, nc_out, r);
+        rn = nc_out;
+        break;
+      case OP_SCALING_EXPAND:
+        scaling_n(f, a, nc, b[0], 1, r);
+        rn = nc + 1;
+        break;
+    }
+    scatter(f, out, rn, n, i, r);
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------------ */
+/* Matrix products (Appendix A.2.2)                                                  */
+/* ------------------------------------------------------------------------------ */
+
+typedef struct {
+  int f;
+  const void *A; /* MC (nc planes) when a_mc, else one plane */
+  int a_mc;
+  const void *B;
+  int b_mc;
+  int64_t K;
+  int64_t lda_m, lda_k; /* element strides of A along its row index and along k */
+  int64_t ldb_k, ldb_n; /* element strides of B along k and along its column index */
+  int64_t a_plane, b_plane;
+} mm_args;
+
+/* Term k of output (i, j): the MC factor (nc components) and the plain factor.  When
+ * both operands are MC, the plain factor is component `bcomp` of B[k][j]. */
+static void mm_term(const mm_args *g, int nc, int64_t i, int64_t j, int64_t k, int bcomp, double *mc,
+                    double *plain) {
+  if (g->a_mc) {
+    for (int c = 0; c < nc; ++c) mc[c] = load_c(g->f, g->A, c * g->a_plane + i * g->lda_m + k * g->lda_k);
+    *plain = load_c(g->f, g->B, bcomp * g->b_plane + k * g->ldb_k + j * g->ldb_n);
+  } else {
+    for (int c = 0; c < nc; ++c) mc[c] = load_c(g->f, g->B, c * g->b_plane + k * g->ldb_k + j * g->ldb_n);
+    *plain = load_c(g->f, g->A, i * g->lda_m + k * g->lda_k);
+  }
+}
+
+/* MM-MCN for one output of an MC matrix times a plain matrix:
+ * acc = ScalingN(term 0); acc = Add-MCN(acc, ScalingN(term k)) for k = 1..K-1,
+ * the sequential order in which the paper propagates the addition error.
+ * K = 0 gives +0 in every component. */
+static void mm_entry_plain(const mm_args *g, int nc, int64_t i, int64_t j, int bcomp, double *acc) {
+  double mc[MAXC], term[MAXC], t[MAXC], v;
+  for (int c = 0; c < nc; ++c) acc[c] = 0.0;
+  for (int64_t k = 0; k < g->K; ++k) {
+    mm_term(g, nc, i, j, k, bcomp, mc, &v);
+    scaling_n(g->f, mc, nc, v, 0, term);
+    if (k == 0) {
+      for (int c = 0; c < nc; ++c) acc[c] = term[c];
+    } else {
+      add_mcn(g->f, acc, term, nc, t);
+      for (int c = 0; c < nc; ++c) acc[c] = t[c];
+    }
+  }
+}
+
+/* One output C[i][j].  MC x plain and plain x MC follow MM-MCN directly.  MC x MC is
+ * not defined in the paper (its matrix operators take one MC and one plain operand);
+ * reading: linearity over the components of B,
+ *   C = MM(A, B^(0)) (+) MM(A, B^(1)) (+) ... (+) MM(A, B^(nc-1)),
+ * with (+) = Add-MCN applied left to right. */
+static void mm_entry(const mm_args *g, int nc, int64_t i, int64_t j, double *out) {
+  if (g->a_mc && g->b_mc) {
+    double part[MAXC], t[MAXC];
+    mm_entry_plain(g, nc, i, j, 0, out);
+    for (int b = 1; b < nc; ++b) {
+      mm_entry_plain(g, nc, i, j, b, part);
+      add_mcn(g->f, out, part, nc, t);
+      for (int c = 0; c < nc; ++c) out[c] = t[c];
+    }
+  } else {
+    mm_entry_plain(g, nc, i, j, 0, out);
+  }
+}
+
+/* C = A x B with A [M][K] and B [K][N] row-major planes (nc planes when MC, one when
+ * plain; at least one MC), evaluated only at the `count` positions (rows[t], cols[t]);
+ * out is [nc][count].  rows == NULL means every position in row-major order (count
+ * must then be M*N).  Returns 0, or -1 on bad arguments. */
+int mcf_oracle_matmul(int f, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc,
+                      const void *B, int b_mc, const int64_t *rows, const int64_t *cols, int64_t count,
+                      void *out) {
+  if (nc < 1 || nc > MAXC || (!a_mc && !b_mc)) return -1;
+  mm_args g = {f, A, a_mc, B, b_mc, K, K, 1, N, 1, M * K, K * N};
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t t = 0; t < count; ++t) {
+    int64_t i = rows ? rows[t] : t / N;
+    int64_t j = rows ? cols[t] : t % N;
+    double r[MAXC];
+    mm_entry(&g, nc, i, j, r);
+    scatter(f, out, nc, count, t, r);
+  }
+  return 0;
+}
+
+/* MC-Linear forward (Section 2.3): the product of the MC weight and the plain input,
+ * Y[t][o] = sum over i of W[o][i] * X[t][i] in MM-MCN order, then Add-MCN with the
+ * MC bias[o] when bias is given.  X is plain [T][I], W is [nc][O][I], bias [nc][O].
+ * Evaluated at the positions (rows[t], cols[t]) = (token, output feature); out is
+ * [nc][count]. */
+int mcf_oracle_linear(int f, int nc, int64_t T, int64_t I, int64_t O, const void *X, const void *W,
+                      const void *bias, const int64_t *rows, const int64_t *cols, int64_t count, void *out) {
+  if (nc < 1 || nc > MAXC) return -1;
+  /* As a product A x B: A = X (plain), B[k=i][j=o] = W[o][i] (MC). */
+  mm_args g = {f, X, 0, W, 1, I, I, 1, 1, I, T * I, O * I};
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t t = 0; t < count; ++t) {
+    int64_t i = rows ? rows[t] : t / O;
+    int64_t j = rows ? cols[t] : t % O;
+    double r[MAXC];
+    mm_entry_plain(&g, nc, i, j, 0, r);
+    if (bias) {
+      double b[MAXC], s[MAXC];
+      for (int c = 0; c < nc; ++c) b[c] = load_c(f, bias, (int64_t)c * O + j);
+      add_mcn(f, r, b, nc, s);
+      for (int c = 0; c < nc; ++c) r[c] = s[c];
+    }
+    scatter(f, out, nc, count, t, r);
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------------ */
+/* Exact arithmetic checker                                                          */
+/* ------------------------------------------------------------------------------ */
+
+/* A long fixed-point accumulator: value = sum_d dig[d] * 2^(32*d - ACC_BIAS), digits
+ * held in int64 so that up to 2^31 signed additions need no intermediate carry.
+ * Every double is a multiple of 2^-1074 below 2^1024, so the window
+ * 2^-1184 .. 2^1120 holds any sum of doubles exactly. */
+#define ACC_DIG 72
+#define ACC_BIAS 1184
+
+typedef struct {
+  int64_t dig[ACC_DIG];
+} exact_acc;
+
+static void acc_clear(exact_acc *a) { memset(a->dig, 0, sizeof(a->dig)); }
+
+/* a += sign * v for a finite double v */
+static void acc_add(exact_acc *a, double v, int sign) {
+  if (v == 0.0) return;
+  if (v < 0) {
+    v = -v;
+    sign = -sign;
+  }
+  int e2;
+  double m = frexp(v, &e2);             /* v = m 2^e2, m in [0.5, 1) */
+  uint64_t mi = (uint64_t)ldexp(m, 53); /* v = mi 2^(e2-53) exactly */
+  int pos = e2 - 53 + ACC_BIAS;         /* bit position of mi's last bit, >= 58 */
+  int d = pos / 32, sh = pos % 32;
+  unsigned __int128 w = ((unsigned __int128)mi) << sh; /* at most 85 bits */
+  for (int q = 0; q < 3; ++q) {
+    int64_t part = (int64_t)(uint32_t)(w >> (32 * q));
+    a->dig[d + q] += sign > 0 ? part : -part;
+  }
+}
+
+/* The accumulated value rounded to double (relative error below 2^-52). */
+static double acc_value(const exact_acc *in) {
+  int64_t dig[ACC_DIG];
+  int64_t carry = 0;
+  for (int d = 0; d < ACC_DIG; ++d) { /* normalise to digits in [0, 2^32) plus a sign carry */
+    int64_t v = in->dig[d] + carry;
+    int64_t lo = v & 0xffffffffLL;
+    carry = (v - lo) / 4294967296LL;
+    dig[d] = lo;
+  }
+  int neg = carry < 0; /* carry is 0 or -1: the value is carry * 2^(32*ACC_DIG) + digits */
+  if (neg) {           /* magnitude = two's complement of the digit string */
+    int64_t c2 = 1;
+    for (int d = 0; d < ACC_DIG; ++d) {
+      int64_t v = (0xffffffffLL - dig[d]) + c2;
+      c2 = v >> 32;
+      dig[d] = v & 0xffffffffLL;
+    }
+  }
+  /* sum from the top: the first three non-zero digits carry 64+ significant bits */
+  double r = 0.0;
+  for (int d = ACC_DIG - 1; d >= 0; --d) r += ldexp((double)dig[d], 32 * d - ACC_BIAS);
+  return neg ? -r : r;
+}
+
+/* Exact error of a computed MC matrix product (plus an optional MC bias per column).
+ * For each requested output t = (rows[t], cols[t]):
+ *   err[t]   = (exact sum of the nc components of C_t) - (exact value of
+ *              sum_k A^_ik B^_kj + bias^_j), computed exactly and rounded to double,
+ *   absab[t] = sum_k |A^_ik| |B^_kj| + |bias^_j| (the bound's denominator; A^, B^ are
+ *              the exact values of the MC entries), rounded to double,
+ *   exact[t] = the exact product (plus bias) rounded to double.
+ * A is [a_planes][M][K], B is [b_planes][K][N] row-major, bias [bias_planes][N] or
+ * NULL, C is [nc][count]. */
+int mcf_oracle_matmul_exact_err(int f, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_planes,
+                                const void *B, int b_planes, const void *bias, int bias_planes,
+                                const int64_t *rows, const int64_t *cols, int64_t count, const void *C,
+                                double *err, double *absab, double *exact) {
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t t = 0; t < count; ++t) {
+    int64_t i = rows ? rows[t] : t / N;
+    int64_t j = rows ? cols[t] : t % N;
+    exact_acc diff, ex;
+    acc_clear(&diff);
+    acc_clear(&ex);
+    double sab = 0.0;
+    for (int64_t k = 0; k < K; ++k) {
+      exact_acc ea, eb;
+      acc_clear(&ea);
+      acc_clear(&eb);
+      for (int ca = 0; ca < a_planes; ++ca) {
+        double a = load_c(f, A, ca * M * K + i * K + k);
+        acc_add(&ea, a, 1);
+        for (int cb = 0; cb < b_planes; ++cb) {
+          double b = load_c(f, B, cb * K * N + k * N + j);
+          acc_add(&diff, a * b, -1); /* a*b is exact in double */
+          acc_add(&ex, a * b, 1);
+        }
+      }
+      for (int cb = 0; cb < b_planes; ++cb) acc_add(&eb, load_c(f, B, cb * K * N + k * N + j), 1);
+      sab += fabs(acc_value(&ea)) * fabs(acc_value(&eb));
+    }
+    if (bias) {
+      exact_acc eb;
+      acc_clear(&eb);
+      for (int cb = 0; cb < bias_planes; ++cb) {
+        double b = load_c(f, bias, cb * N + j);
+        acc_add(&eb, b, 1);
+        acc_add(&diff, b, -1);
+        acc_add(&ex, b, 1);
+      }
+      sab += fabs(acc_value(&eb));
+    }
+    for (int c = 0; c < nc; ++c) acc_add(&diff, load_c(f, C, (int64_t)c * count + t), 1);
+    err[t] = acc_value(&diff);
+    absab[t] = sab;
+    exact[t] = acc_value(&ex);
+  }
+  return 0;
+}
+
+/* diff[i] = (exact value of element i of x) - (exact value of element i of y),
+ * rounded to double; x has x_planes planes, y has y_planes (y may be NULL). */
+void mcf_oracle_exact_diff(int f, int64_t n, const void *x, int x_planes, const void *y, int y_planes,
+                           double *diff) {
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < n; ++i) {
+    exact_acc a;
+    acc_clear(&a);
+    for (int c = 0; c < x_planes; ++c) acc_add(&a, load_c(f, x, (int64_t)c * n + i), 1);
+    if (y)
+      for (int c = 0; c < y_planes; ++c) acc_add(&a, load_c(f, y, (int64_t)c * n + i), -1);
+    diff[i] = acc_value(&a);
+  }
+}

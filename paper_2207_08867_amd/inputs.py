@@ -1,0 +1,89 @@
+"""Seeded synthetic inputs for multi-component (MC) arithmetic.
+
+This module only draws random numbers and splits them into components; it holds
+none of the MC algorithms.  Both the CPU oracle's tests and the GPU path take their
+inputs from here.
+
+An MC value with nc components is built from a float64 draw x by successive
+rounding: c_0 = RN(x), c_1 = RN(x - c_0), c_2 = RN(x - c_0 - c_1), ... where RN
+rounds to the component format (numpy's float64 -> float16/float32 conversion is
+round-to-nearest-even with gradual underflow).  Each residual is exact in float64,
+so the components are non-overlapping and decreasing, as an MCTensor requires
+(Section 2, equation of the MCF expansion).
+
+Arrays are component-major ("planar"): shape (nc, *shape).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+
+def split(x: np.ndarray, nc: int, dtype) -> np.ndarray:
+    """Split float64 values into nc components of `dtype` by successive rounding."""
+    x = np.asarray(x, dtype=np.float64)
+    dtype = np.dtype(dtype)
+    out = np.empty((nc,) + x.shape, dtype=dtype)
+    r = x.copy()
+    with np.errstate(over="ignore"):
+        for c in range(nc):
+            out[c] = r.astype(dtype)
+            r -= out[c].astype(np.float64)
+    return out
+
+
+def rng(seed: int = 0) -> np.random.Generator:
+    return np.random.default_rng(seed)
+
+
+# ---------------------------------------------------------------------------------
+# workload recipes (sizes are parameters so tests can scale them down)
+# ---------------------------------------------------------------------------------
+
+def matmul_uniform(M, N, K, nc, dtype, seed=0, lo=-1.0, hi=1.0):
+    """A, B entries float64 ~ U[lo, hi], split into nc components (A drawn first)."""
+    g = rng(seed)
+    A = split(g.uniform(lo, hi, (M, K)), nc, dtype)
+    B = split(g.uniform(lo, hi, (K, N)), nc, dtype)
+    return A, B
+
+
+def matmul_normal(M, N, K, nc, dtype, seed=0):
+    """A, B entries float64 ~ N(0, 1/K), split into nc components (A drawn first)."""
+    g = rng(seed)
+    s = 1.0 / np.sqrt(K)
+    A = split(g.normal(0.0, s, (M, K)), nc, dtype)
+    B = split(g.normal(0.0, s, (K, N)), nc, dtype)
+    return A, B
+
+
+def elementwise_inputs(op: str, n: int, nc: int, dtype, seed=0):
+    """Operands for the elementwise workload on n elements.
+
+    add: x, y ~ U[-1/2, 1/2];  mul, div: x ~ U[-1/2, 1/2], y ~ U[1/2, 3/2] (y is
+    a divisor inside Mult-MCN and Div-MCN);  exp: x ~ U[-4, 4];  renorm: x ~
+    U[-1/2, 1/2].  Returns (x, y) with y None for unary ops.
+    """
+    g = rng(seed)
+    if op == "exp":
+        return split(g.uniform(-4.0, 4.0, n), nc, dtype), None
+    if op == "renorm":
+        return split(g.uniform(-0.5, 0.5, n), nc, dtype), None
+    x = split(g.uniform(-0.5, 0.5, n), nc, dtype)
+    if op in ("mul", "div"):
+        y = split(g.uniform(0.5, 1.5, n), nc, dtype)
+    else:
+        y = split(g.uniform(-0.5, 0.5, n), nc, dtype)
+    return x, y
+
+
+def linear_inputs(T, I, O, nc, dtype, layers=1, seed=0):
+    """MC-Linear workload: x ~ N(0,1) rounded once (plain), then for each layer
+    W ~ U(-1/sqrt(I), 1/sqrt(I)) of shape (O, I) and b ~ same of shape (O,), split
+    into nc components.  Yields (x, W, b) per layer; x is shared."""
+    g = rng(seed)
+    x = g.normal(0.0, 1.0, (T, I)).astype(dtype)
+    lim = 1.0 / np.sqrt(I)
+    for _ in range(layers):
+        W = split(g.uniform(-lim, lim, (O, I)), nc, dtype)
+        b = split(g.uniform(-lim, lim, (O,)), nc, dtype)
+        yield x, W, b
