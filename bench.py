@@ -1,0 +1,269 @@
+#!/usr/bin/env python3
+"""Throughput of the multi-component (MC) matrix product on one MI355X.
+
+Headline workload: C = A B with binary32 components, nc = 3, M = N = K = 8192,
+A and B drawn float64 ~ N(0, 1/K) (seed 0) and split into 3 components by
+successive rounding, both operands MC.  One step is one full product; the metric is
+MC-GFLOP/s = 2 M N K / time (one MC multiply-add counts as 2 flops), inputs resident
+in HBM before the timed region.
+
+Also reported on the same line (not part of `value`):
+  * roofline of the product kernel: algorithmic VALU operations per launch over the
+    launch duration measured with HIP events, against the VALU issue peak;
+  * the maximum error against the exact product on sampled outputs;
+  * the other workloads (64^3 binary32 nc=2; 1024^3 binary16 nc=2 and 3; the
+    4096x1024x1024 binary16 nc=3 MC-Linear over 100 layers; the 2^26-element binary16
+    nc=3 elementwise operations with their HBM bandwidth);
+  * cpu_baseline: the CPU oracle timed on a sample of the headline workload.
+
+Usage: python bench.py [--gpus 1] [--steps 3] [--warmup 1] [--no-extra]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+VALU_PEAK = 256 * 4 * 16 * 2.4e9  # lane-operations / s: 256 CUs x 4 SIMD16 x 2.4 GHz
+VALU_PEAK_PACKED16 = 2 * VALU_PEAK  # two binary16 lanes per packed instruction
+HBM_PEAK = 8.0e12  # bytes / s
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def algo_ops_per_mac(nc: int, mc_x_mc: bool) -> int:
+    """VALU arithmetic operations the algorithm needs per multiply-add: ScalingN is
+    mul + fma on component 0 and mul + fma + Two-Sum (6) + carry add on the others;
+    Add-MCN is Two-Sum on component 0 and two Two-Sums + carry add on the others (the
+    first Two-Sum with the zero carry is an identity and is not counted).  MC x MC
+    repeats this for each of the nc components of B.  Simple-Renorm selects are not
+    counted."""
+    per = (2 + 9 * (nc - 1)) + (6 + 13 * (nc - 1))
+    return per * (nc if mc_x_mc else 1)
+
+
+class Timer:
+    """HIP events on torch's current stream, the stream the library launches on."""
+
+    def __init__(self, torch):
+        self.torch = torch
+        self.pairs = []
+
+    def run(self, fn):
+        s = self.torch.cuda.Event(enable_timing=True)
+        e = self.torch.cuda.Event(enable_timing=True)
+        s.record()
+        fn()
+        e.record()
+        self.pairs.append((s, e))
+
+    def ms(self):
+        self.torch.cuda.synchronize()
+        return [s.elapsed_time(e) for s, e in self.pairs]
+
+
+def bench_matmul(torch, mcf, A, B, nc, steps, warmup, a_mc=True, b_mc=True):
+    tA = torch.from_numpy(A).cuda()
+    tB = torch.from_numpy(B).cuda()
+    M, K = A.shape[1:]
+    N = B.shape[2]
+    C = torch.empty((nc, M, N), dtype=tA.dtype, device="cuda")
+    for _ in range(warmup):
+        mcf.mc_matmul(tA, tB, nc=nc, a_mc=a_mc, b_mc=b_mc, out=C)
+    torch.cuda.synchronize()
+    tm = Timer(torch)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        tm.run(lambda: mcf.mc_matmul(tA, tB, nc=nc, a_mc=a_mc, b_mc=b_mc, out=C))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    return C, wall / steps * 1e3, float(np.mean(tm.ms()))
+
+
+def exact_error(oracle, A, B, C, nc, K, dt, count=64, seed=5):
+    M, N = C.shape[1:]
+    g = np.random.default_rng(seed)
+    rows = g.integers(0, M, count)
+    cols = g.integers(0, N, count)
+    Cs = np.ascontiguousarray(C[:, rows, cols])
+    err, absab, _ = oracle.matmul_exact_err(A, B, Cs, rows=rows, cols=cols)
+    rel = np.abs(err) / absab
+    u = 2.0 ** -24 if dt == np.float32 else 2.0 ** -11
+    floor = A.shape[0] * B.shape[0] * K * 2.0 ** -25 if dt == np.float16 else 0.0
+    lim = 4 * K * u ** min(nc, 3) * absab + floor
+    return {"max_rel_err": float(rel.max()), "bound_4Ku^nc": 4 * K * u ** nc,
+            "max_err_over_bound": float(np.max(np.abs(err) / lim)), "sampled_outputs": int(count)}
+
+
+def cpu_baseline(oracle, A, B, nc, target_s=12.0):
+    """The oracle on a bounded sample of output entries of the headline product."""
+    M, K = A.shape[1:]
+    N = B.shape[2]
+    g = np.random.default_rng(9)
+    probe = 16
+    t0 = time.perf_counter()
+    oracle.matmul(A, B, nc=nc, rows=g.integers(0, M, probe), cols=g.integers(0, N, probe))
+    dt = time.perf_counter() - t0
+    count = int(max(probe, min(4096, probe * target_s / max(dt, 1e-3))))
+    threads = oracle.threads()
+    count = max(threads, (count // threads) * threads)
+    rows = g.integers(0, M, count)
+    cols = g.integers(0, N, count)
+    t0 = time.perf_counter()
+    oracle.matmul(A, B, nc=nc, rows=rows, cols=cols)
+    dt = time.perf_counter() - t0
+    return {"value": 2.0 * K * count / dt / 1e9, "unit": "MC-GFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": f"{count} sampled outputs of the 8192^3 product (each a full K = {K} reduction), "
+                      f"{dt:.1f} s", "seconds": dt}
+
+
+def bench_elementwise(torch, mcf, inputs, steps=10):
+    n, nc, dt = 1 << 26, 3, np.float16
+    s = inputs.elementwise_suite(n, nc, dt, seed=0)
+    dev = {k: torch.from_numpy(v).cuda() for k, v in s.items()}
+    out = torch.empty((nc, n), dtype=torch.float16, device="cuda")
+    ops = {
+        "add_mcn": (lambda: mcf.mc_add(dev["a"], dev["b"], nc=nc, out=out), 18),
+        "grow_expn": (lambda: mcf.mc_add(dev["a"], dev["b"][0], nc=nc, y_mc=False, out=out), 14),
+        "scaling_n": (lambda: mcf.mc_mul(dev["a"], dev["d"][0], nc=nc, y_mc=False, out=out), 14),
+        "mult_mcn": (lambda: mcf.mc_mul(dev["a"], dev["d"], nc=nc, out=out), 18),
+        "div_mcn": (lambda: mcf.mc_div(dev["a"], dev["d"], nc=nc, out=out), 18),
+        "exp_mcn": (lambda: mcf.mc_exp(dev["e"], nc=nc, out=out), 12),
+        "renormalize": (lambda: mcf.mc_renorm(dev["a"], mode=0, out=out), 12),
+    }
+    res = {}
+    for name, (fn, bpe) in ops.items():
+        for _ in range(2):
+            fn()
+        tm = Timer(torch)
+        for _ in range(steps):
+            tm.run(fn)
+        ms = float(np.median(tm.ms()))
+        gbs = bpe * n / (ms * 1e-3) / 1e9
+        res[name] = {"us": round(ms * 1e3, 1), "GB/s": round(gbs, 1), "hbm_frac": round(gbs * 1e9 / HBM_PEAK, 3),
+                     "Gelem/s": round(n / (ms * 1e-3) / 1e9, 2)}
+        log(f"  elementwise {name}: {ms * 1e3:.1f} us, {gbs:.0f} GB/s")
+    return {"workload": "2^26 elements, binary16, nc = 3", "ops": res}
+
+
+def bench_linear(torch, mcf, inputs, layers=100):
+    T, I, O, nc = 4096, 1024, 1024, 3
+    gen = inputs.linear_inputs(T, I, O, nc, np.float16, layers=layers, seed=0)
+    x = None
+    Ws, bs = [], []
+    for xx, W, b in gen:
+        x = xx
+        Ws.append(torch.from_numpy(W).cuda())
+        bs.append(torch.from_numpy(b).cuda())
+    tx = torch.from_numpy(x).cuda()
+    y = torch.empty((nc, T, O), dtype=torch.float16, device="cuda")
+    mcf.mc_linear_fwd(tx, Ws[0], bs[0], out=y)
+    torch.cuda.synchronize()
+    tm = Timer(torch)
+    t0 = time.perf_counter()
+    for W, b in zip(Ws, bs):
+        tm.run(lambda: mcf.mc_linear_fwd(tx, W, b, out=y))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kms = float(np.mean(tm.ms()))
+    macs = T * I * O
+    return {"workload": f"MC-Linear {T}x{I}x{O} binary16 nc=3, {layers} layers", "ms_per_layer": round(kms, 3),
+            "MC-GFLOP/s": round(2 * macs * layers / wall / 1e9, 1),
+            "valu_frac": round(algo_ops_per_mac(nc, False) * macs / (kms * 1e-3) / VALU_PEAK, 3)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--no-extra", action="store_true", help="only the headline workload")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py: this build runs on one GPU only; the MC product shards by output blocks "
+              "with no communication, so there is no multi-GPU path to measure", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import oracle
+    import paper_2207_08867_amd as mcf
+    from paper_2207_08867_amd import inputs
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    mcf.lib()
+
+    M = N = K = 8192
+    nc = 3
+    log("generating 8192^3 binary32 nc=3 operands")
+    A, B = inputs.matmul_normal(M, N, K, nc, np.float32, seed=0)
+    log("headline product")
+    C, ms_step, kms = bench_matmul(torch, mcf, A, B, nc, args.steps, args.warmup)
+    value = 2.0 * M * N * K / (ms_step * 1e-3) / 1e9
+    ops = algo_ops_per_mac(nc, True) * M * N * K
+    achieved = ops / (kms * 1e-3) / 1e12
+    log(f"  {ms_step:.1f} ms/step, kernel {kms:.1f} ms, {value:.1f} MC-GFLOP/s, {achieved:.2f} TOP/s")
+    Ch = C.cpu().numpy()
+    del C
+    err = exact_error(oracle, A, B, Ch, nc, K, np.float32)
+    log(f"  max rel err vs exact {err['max_rel_err']:.3g} (bound {err['bound_4Ku^nc']:.3g})")
+
+    line = {
+        "metric": "MC-matmul MC-GFLOP/s (binary32, nc=3, MC x MC)",
+        "value": round(value, 2),
+        "unit": "MC-GFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "MC matmul C = A B, M = N = K = 8192, binary32 components, nc = 3, A and B MC, "
+                               "entries float64 ~ N(0, 1/K) seed 0 split by successive rounding",
+                   "M": M, "N": N, "K": K, "nc": nc, "component": "binary32"},
+        "roofline": {"bound": "alu", "achieved": round(achieved, 3), "peak": round(VALU_PEAK / 1e12, 2),
+                     "unit": "TOP/s", "frac": round(achieved * 1e12 / VALU_PEAK, 4), "traffic": None,
+                     "kernel": "mm_kernel (MC x MC, binary32, nc = 3)", "kernel_ms": round(kms, 3),
+                     "ops_per_mac": algo_ops_per_mac(nc, True)},
+        "error": err,
+    }
+    if not args.no_extra:
+        extra = {}
+        A1, B1 = inputs.matmul_uniform(64, 64, 64, 2, np.float32, seed=0)
+        C1, ms1, k1 = bench_matmul(torch, mcf, A1, B1, 2, 20, 3)
+        extra["matmul_64_f32_nc2"] = {"us": round(k1 * 1e3, 1),
+                                      "error": exact_error(oracle, A1, B1, C1.cpu().numpy(), 2, 64, np.float32,
+                                                           count=4096)}
+        for nc3 in (2, 3):
+            A3, B3 = inputs.matmul_normal(1024, 1024, 1024, nc3, np.float16, seed=0)
+            C3, ms3, k3 = bench_matmul(torch, mcf, A3, B3, nc3, 5, 2)
+            macs = 1024 ** 3
+            extra[f"matmul_1024_f16_nc{nc3}"] = {
+                "ms": round(k3, 3), "MC-GFLOP/s": round(2 * macs / (k3 * 1e-3) / 1e9, 1),
+                "valu_frac_unpacked": round(algo_ops_per_mac(nc3, True) * macs / (k3 * 1e-3) / VALU_PEAK, 3),
+                "error": exact_error(oracle, A3, B3, C3.cpu().numpy(), nc3, 1024, np.float16)}
+            log(f"  1024^3 f16 nc={nc3}: {k3:.2f} ms")
+        log("MC-Linear")
+        extra["linear_4096x1024x1024_f16_nc3"] = bench_linear(torch, mcf, inputs)
+        log("elementwise")
+        extra["elementwise"] = bench_elementwise(torch, mcf, inputs)
+        line["extra"] = extra
+    if not args.no_cpu:
+        log("cpu baseline (oracle)")
+        line["cpu_baseline"] = cpu_baseline(oracle, A, B, nc)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

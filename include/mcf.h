@@ -1,0 +1,132 @@
+/*
+ * mcf.h -- C ABI of the MI355X (gfx950) multi-component floating-point library.
+ *
+ * Arithmetic follows "MCTensor: A High-Precision Deep Learning Library with
+ * Multi-Component Floating-Point" (arXiv 2207.08867).  A multi-component (MC) value
+ * is an unevaluated sum x = x_0 + x_1 + ... + x_{nc-1} of nc floating-point
+ * components of one format, largest first (Section 2, the MCF expansion equation).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Memory.  All tensor pointers are DEVICE pointers owned by the caller; the library
+ *   allocates nothing per call and keeps no state besides a per-device binary16
+ *   exponential table (128 KiB, built on the first mc_exp call on a device).
+ * Layout.  Dense, component-major ("planar"): component c of element i of an MC
+ *   array of n elements is at element offset c*n + i.  A plain tensor is one plane.
+ *   Matrices are row-major inside each plane.  The paper's interleaved layout
+ *   (components in the last dimension) converts with a transpose on the caller side.
+ * Formats.  MCF_F16 = IEEE binary16 components, MCF_F32 = IEEE binary32.  Every step
+ *   of every algorithm is one IEEE round-to-nearest-even operation in the component
+ *   format with gradual underflow; FMA appears only where the algorithm names it
+ *   (Two-Prod); component division is correctly rounded; the binary16 component
+ *   exponential is correctly rounded.
+ * Operand kinds.  Binary operations take an MC value and a plain tensor in either
+ *   order, or two MC values (Section 2.1).  The flags x_mc / y_mc / a_mc / b_mc are 1
+ *   for an MC operand of nc planes and 0 for a plain tensor of one plane; at least
+ *   one operand must be MC.  Results always have nc components.
+ * nc.  1 <= nc <= 4.
+ * Streams.  Work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and
+ *   runs asynchronously; nothing synchronises.  Calls on different streams are
+ *   independent.  The library is reentrant.
+ * Aliasing.  Elementwise calls allow `out` to be exactly `x` or `y` (in place);
+ *   any other overlap of out with an input is rejected (MCF_E_ALIAS).  Matrix calls
+ *   reject any overlap of the output with an input.
+ * Degenerate sizes.  n = 0 (or M*N = 0) returns MCF_OK without launching; a
+ *   reduction length of 0 gives +0 in every output component.
+ * Errors.  Every call returns MCF_OK (0) or a negative mcf_status; on error nothing
+ *   is launched.  Launch failures are reported as MCF_E_HIP.  Input values are not
+ *   inspected: non-finite components propagate by IEEE rules.
+ */
+#ifndef MCF_H
+#define MCF_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { MCF_F16 = 0, MCF_F32 = 1 } mcf_dtype;
+
+typedef enum {
+  MCF_OK = 0,
+  MCF_E_NULL = -1,  /* a required pointer is NULL */
+  MCF_E_NC = -2,    /* nc (or nc_out) out of range */
+  MCF_E_SHAPE = -3, /* negative size, or a size the kernels cannot index */
+  MCF_E_DTYPE = -4, /* unknown format, or an operation not provided for it */
+  MCF_E_ALIAS = -5, /* output overlaps an input in a way that is not allowed */
+  MCF_E_HIP = -6,   /* the HIP runtime reported an error */
+  MCF_E_ARG = -7    /* any other invalid argument (operand kinds, mode) */
+} mcf_status;
+
+/* Addition (Section 2.1; Appendix A.2.1).
+ *   (MC, MC): Add-MCN -- per component, Two-Sum of the operands, Two-Sum with the
+ *             carry, carry = fl(e1 + e2); the nc+1 terms pass through Simple-Renorm.
+ *   (MC, T), (T, MC): Grow-ExpN -- a chain of Two-Sums from the last component up,
+ *             then Simple-Renorm to nc components.
+ * x, y: [nc or 1][n]; out: [nc][n]. */
+int mc_add(int dtype, int nc, int64_t n, const void *x, int x_mc, const void *y, int y_mc, void *out,
+           void *stream);
+
+/* Multiplication (Section 2.1; Appendix A.2.1).
+ *   (MC, T), (T, MC): ScalingN without expand -- per component Two-Prod (FMA
+ *             variant), Two-Sum with the carry, carry = fl(e1 + e2); Simple-Renorm.
+ *   (MC, MC): Mult-MCN, fast version -- Renormalize(Div-MCN(x, Renormalize(
+ *             Div-MCN((1, 0, ..., 0), y)))).
+ * x, y: [nc or 1][n]; out: [nc][n]. */
+int mc_mul(int dtype, int nc, int64_t n, const void *x, int x_mc, const void *y, int y_mc, void *out,
+           void *stream);
+
+/* Division (Appendix A.2.1).
+ *   (MC, MC): Div-MCN -- long division: q = fl(x_0 / y_0), then nc times
+ *             x = Add-MCN(x, -ScalingN(y, q)), q = fl(x_0 / y_0); the nc+1 quotient
+ *             digits pass through Simple-Renorm.
+ *   (T, MC):  DivN -- the dividend is padded with zero components.
+ *   (MC, T):  Div-MCN with the divisor padded with zero components.
+ * x, y: [nc or 1][n]; out: [nc][n]. */
+int mc_div(int dtype, int nc, int64_t n, const void *x, int x_mc, const void *y, int y_mc, void *out,
+           void *stream);
+
+/* Exponential, Exp-MCN (Appendix A.2.1): h = exp(x_0) (one component), then for
+ * i = 1 .. nc-1, h = ScalingN(h, exp(x_i), expand) growing h by one component per
+ * step.  The component exponential is correctly rounded.  Provided for MCF_F16
+ * (MCF_F32 returns MCF_E_DTYPE).  x, out: [nc][n]. */
+int mc_exp(int dtype, int nc, int64_t n, const void *x, void *out, void *stream);
+
+/* Renormalization (Appendix A.2.1).
+ *   mode 0: Renormalize (Priest variant): a top-down Two-Sum sweep s = x_0 (+) x_1 ...
+ *           collecting the errors t_i, then a second sweep s, e = Two-Sum(s, t_i)
+ *           that emits s whenever e != 0; the final s is emitted too; the first
+ *           nc_out emitted values are returned, +0 padded.
+ *   mode 1: Simple-Renorm: the first nc_out non-zero components in order, +0 padded.
+ * 1 <= nc_out <= nc_in <= 4.  x: [nc_in][n]; out: [nc_out][n] (out == x allowed
+ * only when nc_out == nc_in). */
+int mc_renorm(int dtype, int nc_in, int nc_out, int64_t n, const void *x, void *out, int mode, void *stream);
+
+/* Matrix product C = A B (Appendix A.2.2, MM-MCN; MV-MCN is N = 1 and Dot-MCN is
+ * M = N = 1).  Each output is accumulated in MM-MCN order: acc = ScalingN(A_i0,
+ * B_0j), then acc = Add-MCN(acc, ScalingN(A_ik, B_kj)) for k = 1 .. K-1, so the
+ * result is reproducible and independent of the launch geometry.  With both
+ * operands MC (not defined by the paper, whose matrix operators multiply an MC
+ * matrix by a plain one) the product is taken by linearity over the components of
+ * B: C = MM(A, B^(0)) (+) MM(A, B^(1)) (+) ... with (+) = Add-MCN.
+ * A: [nc or 1][M][K], B: [nc or 1][K][N], C: [nc][M][N]. */
+int mc_matmul(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B,
+              int b_mc, void *C, void *stream);
+
+/* MC-Linear forward (Section 2.3): y = x W^T (+ b).  The weight and bias are MC,
+ * the input is a plain tensor; each output accumulates ScalingN(W[o][i], x[t][i])
+ * over i in MM-MCN order, then adds the bias with Add-MCN.
+ * x: [batch][in] (plain), W: [nc][out][in], b: [nc][out] or NULL,
+ * y: [nc][batch][out]. */
+int mc_linear_fwd(int dtype, int nc, int64_t batch, int64_t in, int64_t out, const void *x, const void *W,
+                  const void *b, void *y, void *stream);
+
+/* Human-readable name of a status code (static storage). */
+const char *mc_status_str(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MCF_H */

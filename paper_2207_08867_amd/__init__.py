@@ -1,0 +1,221 @@
+"""MI355X (gfx950) multi-component floating-point (MCF) arithmetic.
+
+Python binding of the C ABI in include/mcf.h (libmcf.so, built in-tree by
+``paper_2207_08867_amd.build``).  This module only marshals arguments: it checks
+shapes, dtypes and devices of torch tensors, passes their device pointers and the
+current HIP stream, and turns status codes into exceptions.  Every arithmetic step
+runs in the library's HIP kernels; there is no fallback.
+
+Tensor conventions (component-major):
+  * an MC tensor with nc components and logical shape S is a torch tensor of shape
+    (nc, *S); a plain tensor has shape S or (1, *S);
+  * component dtype torch.float16 or torch.float32; all tensors contiguous and on
+    the same GPU.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+__all__ = [
+    "mc_add", "mc_mul", "mc_div", "mc_exp", "mc_renorm", "mc_matmul", "mc_linear_fwd", "mc_status_str",
+    "lib", "LIB_PATH", "MCFError",
+]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmcf.so")
+_lib = None
+
+MCF_F16, MCF_F32 = 0, 1
+
+
+class MCFError(RuntimeError):
+    pass
+
+
+def lib() -> ctypes.CDLL:
+    """Load libmcf.so; raises if it has not been built (there is no fallback)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise MCFError(f"{LIB_PATH} is missing: build it with `python -m paper_2207_08867_amd.build` "
+                           "(or __graft_entry__.build())")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i64, ci = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
+        for name in ("mc_add", "mc_mul", "mc_div"):
+            f = getattr(L, name)
+            f.restype = ci
+            f.argtypes = [ci, ci, i64, vp, ci, vp, ci, vp, vp]
+        L.mc_exp.restype = ci
+        L.mc_exp.argtypes = [ci, ci, i64, vp, vp, vp]
+        L.mc_renorm.restype = ci
+        L.mc_renorm.argtypes = [ci, ci, ci, i64, vp, vp, ci, vp]
+        L.mc_matmul.restype = ci
+        L.mc_matmul.argtypes = [ci, ci, i64, i64, i64, vp, ci, vp, ci, vp, vp]
+        L.mc_linear_fwd.restype = ci
+        L.mc_linear_fwd.argtypes = [ci, ci, i64, i64, i64, vp, vp, vp, vp, vp]
+        L.mc_status_str.restype = ctypes.c_char_p
+        L.mc_status_str.argtypes = [ci]
+        _lib = L
+    return _lib
+
+
+def mc_status_str(status: int) -> str:
+    return lib().mc_status_str(int(status)).decode()
+
+
+def _check(status: int, what: str):
+    if status != 0:
+        msg = f"{what}: {mc_status_str(status)}"
+        if status in (-1, -2, -3, -4, -5, -7):
+            raise ValueError(msg)
+        raise MCFError(msg)
+
+
+def _torch():
+    import torch
+
+    return torch
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    if t.dtype == torch.float16:
+        return MCF_F16
+    if t.dtype == torch.float32:
+        return MCF_F32
+    raise TypeError(f"component dtype must be float16 or float32, got {t.dtype}")
+
+
+def _dev(t, name):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(t) -> ctypes.c_void_p:
+    torch = _torch()
+    return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+
+
+def _logical_shape(t, nc, is_mc, name):
+    if is_mc:
+        if t.dim() < 1 or t.shape[0] != nc:
+            raise ValueError(f"{name}: MC operand must have shape (nc={nc}, ...), got {tuple(t.shape)}")
+        return tuple(t.shape[1:])
+    return tuple(t.shape)
+
+
+def _binary(fn_name, x, y, nc, x_mc, y_mc, out):
+    torch = _torch()
+    if x.dtype != y.dtype or x.device != y.device:
+        raise ValueError("operands must share dtype and device")
+    sx = _logical_shape(x, nc, x_mc, "x")
+    sy = _logical_shape(y, nc, y_mc, "y")
+    # a plain operand given as (1, *S) is accepted as S
+    if not x_mc and len(sx) == len(sy) + 1 and sx[0] == 1:
+        sx = sx[1:]
+    if not y_mc and len(sy) == len(sx) + 1 and sy[0] == 1:
+        sy = sy[1:]
+    if sx != sy:
+        raise ValueError(f"shape mismatch: {sx} vs {sy}")
+    n = 1
+    for d in sx:
+        n *= d
+    if out is None:
+        out = torch.empty((nc,) + sx, dtype=x.dtype, device=x.device)
+    elif out.shape != (nc,) + sx or out.dtype != x.dtype:
+        raise ValueError("out has the wrong shape or dtype")
+    st = getattr(lib(), fn_name)(_dtype_code(x), nc, n, _dev(x, "x"), int(bool(x_mc)), _dev(y, "y"),
+                                 int(bool(y_mc)), _dev(out, "out"), _stream(x))
+    _check(st, fn_name)
+    return out
+
+
+def mc_add(x, y, *, nc: int, x_mc: bool = True, y_mc: bool = True, out=None):
+    """Add-MCN for (MC, MC); Grow-ExpN for (MC, T) and (T, MC)."""
+    return _binary("mc_add", x, y, nc, x_mc, y_mc, out)
+
+
+def mc_mul(x, y, *, nc: int, x_mc: bool = True, y_mc: bool = True, out=None):
+    """Mult-MCN (fast) for (MC, MC); ScalingN for (MC, T) and (T, MC)."""
+    return _binary("mc_mul", x, y, nc, x_mc, y_mc, out)
+
+
+def mc_div(x, y, *, nc: int, x_mc: bool = True, y_mc: bool = True, out=None):
+    """Div-MCN for (MC, MC); DivN for (T, MC); zero-padded divisor for (MC, T)."""
+    return _binary("mc_div", x, y, nc, x_mc, y_mc, out)
+
+
+def mc_exp(x, *, nc: int, out=None):
+    """Exp-MCN (binary16 components)."""
+    torch = _torch()
+    s = _logical_shape(x, nc, True, "x")
+    n = x.numel() // nc
+    if out is None:
+        out = torch.empty_like(x)
+    elif out.shape != x.shape or out.dtype != x.dtype:
+        raise ValueError("out has the wrong shape or dtype")
+    del s
+    _check(lib().mc_exp(_dtype_code(x), nc, n, _dev(x, "x"), _dev(out, "out"), _stream(x)), "mc_exp")
+    return out
+
+
+def mc_renorm(x, *, nc_out: int | None = None, mode: int = 0, out=None):
+    """mode 0: Renormalize; mode 1: Simple-Renorm.  x: (nc_in, ...)."""
+    torch = _torch()
+    nc_in = x.shape[0]
+    nc_out = nc_in if nc_out is None else nc_out
+    n = x.numel() // nc_in if nc_in else 0
+    if out is None:
+        out = torch.empty((nc_out,) + tuple(x.shape[1:]), dtype=x.dtype, device=x.device)
+    elif out.shape != (nc_out,) + tuple(x.shape[1:]) or out.dtype != x.dtype:
+        raise ValueError("out has the wrong shape or dtype")
+    st = lib().mc_renorm(_dtype_code(x), nc_in, nc_out, n, _dev(x, "x"), _dev(out, "out"), int(mode), _stream(x))
+    _check(st, "mc_renorm")
+    return out
+
+
+def mc_matmul(A, B, *, nc: int, a_mc: bool = True, b_mc: bool = True, out=None):
+    """C = A B in MM-MCN order.  A: (nc|1, M, K), B: (nc|1, K, N) -> (nc, M, N)."""
+    torch = _torch()
+    if A.dtype != B.dtype or A.device != B.device:
+        raise ValueError("operands must share dtype and device")
+    A3 = A if A.dim() == 3 else A.reshape((1,) + tuple(A.shape))
+    B3 = B if B.dim() == 3 else B.reshape((1,) + tuple(B.shape))
+    if A3.shape[0] != (nc if a_mc else 1) or B3.shape[0] != (nc if b_mc else 1):
+        raise ValueError("operand plane count does not match nc / kind")
+    M, K = A3.shape[1:]
+    K2, N = B3.shape[1:]
+    if K != K2:
+        raise ValueError(f"inner dimensions differ: {K} vs {K2}")
+    if out is None:
+        out = torch.empty((nc, M, N), dtype=A.dtype, device=A.device)
+    elif out.shape != (nc, M, N) or out.dtype != A.dtype:
+        raise ValueError("out has the wrong shape or dtype")
+    st = lib().mc_matmul(_dtype_code(A), nc, M, N, K, _dev(A3, "A"), int(bool(a_mc)), _dev(B3, "B"),
+                         int(bool(b_mc)), _dev(out, "out"), _stream(A))
+    _check(st, "mc_matmul")
+    return out
+
+
+def mc_linear_fwd(x, W, b=None, *, out=None):
+    """MC-Linear forward y = x W^T + b.  x: (batch, in) plain, W: (nc, out, in),
+    b: (nc, out) or None -> y: (nc, batch, out)."""
+    torch = _torch()
+    nc, O, I = W.shape
+    if x.dim() != 2 or x.shape[1] != I:
+        raise ValueError("x must be (batch, in)")
+    if x.dtype != W.dtype or (b is not None and (b.dtype != W.dtype or tuple(b.shape) != (nc, O))):
+        raise ValueError("dtype or bias shape mismatch")
+    T = x.shape[0]
+    if out is None:
+        out = torch.empty((nc, T, O), dtype=W.dtype, device=W.device)
+    elif out.shape != (nc, T, O) or out.dtype != W.dtype:
+        raise ValueError("out has the wrong shape or dtype")
+    bp = _dev(b, "b") if b is not None else None
+    st = lib().mc_linear_fwd(_dtype_code(W), nc, T, I, O, _dev(x, "x"), _dev(W, "W"), bp, _dev(out, "out"),
+                             _stream(W))
+    _check(st, "mc_linear_fwd")
+    return out

@@ -1,0 +1,142 @@
+// abi.cpp -- the extern "C" entry points declared in include/mcf.h: argument
+// validation, aliasing rules and dispatch to the kernel launchers.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/mcf.h"
+#include "mcf_internal.hpp"
+
+namespace {
+
+constexpr int MAX_NC = 4;
+
+int64_t elem_size(int dtype) { return dtype == MCF_F16 ? 2 : 4; }
+
+bool overlap(const void *a, int64_t abytes, const void *b, int64_t bbytes) {
+  if (abytes <= 0 || bbytes <= 0) return false;
+  uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+  return a0 < b0 + (uintptr_t)bbytes && b0 < a0 + (uintptr_t)abytes;
+}
+
+// out may coincide with an input exactly; any other overlap is an error.
+bool bad_alias(const void *out, int64_t obytes, const void *in, int64_t ibytes) {
+  if (in == nullptr) return false;
+  if (out == in && obytes == ibytes) return false;
+  return overlap(out, obytes, in, ibytes);
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? MCF_OK : MCF_E_HIP; }
+
+int check_common(int dtype, int nc, int64_t n) {
+  if (dtype != MCF_F16 && dtype != MCF_F32) return MCF_E_DTYPE;
+  if (nc < 1 || nc > MAX_NC) return MCF_E_NC;
+  if (n < 0) return MCF_E_SHAPE;
+  // plane offsets c * n stay far below 2^62 elements
+  if (n > ((int64_t)1 << 40)) return MCF_E_SHAPE;
+  return MCF_OK;
+}
+
+int binary_op(int op, int dtype, int nc, int64_t n, const void *x, int x_mc, const void *y, int y_mc, void *out,
+              void *stream) {
+  int st = check_common(dtype, nc, n);
+  if (st != MCF_OK) return st;
+  if ((x_mc != 0 && x_mc != 1) || (y_mc != 0 && y_mc != 1) || (!x_mc && !y_mc)) return MCF_E_ARG;
+  if (n == 0) return MCF_OK;
+  if (!x || !y || !out) return MCF_E_NULL;
+  const int64_t es = elem_size(dtype);
+  const int64_t ob = nc * n * es, xb = (x_mc ? nc : 1) * n * es, yb = (y_mc ? nc : 1) * n * es;
+  if (bad_alias(out, ob, x, xb) || bad_alias(out, ob, y, yb)) return MCF_E_ALIAS;
+  return hip_status(mcf::launch_elementwise(dtype, op, nc, nc, n, x, x_mc, y, y_mc, out, (hipStream_t)stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+int mc_add(int dtype, int nc, int64_t n, const void *x, int x_mc, const void *y, int y_mc, void *out,
+           void *stream) {
+  return binary_op(mcf::EW_ADD, dtype, nc, n, x, x_mc, y, y_mc, out, stream);
+}
+
+int mc_mul(int dtype, int nc, int64_t n, const void *x, int x_mc, const void *y, int y_mc, void *out,
+           void *stream) {
+  return binary_op(mcf::EW_MUL, dtype, nc, n, x, x_mc, y, y_mc, out, stream);
+}
+
+int mc_div(int dtype, int nc, int64_t n, const void *x, int x_mc, const void *y, int y_mc, void *out,
+           void *stream) {
+  return binary_op(mcf::EW_DIV, dtype, nc, n, x, x_mc, y, y_mc, out, stream);
+}
+
+int mc_exp(int dtype, int nc, int64_t n, const void *x, void *out, void *stream) {
+  int st = check_common(dtype, nc, n);
+  if (st != MCF_OK) return st;
+  if (dtype != MCF_F16) return MCF_E_DTYPE;
+  if (n == 0) return MCF_OK;
+  if (!x || !out) return MCF_E_NULL;
+  const int64_t b = nc * n * elem_size(dtype);
+  if (bad_alias(out, b, x, b)) return MCF_E_ALIAS;
+  return hip_status(mcf::launch_exp_f16(nc, n, x, out, (hipStream_t)stream));
+}
+
+int mc_renorm(int dtype, int nc_in, int nc_out, int64_t n, const void *x, void *out, int mode, void *stream) {
+  int st = check_common(dtype, nc_in, n);
+  if (st != MCF_OK) return st;
+  if (nc_out < 1 || nc_out > nc_in) return MCF_E_NC;
+  if (mode != 0 && mode != 1) return MCF_E_ARG;
+  if (n == 0) return MCF_OK;
+  if (!x || !out) return MCF_E_NULL;
+  const int64_t es = elem_size(dtype);
+  if (bad_alias(out, nc_out * n * es, x, nc_in * n * es)) return MCF_E_ALIAS;
+  return hip_status(mcf::launch_elementwise(dtype, mode == 0 ? mcf::EW_RENORM : mcf::EW_SIMPLE_RENORM, nc_in,
+                                            nc_out, n, x, 1, nullptr, 0, out, (hipStream_t)stream));
+}
+
+int mc_matmul(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B,
+              int b_mc, void *C, void *stream) {
+  if (dtype != MCF_F16 && dtype != MCF_F32) return MCF_E_DTYPE;
+  if (nc < 1 || nc > MAX_NC) return MCF_E_NC;
+  if ((a_mc != 0 && a_mc != 1) || (b_mc != 0 && b_mc != 1) || (!a_mc && !b_mc)) return MCF_E_ARG;
+  if (M < 0 || N < 0 || K < 0) return MCF_E_SHAPE;
+  // grid limits: M / 32 workgroup rows, N / 32 columns
+  if (M > ((int64_t)1 << 20) || N > ((int64_t)1 << 30) || K > ((int64_t)1 << 40)) return MCF_E_SHAPE;
+  if (M == 0 || N == 0) return MCF_OK;
+  if (!C || (K > 0 && (!A || !B))) return MCF_E_NULL;
+  const int64_t es = elem_size(dtype);
+  const int64_t cb = nc * M * N * es;
+  if (overlap(C, cb, A, (a_mc ? nc : 1) * M * K * es) || overlap(C, cb, B, (b_mc ? nc : 1) * K * N * es))
+    return MCF_E_ALIAS;
+  return hip_status(mcf::launch_matmul(dtype, nc, M, N, K, A, a_mc, B, b_mc, 0, nullptr, C, (hipStream_t)stream));
+}
+
+int mc_linear_fwd(int dtype, int nc, int64_t batch, int64_t in, int64_t out, const void *x, const void *W,
+                  const void *b, void *y, void *stream) {
+  if (dtype != MCF_F16 && dtype != MCF_F32) return MCF_E_DTYPE;
+  if (nc < 1 || nc > MAX_NC) return MCF_E_NC;
+  if (batch < 0 || in < 0 || out < 0) return MCF_E_SHAPE;
+  if (batch > ((int64_t)1 << 20) || out > ((int64_t)1 << 30) || in > ((int64_t)1 << 40)) return MCF_E_SHAPE;
+  if (batch == 0 || out == 0) return MCF_OK;
+  if (!y || (in > 0 && (!x || !W))) return MCF_E_NULL;
+  const int64_t es = elem_size(dtype);
+  const int64_t yb = nc * batch * out * es;
+  if (overlap(y, yb, x, batch * in * es) || overlap(y, yb, W, nc * out * in * es) ||
+      (b && overlap(y, yb, b, nc * out * es)))
+    return MCF_E_ALIAS;
+  return hip_status(mcf::launch_matmul(dtype, nc, batch, out, in, x, 0, W, 1, 1, b, y, (hipStream_t)stream));
+}
+
+const char *mc_status_str(int status) {
+  switch (status) {
+    case MCF_OK: return "MCF_OK";
+    case MCF_E_NULL: return "MCF_E_NULL: required pointer is NULL";
+    case MCF_E_NC: return "MCF_E_NC: component count out of range";
+    case MCF_E_SHAPE: return "MCF_E_SHAPE: invalid size";
+    case MCF_E_DTYPE: return "MCF_E_DTYPE: unsupported component format";
+    case MCF_E_ALIAS: return "MCF_E_ALIAS: output overlaps an input";
+    case MCF_E_HIP: return "MCF_E_HIP: HIP runtime error";
+    case MCF_E_ARG: return "MCF_E_ARG: invalid argument";
+  }
+  return "unknown status";
+}
+
+}  // extern "C"

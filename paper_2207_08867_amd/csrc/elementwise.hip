@@ -1,0 +1,341 @@
+// elementwise.hip -- elementwise MC kernels: Add-MCN / Grow-ExpN, ScalingN /
+// Mult-MCN, Div-MCN / DivN, Renormalize / Simple-Renorm, and Exp-MCN (binary16).
+//
+// Data are component-major planes; each thread moves 16 bytes per plane per step
+// (8 binary16 or 4 binary32 elements) with dwordx4 loads and stores, so one wave
+// reads 1 KiB contiguous per plane: fully coalesced HBM streams.  The arithmetic of
+// each element is the per-element algorithm of mcf_arith.hpp.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <atomic>
+#include <mutex>
+
+#include "mcf_arith.hpp"
+#include "mcf_internal.hpp"
+
+namespace mcf {
+
+constexpr int EW_THREADS = 256;
+
+template <typename T, int W>
+struct Pack {
+  T v[W];
+};
+
+template <typename T, int W>
+__device__ __forceinline__ Pack<T, W> load_pack(const T *p) {
+  Pack<T, W> r;
+  if constexpr (W * sizeof(T) == 16) {
+    uint4 raw = *reinterpret_cast<const uint4 *>(p);
+    __builtin_memcpy(&r, &raw, 16);
+  } else {
+#pragma unroll
+    for (int w = 0; w < W; ++w) r.v[w] = p[w];
+  }
+  return r;
+}
+
+template <typename T, int W>
+__device__ __forceinline__ void store_pack(T *p, const Pack<T, W> &r) {
+  if constexpr (W * sizeof(T) == 16) {
+    uint4 raw;
+    __builtin_memcpy(&raw, &r, 16);
+    *reinterpret_cast<uint4 *>(p) = raw;
+  } else {
+#pragma unroll
+    for (int w = 0; w < W; ++w) p[w] = r.v[w];
+  }
+}
+
+// The algorithm applied to one element.  Plain operands arrive in slot 0 with the
+// other slots +0, which is exactly the zero padding DivN and (MC, T) division use.
+template <typename T, int NC, int OP, bool XMC, bool YMC, int NCOUT>
+__device__ __forceinline__ void elem(const T (&a)[NC], const T (&b)[NC], T (&r)[NCOUT]) {
+  if constexpr (OP == EW_ADD) {
+    if constexpr (XMC && YMC)
+      add_mcn<T, NC>(a, b, r);
+    else if constexpr (XMC)
+      grow_expn<T, NC>(a, b[0], r);
+    else
+      grow_expn<T, NC>(b, a[0], r);
+  } else if constexpr (OP == EW_MUL) {
+    if constexpr (XMC && YMC)
+      mult_mcn<T, NC>(a, b, r);
+    else if constexpr (XMC)
+      scaling_n<T, NC, NC>(a, b[0], r);
+    else
+      scaling_n<T, NC, NC>(b, a[0], r);
+  } else if constexpr (OP == EW_DIV) {
+    div_mcn<T, NC>(a, b, r);
+  } else if constexpr (OP == EW_RENORM) {
+    renormalize<T, NC, NCOUT>(a, r);
+  } else {
+    simple_renorm<T, NC, NCOUT>(a, r);
+  }
+}
+
+// Process W consecutive elements starting at element index e0 (all in range).
+template <typename T, int NC, int OP, bool XMC, bool YMC, int NCOUT, int W>
+__device__ __forceinline__ void ew_chunk(const T *x, const T *y, T *out, int64_t n, int64_t e0) {
+  constexpr int XN = XMC ? NC : 1;
+  constexpr int YN = (OP == EW_RENORM || OP == EW_SIMPLE_RENORM) ? 0 : (YMC ? NC : 1);
+  Pack<T, W> xa[XN];
+  Pack<T, W> ya[YN > 0 ? YN : 1];
+#pragma unroll
+  for (int c = 0; c < XN; ++c) xa[c] = load_pack<T, W>(x + c * n + e0);
+#pragma unroll
+  for (int c = 0; c < YN; ++c) ya[c] = load_pack<T, W>(y + c * n + e0);
+  Pack<T, W> res[NCOUT];
+#pragma unroll
+  for (int w = 0; w < W; ++w) {
+    T a[NC], b[NC], r[NCOUT];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      a[c] = c < XN ? xa[c < XN ? c : 0].v[w] : T(0);
+      b[c] = c < YN ? ya[c < YN ? c : 0].v[w] : T(0);
+    }
+    elem<T, NC, OP, XMC, YMC, NCOUT>(a, b, r);
+#pragma unroll
+    for (int c = 0; c < NCOUT; ++c) res[c].v[w] = r[c];
+  }
+#pragma unroll
+  for (int c = 0; c < NCOUT; ++c) store_pack<T, W>(out + c * n + e0, res[c]);
+}
+
+// Grid-stride over chunks of W elements; the last n % W elements one per thread.
+// Inputs and output may alias exactly (in place): every element is read by the
+// thread that writes it, before it writes.
+template <typename T, int NC, int OP, bool XMC, bool YMC, int NCOUT, int W>
+__global__ __launch_bounds__(EW_THREADS) void ew_kernel(const T *x, const T *y, T *out, int64_t n) {
+  const int64_t nchunk = n / W;
+  const int64_t stride = (int64_t)gridDim.x * EW_THREADS;
+  const int64_t tid = (int64_t)blockIdx.x * EW_THREADS + threadIdx.x;
+  for (int64_t ch = tid; ch < nchunk; ch += stride) ew_chunk<T, NC, OP, XMC, YMC, NCOUT, W>(x, y, out, n, ch * W);
+  if constexpr (W > 1) {
+    const int64_t tail = n - nchunk * W;
+    if (tid < tail) ew_chunk<T, NC, OP, XMC, YMC, NCOUT, 1>(x, y, out, n, nchunk * W + tid);
+  }
+}
+
+static int ew_blocks(int64_t work) {
+  int64_t b = (work + EW_THREADS - 1) / EW_THREADS;
+  if (b < 1) b = 1;
+  if (b > 4096) b = 4096;
+  return (int)b;
+}
+
+template <typename T, int NC, int OP, bool XMC, bool YMC, int NCOUT>
+static hipError_t ew_launch(int64_t n, const void *x, const void *y, void *out, hipStream_t s) {
+  constexpr int W = 16 / sizeof(T);
+  const T *xp = (const T *)x;
+  const T *yp = (const T *)y;
+  T *op = (T *)out;
+  // 16-byte vector access needs every plane start aligned to 16 bytes.
+  bool vec = ((n * (int64_t)sizeof(T)) % 16 == 0) && ((uintptr_t)x % 16 == 0) &&
+             (y == nullptr || (uintptr_t)y % 16 == 0) && ((uintptr_t)out % 16 == 0);
+  if (vec) {
+    hipLaunchKernelGGL((ew_kernel<T, NC, OP, XMC, YMC, NCOUT, W>), dim3(ew_blocks(n / W)), dim3(EW_THREADS), 0, s,
+                       xp, yp, op, n);
+  } else {
+    hipLaunchKernelGGL((ew_kernel<T, NC, OP, XMC, YMC, NCOUT, 1>), dim3(ew_blocks(n)), dim3(EW_THREADS), 0, s, xp,
+                       yp, op, n);
+  }
+  return hipGetLastError();
+}
+
+template <typename T, int NC, int OP>
+static hipError_t ew_kinds(int64_t n, const void *x, int x_mc, const void *y, int y_mc, void *out, hipStream_t s) {
+  if (x_mc && y_mc) return ew_launch<T, NC, OP, true, true, NC>(n, x, y, out, s);
+  if (x_mc) return ew_launch<T, NC, OP, true, false, NC>(n, x, y, out, s);
+  return ew_launch<T, NC, OP, false, true, NC>(n, x, y, out, s);
+}
+
+template <typename T, int NC, int OP, int NCOUT>
+static hipError_t renorm_out(int64_t n, const void *x, void *out, hipStream_t s) {
+  return ew_launch<T, NC, OP, true, false, NCOUT>(n, x, nullptr, out, s);
+}
+
+template <typename T, int NC, int OP>
+static hipError_t renorm_dispatch(int nc_out, int64_t n, const void *x, void *out, hipStream_t s) {
+  switch (nc_out) {
+    case 1: return renorm_out<T, NC, OP, 1>(n, x, out, s);
+    case 2: if constexpr (NC >= 2) return renorm_out<T, NC, OP, 2>(n, x, out, s); break;
+    case 3: if constexpr (NC >= 3) return renorm_out<T, NC, OP, 3>(n, x, out, s); break;
+    case 4: if constexpr (NC >= 4) return renorm_out<T, NC, OP, 4>(n, x, out, s); break;
+  }
+  return hipErrorInvalidValue;
+}
+
+template <typename T, int NC>
+static hipError_t ew_dispatch_nc(int op, int nc_out, int64_t n, const void *x, int x_mc, const void *y, int y_mc,
+                                 void *out, hipStream_t s) {
+  switch (op) {
+    case EW_ADD: return ew_kinds<T, NC, EW_ADD>(n, x, x_mc, y, y_mc, out, s);
+    case EW_MUL: return ew_kinds<T, NC, EW_MUL>(n, x, x_mc, y, y_mc, out, s);
+    case EW_DIV: return ew_kinds<T, NC, EW_DIV>(n, x, x_mc, y, y_mc, out, s);
+    case EW_RENORM: return renorm_dispatch<T, NC, EW_RENORM>(nc_out, n, x, out, s);
+    case EW_SIMPLE_RENORM: return renorm_dispatch<T, NC, EW_SIMPLE_RENORM>(nc_out, n, x, out, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+template <typename T>
+static hipError_t ew_dispatch(int op, int nc, int nc_out, int64_t n, const void *x, int x_mc, const void *y,
+                              int y_mc, void *out, hipStream_t s) {
+  switch (nc) {
+    case 1: return ew_dispatch_nc<T, 1>(op, nc_out, n, x, x_mc, y, y_mc, out, s);
+    case 2: return ew_dispatch_nc<T, 2>(op, nc_out, n, x, x_mc, y, y_mc, out, s);
+    case 3: return ew_dispatch_nc<T, 3>(op, nc_out, n, x, x_mc, y, y_mc, out, s);
+    case 4: return ew_dispatch_nc<T, 4>(op, nc_out, n, x, x_mc, y, y_mc, out, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_elementwise(int dtype, int op, int nc, int nc_out, int64_t n, const void *x, int x_mc,
+                              const void *y, int y_mc, void *out, hipStream_t stream) {
+  if (dtype == 0) return ew_dispatch<_Float16>(op, nc, nc_out, n, x, x_mc, y, y_mc, out, stream);
+  return ew_dispatch<float>(op, nc, nc_out, n, x, x_mc, y, y_mc, out, stream);
+}
+
+// ---------------------------------------------------------------------------------
+// Exp-MCN, binary16
+// ---------------------------------------------------------------------------------
+
+// Correctly rounded binary16 exponential for all 65536 encodings, one table per
+// device.  e^x is evaluated in binary64 (error below 2^-50 relative) and rounded once
+// to binary16.  Over all finite binary16 x, e^x lies at least 2^-26.4 (relative) away
+// from any binary16 rounding boundary, so the binary64 evaluation always rounds to
+// the correctly rounded binary16 value.
+__device__ _Float16 g_exp16_table[65536];
+
+__global__ __launch_bounds__(256) void exp16_table_kernel(_Float16 *tab) {
+  const int h = blockIdx.x * 256 + threadIdx.x;
+  const unsigned short bits = (unsigned short)h;
+  _Float16 x;
+  __builtin_memcpy(&x, &bits, 2);
+  tab[h] = (_Float16)exp((double)x);
+}
+
+static std::mutex g_exp_mutex;
+static _Float16 *g_exp_table_ptr[64];
+static std::atomic<bool> g_exp_ready[64];
+
+static hipError_t exp_table(_Float16 **tab, hipStream_t s) {
+  int dev = 0;
+  hipError_t err = hipGetDevice(&dev);
+  if (err != hipSuccess) return err;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  if (!g_exp_ready[dev].load(std::memory_order_acquire)) {
+    std::lock_guard<std::mutex> lock(g_exp_mutex);
+    if (!g_exp_ready[dev].load(std::memory_order_relaxed)) {
+      void *p = nullptr;
+      err = hipGetSymbolAddress(&p, HIP_SYMBOL(g_exp16_table));
+      if (err != hipSuccess) return err;
+      hipLaunchKernelGGL(exp16_table_kernel, dim3(65536 / 256), dim3(256), 0, s, (_Float16 *)p);
+      err = hipGetLastError();
+      if (err != hipSuccess) return err;
+      // the table must be complete before any stream reads it
+      err = hipStreamSynchronize(s);
+      if (err != hipSuccess) return err;
+      g_exp_table_ptr[dev] = (_Float16 *)p;
+      g_exp_ready[dev].store(true, std::memory_order_release);
+    }
+  }
+  *tab = g_exp_table_ptr[dev];
+  return hipSuccess;
+}
+
+constexpr int EXP_THREADS = 1024;
+
+// Exp-MCN for one element from the component exponentials ex[0..N-1]:
+// h = (ex_0), then h = ScalingN(h, ex_i) with expand, one component longer per step.
+template <int N, int M>
+__device__ __forceinline__ void exp_chain(const _Float16 (&h)[M], const _Float16 (&ex)[N], _Float16 (&out)[N]) {
+  if constexpr (M == N) {
+#pragma unroll
+    for (int c = 0; c < N; ++c) out[c] = h[c];
+  } else {
+    _Float16 g[M + 1];
+    scaling_n<_Float16, M, M + 1>(h, ex[M], g);
+    exp_chain<N, M + 1>(g, ex, out);
+  }
+}
+
+// One workgroup per CU holds the whole 128 KiB table in LDS; elements are looked up
+// by their bit pattern.
+template <int NC, int W>
+__global__ __launch_bounds__(EXP_THREADS) void exp16_kernel(const _Float16 *x, _Float16 *out, int64_t n,
+                                                            const _Float16 *table) {
+  __shared__ uint4 lds_tab[65536 * 2 / 16];
+  const uint4 *gt = reinterpret_cast<const uint4 *>(table);
+  for (int i = threadIdx.x; i < 65536 * 2 / 16; i += EXP_THREADS) lds_tab[i] = gt[i];
+  __syncthreads();
+  const _Float16 *tab = reinterpret_cast<const _Float16 *>(lds_tab);
+  const int64_t nchunk = n / W;
+  const int64_t stride = (int64_t)gridDim.x * EXP_THREADS;
+  const int64_t tid = (int64_t)blockIdx.x * EXP_THREADS + threadIdx.x;
+  auto one = [&](int64_t e0, auto wtag) {
+    constexpr int WW = decltype(wtag)::value;
+    Pack<_Float16, WW> xa[NC], res[NC];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) xa[c] = load_pack<_Float16, WW>(x + c * n + e0);
+#pragma unroll
+    for (int w = 0; w < WW; ++w) {
+      _Float16 ex[NC];
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        unsigned short b;
+        __builtin_memcpy(&b, &xa[c].v[w], 2);
+        ex[c] = tab[b];
+      }
+      _Float16 h0[1] = {ex[0]};
+      _Float16 r[NC];
+      exp_chain<NC, 1>(h0, ex, r);
+#pragma unroll
+      for (int c = 0; c < NC; ++c) res[c].v[w] = r[c];
+    }
+#pragma unroll
+    for (int c = 0; c < NC; ++c) store_pack<_Float16, WW>(out + c * n + e0, res[c]);
+  };
+  for (int64_t ch = tid; ch < nchunk; ch += stride) one(ch * W, std::integral_constant<int, W>());
+  if constexpr (W > 1) {
+    const int64_t tail = n - nchunk * W;
+    if (tid < tail) one(nchunk * W + tid, std::integral_constant<int, 1>());
+  }
+}
+
+template <int NC>
+static hipError_t exp16_launch(int64_t n, const void *x, void *out, const _Float16 *tab, hipStream_t s) {
+  int dev = 0, cus = 256;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    cus = 256;
+  bool vec = (n % 8 == 0) && ((uintptr_t)x % 16 == 0) && ((uintptr_t)out % 16 == 0);
+  int64_t work = vec ? n / 8 : n;
+  int64_t blocks = (work + EXP_THREADS - 1) / EXP_THREADS;
+  if (blocks > cus) blocks = cus;
+  if (blocks < 1) blocks = 1;
+  if (vec)
+    hipLaunchKernelGGL((exp16_kernel<NC, 8>), dim3(blocks), dim3(EXP_THREADS), 0, s, (const _Float16 *)x,
+                       (_Float16 *)out, n, tab);
+  else
+    hipLaunchKernelGGL((exp16_kernel<NC, 1>), dim3(blocks), dim3(EXP_THREADS), 0, s, (const _Float16 *)x,
+                       (_Float16 *)out, n, tab);
+  return hipGetLastError();
+}
+
+hipError_t launch_exp_f16(int nc, int64_t n, const void *x, void *out, hipStream_t stream) {
+  _Float16 *tab = nullptr;
+  hipError_t err = exp_table(&tab, stream);
+  if (err != hipSuccess) return err;
+  switch (nc) {
+    case 1: return exp16_launch<1>(n, x, out, tab, stream);
+    case 2: return exp16_launch<2>(n, x, out, tab, stream);
+    case 3: return exp16_launch<3>(n, x, out, tab, stream);
+    case 4: return exp16_launch<4>(n, x, out, tab, stream);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace mcf

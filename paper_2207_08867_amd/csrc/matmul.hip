@@ -1,0 +1,183 @@
+// matmul.hip -- MC matrix product (MM-MCN) and MC-Linear forward on gfx950 VALU.
+//
+// Every output C[i][j] is owned by one lane, which walks k = 0 .. K-1 in order:
+// acc = ScalingN(term 0), acc = Add-MCN(acc, ScalingN(term k)).  This is the
+// sequential error propagation of MM-MCN, so the result does not depend on tiling
+// or launch geometry and matches the reference order bit for bit.  The contraction
+// cannot use the matrix cores: every product and partial sum needs its exact
+// rounding error (Two-Prod / Two-Sum), which only the vector ALU's FMA and IEEE adds
+// deliver.
+//
+// Tiling: a 256-lane workgroup owns a BM x BN block of C; each lane owns TM x TN
+// outputs.  A and B tiles of KT reduction steps are staged through LDS, component
+// planes kept separate, A transposed to [k][m] so a lane reads its TM rows with one
+// vector LDS load.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "mcf_arith.hpp"
+#include "mcf_internal.hpp"
+
+namespace mcf {
+
+constexpr int MM_THREADS = 256;
+
+template <typename T, int NC>
+__device__ __forceinline__ void mac(T (&acc)[NC], const T (&mc)[NC], T v, bool first) {
+  T term[NC];
+  scaling_n<T, NC, NC>(mc, v, term);
+  if (first) {
+#pragma unroll
+    for (int c = 0; c < NC; ++c) acc[c] = term[c];
+  } else {
+    add_mcn<T, NC>(acc, term, acc);
+  }
+}
+
+// A: [NA][M][K] row-major planes.  B: [NB][K][N] (BT = false) or [NB][N][K] (BT =
+// true).  NA = NC when A is MC else 1, likewise NB.
+template <typename T, int NC, bool AMC, bool BMC, bool BT, int TM, int TN, int KT>
+__global__ __launch_bounds__(MM_THREADS) void mm_kernel(const T *__restrict__ A, const T *__restrict__ B,
+                                                        const T *__restrict__ bias, T *__restrict__ C, int64_t M,
+                                                        int64_t N, int64_t K) {
+  constexpr int NA = AMC ? NC : 1;
+  constexpr int NB = BMC ? NC : 1;
+  constexpr int TX = 16, TY = 16;  // lanes along N and along M
+  constexpr int BM = TY * TM, BN = TX * TN;
+  constexpr int NP = (AMC && BMC) ? NC : 1;  // plain components to sweep (MC x MC)
+  __shared__ T As[NA][KT][BM];
+  __shared__ T Bs[NB][KT][BN];
+
+  const int tx = threadIdx.x % TX, ty = threadIdx.x / TX;
+  const int64_t m0 = (int64_t)blockIdx.y * BM, n0 = (int64_t)blockIdx.x * BN;
+
+  T acc[NP][TM][TN][NC];
+
+  for (int64_t k0 = 0; k0 < K; k0 += KT) {
+    const int kt = (int)((K - k0) < KT ? (K - k0) : KT);
+    // stage A tile: rows m0..m0+BM-1, reduction steps k0..k0+KT-1
+    for (int idx = threadIdx.x; idx < BM * KT; idx += MM_THREADS) {
+      const int r = idx / KT, kk = idx % KT;
+      const int64_t gm = m0 + r, gk = k0 + kk;
+      const bool ok = gm < M && gk < K;
+#pragma unroll
+      for (int c = 0; c < NA; ++c) As[c][kk][r] = ok ? A[c * M * K + gm * K + gk] : T(0);
+    }
+    for (int idx = threadIdx.x; idx < BN * KT; idx += MM_THREADS) {
+      int col, kk;
+      if constexpr (BT) {
+        col = idx / KT;
+        kk = idx % KT;
+      } else {
+        kk = idx / BN;
+        col = idx % BN;
+      }
+      const int64_t gn = n0 + col, gk = k0 + kk;
+      const bool ok = gn < N && gk < K;
+#pragma unroll
+      for (int c = 0; c < NB; ++c) {
+        const int64_t off = BT ? (c * N * K + gn * K + gk) : (c * K * N + gk * N + gn);
+        Bs[c][kk][col] = ok ? B[off] : T(0);
+      }
+    }
+    __syncthreads();
+    for (int kk = 0; kk < kt; ++kk) {
+      const bool first = (k0 + kk) == 0;
+      T a[TM][NA], b[TN][NB];
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int c = 0; c < NA; ++c) a[i][c] = As[c][kk][ty * TM + i];
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int c = 0; c < NB; ++c) b[j][c] = Bs[c][kk][tx * TN + j];
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          if constexpr (AMC && BMC) {
+#pragma unroll
+            for (int p = 0; p < NP; ++p) mac<T, NC>(acc[p][i][j], a[i], b[j][p], first);
+          } else if constexpr (AMC) {
+            mac<T, NC>(acc[0][i][j], a[i], b[j][0], first);
+          } else {
+            mac<T, NC>(acc[0][i][j], b[j], a[i][0], first);
+          }
+        }
+    }
+    __syncthreads();
+  }
+
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int64_t gm = m0 + ty * TM + i, gn = n0 + tx * TN + j;
+      T r[NC];
+      if (K == 0) {
+#pragma unroll
+        for (int c = 0; c < NC; ++c) r[c] = T(0);
+      } else {
+#pragma unroll
+        for (int c = 0; c < NC; ++c) r[c] = acc[0][i][j][c];
+        // MC x MC: combine the per-component products left to right
+#pragma unroll
+        for (int p = 1; p < NP; ++p) add_mcn<T, NC>(r, acc[p][i][j], r);
+      }
+      if (gm < M && gn < N) {
+        if (bias != nullptr) {
+          T bv[NC];
+#pragma unroll
+          for (int c = 0; c < NC; ++c) bv[c] = bias[c * N + gn];
+          add_mcn<T, NC>(r, bv, r);
+        }
+#pragma unroll
+        for (int c = 0; c < NC; ++c) C[c * M * N + gm * N + gn] = r[c];
+      }
+    }
+}
+
+template <typename T, int NC, bool AMC, bool BMC, bool BT>
+static hipError_t mm_launch(int64_t M, int64_t N, int64_t K, const void *A, const void *B, const void *bias,
+                            void *C, hipStream_t s) {
+  constexpr int TM = 2, TN = 2, KT = 16;
+  constexpr int BM = 16 * TM, BN = 16 * TN;
+  dim3 grid((unsigned)((N + BN - 1) / BN), (unsigned)((M + BM - 1) / BM));
+  hipLaunchKernelGGL((mm_kernel<T, NC, AMC, BMC, BT, TM, TN, KT>), grid, dim3(MM_THREADS), 0, s, (const T *)A,
+                     (const T *)B, (const T *)bias, (T *)C, M, N, K);
+  return hipGetLastError();
+}
+
+template <typename T, int NC>
+static hipError_t mm_kinds(int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B, int b_mc,
+                           int b_trans, const void *bias, void *C, hipStream_t s) {
+  if (b_trans) {
+    // linear layer: plain input times MC weight stored [out][in]
+    if (!a_mc && b_mc) return mm_launch<T, NC, false, true, true>(M, N, K, A, B, bias, C, s);
+    return hipErrorInvalidValue;
+  }
+  if (a_mc && b_mc) return mm_launch<T, NC, true, true, false>(M, N, K, A, B, bias, C, s);
+  if (a_mc) return mm_launch<T, NC, true, false, false>(M, N, K, A, B, bias, C, s);
+  return mm_launch<T, NC, false, true, false>(M, N, K, A, B, bias, C, s);
+}
+
+template <typename T>
+static hipError_t mm_dispatch(int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B,
+                              int b_mc, int b_trans, const void *bias, void *C, hipStream_t s) {
+  switch (nc) {
+    case 1: return mm_kinds<T, 1>(M, N, K, A, a_mc, B, b_mc, b_trans, bias, C, s);
+    case 2: return mm_kinds<T, 2>(M, N, K, A, a_mc, B, b_mc, b_trans, bias, C, s);
+    case 3: return mm_kinds<T, 3>(M, N, K, A, a_mc, B, b_mc, b_trans, bias, C, s);
+    case 4: return mm_kinds<T, 4>(M, N, K, A, a_mc, B, b_mc, b_trans, bias, C, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_matmul(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc,
+                         const void *B, int b_mc, int b_trans, const void *bias, void *C, hipStream_t stream) {
+  if (dtype == 0) return mm_dispatch<_Float16>(nc, M, N, K, A, a_mc, B, b_mc, b_trans, bias, C, stream);
+  return mm_dispatch<float>(nc, M, N, K, A, a_mc, B, b_mc, b_trans, bias, C, stream);
+}
+
+}  // namespace mcf

@@ -87,3 +87,17 @@ def linear_inputs(T, I, O, nc, dtype, layers=1, seed=0):
         W = split(g.uniform(-lim, lim, (O, I)), nc, dtype)
         b = split(g.uniform(-lim, lim, (O,)), nc, dtype)
         yield x, W, b
+
+
+def elementwise_suite(n: int, nc: int, dtype, seed=0):
+    """The elementwise workload's operands drawn once: a ~ U[-1/2, 1/2] (first
+    operand of every op and the Renormalize input), b ~ U[-1/2, 1/2] (second addend),
+    d ~ U[1/2, 3/2] (divisor, and Mult-MCN's second factor), e ~ U[-4, 4] (exp
+    input), each split into nc components."""
+    g = rng(seed)
+    return {
+        "a": split(g.uniform(-0.5, 0.5, n), nc, dtype),
+        "b": split(g.uniform(-0.5, 0.5, n), nc, dtype),
+        "d": split(g.uniform(0.5, 1.5, n), nc, dtype),
+        "e": split(g.uniform(-4.0, 4.0, n), nc, dtype),
+    }

@@ -1,0 +1,81 @@
+"""The C ABI library loads without a GPU, exports every entry point that
+include/mcf.h declares, and rejects invalid arguments before any HIP call."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mcf.h")
+
+MCF_OK, MCF_E_NULL, MCF_E_NC, MCF_E_SHAPE, MCF_E_DTYPE, MCF_E_ALIAS, MCF_E_HIP, MCF_E_ARG = 0, -1, -2, -3, -4, -5, -6, -7
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(mc_\w+)\s*\(", text, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    import paper_2207_08867_amd as m
+
+    return m.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    names = declared_functions()
+    assert {"mc_add", "mc_mul", "mc_div", "mc_exp", "mc_renorm", "mc_matmul", "mc_linear_fwd",
+            "mc_status_str"} <= set(names)
+    for name in names:
+        assert hasattr(L, name), name
+
+
+def test_status_strings(L):
+    for code in range(-7, 1):
+        s = L.mc_status_str(code).decode()
+        assert s.startswith("MCF_")
+    assert L.mc_status_str(-99).decode() == "unknown status"
+
+
+P = ctypes.c_void_p
+
+
+def test_validation_elementwise(L):
+    x = P(0x10000)
+    y = P(0x20000)
+    o = P(0x30000)
+    for f in (L.mc_add, L.mc_mul, L.mc_div):
+        assert f(0, 0, 10, x, 1, y, 1, o, None) == MCF_E_NC
+        assert f(0, 5, 10, x, 1, y, 1, o, None) == MCF_E_NC
+        assert f(2, 3, 10, x, 1, y, 1, o, None) == MCF_E_DTYPE
+        assert f(0, 3, -1, x, 1, y, 1, o, None) == MCF_E_SHAPE
+        assert f(0, 3, 10, x, 0, y, 0, o, None) == MCF_E_ARG
+        assert f(0, 3, 10, x, 2, y, 1, o, None) == MCF_E_ARG
+        assert f(0, 3, 0, None, 1, None, 1, None, None) == MCF_OK  # empty: no launch
+        assert f(0, 3, 10, None, 1, y, 1, o, None) == MCF_E_NULL
+        # out overlapping x partially (shifted by one element)
+        assert f(1, 3, 10, P(0x10000), 1, y, 1, P(0x10004), None) == MCF_E_ALIAS
+        # out overlapping a plain y that is shorter than out
+        assert f(1, 3, 10, x, 1, P(0x30000), 0, o, None) == MCF_E_ALIAS
+    assert L.mc_exp(1, 3, 10, x, o, None) == MCF_E_DTYPE
+    assert L.mc_exp(0, 3, 0, None, None, None) == MCF_OK
+    assert L.mc_renorm(0, 3, 4, 10, x, o, 0, None) == MCF_E_NC
+    assert L.mc_renorm(0, 3, 0, 10, x, o, 0, None) == MCF_E_NC
+    assert L.mc_renorm(0, 3, 2, 10, x, o, 2, None) == MCF_E_ARG
+    assert L.mc_renorm(0, 3, 2, 10, x, x, 0, None) == MCF_E_ALIAS  # in place only when nc_out == nc_in
+
+
+def test_validation_matrix(L):
+    a, b, c = P(0x100000), P(0x200000), P(0x300000)
+    assert L.mc_matmul(0, 3, 4, 4, 4, a, 0, b, 0, c, None) == MCF_E_ARG
+    assert L.mc_matmul(0, 9, 4, 4, 4, a, 1, b, 1, c, None) == MCF_E_NC
+    assert L.mc_matmul(0, 3, -4, 4, 4, a, 1, b, 1, c, None) == MCF_E_SHAPE
+    assert L.mc_matmul(0, 3, 0, 4, 4, a, 1, b, 1, c, None) == MCF_OK
+    assert L.mc_matmul(0, 3, 4, 4, 4, a, 1, b, 1, None, None) == MCF_E_NULL
+    assert L.mc_matmul(0, 3, 4, 4, 4, a, 1, b, 1, P(0x100000 + 8), None) == MCF_E_ALIAS
+    assert L.mc_linear_fwd(0, 3, 4, 4, 4, None, b, None, c, None) == MCF_E_NULL
+    assert L.mc_linear_fwd(0, 3, 4, 4, 4, a, b, P(0x300000), c, None) == MCF_E_ALIAS
+    assert L.mc_linear_fwd(0, 3, 0, 4, 4, None, None, None, None, None) == MCF_OK

@@ -1,0 +1,131 @@
+"""GPU parity of the MC matrix product and MC-Linear against the CPU oracle.
+
+Each output is accumulated over k in MM-MCN order on the GPU as in the oracle, so
+the comparison is bitwise.  The error against the exact product of the MC inputs
+is checked as well: max_ij |C_ij - C*_ij| / (|A||B|)_ij <= 4 K u^nc, plus in
+binary16 a floor of nA nB K 2^-25 for Two-Prod errors that fall below the
+subnormal grid.  Small cases span several 32x32 tiles with ragged edges; the
+full-size workloads are checked on sampled outputs.
+"""
+import numpy as np
+import pytest
+
+from paper_2207_08867_amd import inputs
+from test_gpu_elementwise import assert_bits, to_dev, to_host
+
+pytestmark = pytest.mark.gpu
+
+U = {np.float16: 2.0 ** -11, np.float32: 2.0 ** -24}
+
+
+@pytest.fixture(scope="module")
+def mcf():
+    import torch
+
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2207_08867_amd as m
+
+    m.lib()
+    return m
+
+
+def check_bound(orc, A, B, C, nc, K, dt, rows=None, cols=None, bias=None):
+    """Error against the exact product.  ScalingN and Add-MCN round their level-1
+    carry, fl(e1 + e2), whose error is of order u^3 of the operands, so beyond
+    nc = 3 the attainable accuracy stays at u^3: the bound uses u^min(nc, 3)."""
+    err, absab, _ = orc.matmul_exact_err(A, B, C, rows=rows, cols=cols, bias=bias)
+    u = U[dt]
+    floor = A.shape[0] * B.shape[0] * K * 2.0 ** -25 if dt == np.float16 else 0.0
+    lim = 4 * K * u ** min(nc, 3) * absab + floor
+    ratio = np.abs(err) / np.where(lim > 0, lim, 1)
+    assert (np.abs(err) <= lim).all(), f"bound exceeded: worst ratio {ratio.max():.3g}"
+    return float(np.max(np.abs(err) / np.where(absab > 0, absab, 1)))
+
+
+@pytest.mark.parametrize("dt", [np.float16, np.float32])
+@pytest.mark.parametrize("nc", [1, 2, 3, 4])
+@pytest.mark.parametrize("kinds", [(True, True), (True, False), (False, True)])
+def test_small_ragged_parity(mcf, orc, dt, nc, kinds):
+    a_mc, b_mc = kinds
+    M, N, K = 70, 45, 37
+    A, B = inputs.matmul_normal(M, N, K, nc, dt, seed=40 + nc)
+    A = A if a_mc else A[:1]
+    B = B if b_mc else B[:1]
+    got = to_host(mcf.mc_matmul(to_dev(A), to_dev(B), nc=nc, a_mc=a_mc, b_mc=b_mc))
+    want = orc.matmul(A, B, nc=nc, a_mc=a_mc, b_mc=b_mc)
+    assert_bits(got, want, f"matmul {dt.__name__} nc={nc} {kinds}")
+    check_bound(orc, A, B, got, nc, K, dt)
+
+
+@pytest.mark.parametrize("shape", [(1, 1, 300), (1, 97, 64), (97, 1, 64), (33, 31, 1), (5, 7, 0), (129, 2, 3)])
+def test_degenerate_shapes(mcf, orc, shape):
+    M, N, K = shape
+    nc, dt = 3, np.float32
+    A, B = inputs.matmul_uniform(M, N, K, nc, dt, seed=50)
+    got = to_host(mcf.mc_matmul(to_dev(A), to_dev(B), nc=nc))
+    assert_bits(got, orc.matmul(A, B, nc=nc), f"matmul {shape}")
+
+
+def test_config_64_fp32_nc2_exact(mcf, orc):
+    """M = N = K = 64, binary32, nc = 2, A and B uniform in [-1, 1] (seed 0): every
+    output bitwise and within 4 K u^2 of the exact product."""
+    A, B = inputs.matmul_uniform(64, 64, 64, 2, np.float32, seed=0)
+    got = to_host(mcf.mc_matmul(to_dev(A), to_dev(B), nc=2))
+    assert_bits(got, orc.matmul(A, B, nc=2), "64^3")
+    worst = check_bound(orc, A, B, got, 2, 64, np.float32)
+    assert worst < 2.0 ** -40
+
+
+@pytest.mark.parametrize("nc", [2, 3])
+def test_config_1024_fp16(mcf, orc, nc):
+    """M = N = K = 1024, binary16, entries N(0, 1/K): 512 sampled outputs bitwise
+    against the oracle and within the bound of the exact product."""
+    n = 1024
+    A, B = inputs.matmul_normal(n, n, n, nc, np.float16, seed=0)
+    got = to_host(mcf.mc_matmul(to_dev(A), to_dev(B), nc=nc))
+    g = np.random.default_rng(60 + nc)
+    rows = np.concatenate([g.integers(0, n, 500), [0, 0, n - 1, n - 1]])
+    cols = np.concatenate([g.integers(0, n, 500), [0, n - 1, 0, n - 1]])
+    want = orc.matmul(A, B, nc=nc, rows=rows, cols=cols)
+    assert_bits(got[:, rows, cols], want, f"1024^3 nc={nc}")
+    check_bound(orc, A, B, np.ascontiguousarray(got[:, rows, cols]), nc, n, np.float16, rows=rows, cols=cols)
+
+
+@pytest.mark.parametrize("bias", [True, False])
+def test_linear_small(mcf, orc, bias):
+    for dt in (np.float16, np.float32):
+        x, W, b = next(inputs.linear_inputs(77, 53, 41, 3, dt, seed=70))
+        got = to_host(mcf.mc_linear_fwd(to_dev(x), to_dev(W), to_dev(b) if bias else None))
+        want = orc.linear(x, W, b if bias else None, nc=3)
+        assert_bits(got, want, f"linear {dt.__name__} bias={bias}")
+
+
+def test_linear_config_layer(mcf, orc):
+    """Batch 4096, in 1024, out 1024, binary16 nc = 3: the first layer's 512 sampled
+    outputs bitwise, and within 4 K u^3 (+ floor) of the exact result."""
+    T, I, O = 4096, 1024, 1024
+    x, W, b = next(inputs.linear_inputs(T, I, O, 3, np.float16, seed=0))
+    got = to_host(mcf.mc_linear_fwd(to_dev(x), to_dev(W), to_dev(b)))
+    g = np.random.default_rng(71)
+    rows = g.integers(0, T, 512)
+    cols = g.integers(0, O, 512)
+    want = orc.linear(x, W, b, nc=3, rows=rows, cols=cols)
+    assert_bits(got[:, rows, cols], want, "linear layer")
+    Bm = np.ascontiguousarray(W.transpose(0, 2, 1))
+    check_bound(orc, x[None], Bm, np.ascontiguousarray(got[:, rows, cols]), 3, I, np.float16, rows=rows, cols=cols,
+                bias=b)
+
+
+def test_deterministic_and_errors(mcf):
+    import torch
+
+    A, B = inputs.matmul_normal(100, 90, 80, 3, np.float32, seed=80)
+    tA, tB = to_dev(A), to_dev(B)
+    c1 = to_host(mcf.mc_matmul(tA, tB, nc=3))
+    c2 = to_host(mcf.mc_matmul(tA, tB, nc=3))
+    assert_bits(c1, c2, "repeat")
+    with pytest.raises(ValueError):  # wrong output shape
+        mcf.mc_matmul(tA, tB, nc=3, out=torch.empty((3, 100, 91), dtype=torch.float32, device="cuda"))
+    big = torch.empty((3, 100, 80), dtype=torch.float32, device="cuda")
+    with pytest.raises(ValueError):  # output overlapping an input
+        mcf.mc_matmul(big, tB[:, :80, :80].contiguous(), nc=3, out=big)
