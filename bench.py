@@ -29,8 +29,11 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-VALU_PEAK = 256 * 4 * 16 * 2.4e9  # lane-operations / s: 256 CUs x 4 SIMD16 x 2.4 GHz
-VALU_PEAK_PACKED16 = 2 * VALU_PEAK  # two binary16 lanes per packed instruction
+# VALU issue peak: 256 CUs x 128 binary32 lane-operations per clock x 2.4 GHz = 78.6e12
+# lane-operations / s (the 157.3 TFLOP/s binary32 vector figure counts an FMA as two).
+# A packed binary16 instruction carries two lanes of work but issues at half rate, so
+# the element-operation peak is the same for binary16.
+VALU_PEAK = 256 * 128 * 2.4e9
 HBM_PEAK = 8.0e12  # bytes / s
 
 
@@ -186,6 +189,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-extra", action="store_true", help="only the headline workload")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="also run one 1 GiB device-to-device copy (reference for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py: this build runs on one GPU only; the MC product shards by output blocks "
@@ -200,6 +205,13 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     mcf.lib()
+
+    if args.copy_probe:
+        src = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     M = N = K = 8192
     nc = 3
@@ -251,7 +263,7 @@ def main():
             macs = 1024 ** 3
             extra[f"matmul_1024_f16_nc{nc3}"] = {
                 "ms": round(k3, 3), "MC-GFLOP/s": round(2 * macs / (k3 * 1e-3) / 1e9, 1),
-                "valu_frac_unpacked": round(algo_ops_per_mac(nc3, True) * macs / (k3 * 1e-3) / VALU_PEAK, 3),
+                "valu_frac": round(algo_ops_per_mac(nc3, True) * macs / (k3 * 1e-3) / VALU_PEAK, 3),
                 "error": exact_error(oracle, A3, B3, C3.cpu().numpy(), nc3, 1024, np.float16)}
             log(f"  1024^3 f16 nc={nc3}: {k3:.2f} ms")
         log("MC-Linear")
