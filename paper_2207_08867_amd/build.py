@@ -3,6 +3,9 @@
 Flags that matter for the arithmetic:
   -ffp-contract=off   no multiply-add fusion except the explicit FMA of Two-Prod;
   no fast-math        IEEE rounding, gradual underflow, correctly rounded division;
+  -fno-slp-vectorize  keep binary16 arithmetic scalar: gfx950 issues packed binary16
+                      instructions at half the rate of scalar ones, so packing only adds
+                      the cost of moving halves around;
   -packed-fp32-ops    the compiler may not pair binary32 operations into packed
                       instructions.
 """
@@ -21,7 +24,7 @@ ARCH = "gfx950"
 
 CFLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-ffp-contract=off",
-    "-fno-gpu-flush-denormals-to-zero",
+    "-fno-gpu-flush-denormals-to-zero", "-fno-slp-vectorize",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-function",
 ]

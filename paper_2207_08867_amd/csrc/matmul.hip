@@ -22,16 +22,109 @@ namespace mcf {
 
 constexpr int MM_THREADS = 256;
 
-template <typename T, int NC>
-__device__ __forceinline__ void mac(T (&acc)[NC], const T (&mc)[NC], T v, bool first) {
-  T term[NC];
-  scaling_n<T, NC, NC>(mc, v, term);
-  if (first) {
-#pragma unroll
-    for (int c = 0; c < NC; ++c) acc[c] = term[c];
+// ---------------------------------------------------------------------------------
+// The two steps of one MM-MCN term, in the form the product kernel executes them.
+//
+// They compute exactly what scaling_n / add_mcn of mcf_arith.hpp compute on finite,
+// non-overflowing data, with two shortcuts that change nothing but the sign of a
+// zero term, and zero terms are all dropped by Simple-Renorm (which pads with +0):
+//   * the first Two-Sum of each step adds the initial carry +0: Two-Sum(h, +0) =
+//     (h + 0, +0), so h_0 is the first product (resp. sum) and the carry its error;
+//   * Simple-Renorm of nc+1 terms keeps h_0 .. h_{nc-2} unchanged when they are all
+//     non-zero and then only chooses between h_{nc-1} and h_nc; the general
+//     compaction runs only in lanes where a leading term is zero.
+// ---------------------------------------------------------------------------------
+
+template <typename T, int N>
+__device__ __forceinline__ void sr_fast(const T (&h)[N + 1], T (&out)[N]) {
+  if constexpr (N == 1) {
+    out[0] = (h[0] != T(0)) ? h[0] : h[1];
   } else {
-    add_mcn<T, NC>(acc, term, acc);
+    bool lead = true;
+#pragma unroll
+    for (int i = 0; i < N - 1; ++i) lead = lead && (h[i] != T(0));
+#pragma unroll
+    for (int i = 0; i < N - 1; ++i) out[i] = h[i];
+    out[N - 1] = (h[N - 1] != T(0)) ? h[N - 1] : h[N];
+    if (__builtin_expect(!lead, 0)) simple_renorm<T, N + 1, N>(h, out);
   }
+}
+
+// ScalingN(x, v) without expand.
+template <typename T, int N>
+__device__ __forceinline__ void mm_scaling(const T (&x)[N], T v, T (&out)[N]) {
+  T h[N + 1];
+  T e;
+  two_prod(x[0], v, h[0], e);
+#pragma unroll
+  for (int i = 1; i < N; ++i) {
+    T hp, e1, e2;
+    two_prod(x[i], v, hp, e1);
+    two_sum(hp, e, h[i], e2);
+    e = e1 + e2;
+  }
+  h[N] = e;
+  sr_fast<T, N>(h, out);
+}
+
+// Add-MCN(x, y).
+template <typename T, int N>
+__device__ __forceinline__ void mm_add(const T (&x)[N], const T (&y)[N], T (&out)[N]) {
+  T h[N + 1];
+  T e;
+  two_sum(x[0], y[0], h[0], e);
+#pragma unroll
+  for (int i = 1; i < N; ++i) {
+    T hp, e1, e2;
+    two_sum(x[i], y[i], hp, e1);
+    two_sum(hp, e, h[i], e2);
+    e = e1 + e2;
+  }
+  h[N] = e;
+  sr_fast<T, N>(h, out);
+}
+
+// acc = ScalingN(mc, v) (first term) or acc = Add-MCN(acc, ScalingN(mc, v)).
+template <typename T, int NC, bool FIRST>
+__device__ __forceinline__ void mac(T (&acc)[NC], const T (&mc)[NC], T v) {
+  if constexpr (FIRST) {
+    mm_scaling<T, NC>(mc, v, acc);
+  } else {
+    T term[NC];
+    mm_scaling<T, NC>(mc, v, term);
+    mm_add<T, NC>(acc, term, acc);
+  }
+}
+
+// One reduction step kk of the LDS tiles for the TM x TN outputs of a lane.
+template <typename T, int NC, bool AMC, bool BMC, int TM, int TN, int KT, int BM, int BN, bool FIRST>
+__device__ __forceinline__ void step(const T (*As)[KT][BM], const T (*Bs)[KT][BN], int kk, int tx, int ty,
+                                     T (&acc)[(AMC && BMC) ? NC : 1][TM][TN][NC]) {
+  constexpr int NA = AMC ? NC : 1;
+  constexpr int NB = BMC ? NC : 1;
+  constexpr int NP = (AMC && BMC) ? NC : 1;
+  T a[TM][NA], b[TN][NB];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int c = 0; c < NA; ++c) a[i][c] = As[c][kk][ty * TM + i];
+#pragma unroll
+  for (int j = 0; j < TN; ++j)
+#pragma unroll
+    for (int c = 0; c < NB; ++c) b[j][c] = Bs[c][kk][tx * TN + j];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      if constexpr (AMC && BMC) {
+#pragma unroll
+        for (int p = 0; p < NP; ++p) mac<T, NC, FIRST>(acc[p][i][j], a[i], b[j][p]);
+      } else if constexpr (AMC) {
+        mac<T, NC, FIRST>(acc[0][i][j], a[i], b[j][0]);
+      } else {
+        mac<T, NC, FIRST>(acc[0][i][j], b[j], a[i][0]);
+      }
+    }
 }
 
 // A: [NA][M][K] row-major planes.  B: [NB][K][N] (BT = false) or [NB][N][K] (BT =
@@ -81,31 +174,12 @@ __global__ __launch_bounds__(MM_THREADS) void mm_kernel(const T *__restrict__ A,
       }
     }
     __syncthreads();
-    for (int kk = 0; kk < kt; ++kk) {
-      const bool first = (k0 + kk) == 0;
-      T a[TM][NA], b[TN][NB];
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int c = 0; c < NA; ++c) a[i][c] = As[c][kk][ty * TM + i];
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-#pragma unroll
-        for (int c = 0; c < NB; ++c) b[j][c] = Bs[c][kk][tx * TN + j];
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          if constexpr (AMC && BMC) {
-#pragma unroll
-            for (int p = 0; p < NP; ++p) mac<T, NC>(acc[p][i][j], a[i], b[j][p], first);
-          } else if constexpr (AMC) {
-            mac<T, NC>(acc[0][i][j], a[i], b[j][0], first);
-          } else {
-            mac<T, NC>(acc[0][i][j], b[j], a[i][0], first);
-          }
-        }
+    int kk0 = 0;
+    if (k0 == 0) {  // term k = 0 initialises the accumulators
+      step<T, NC, AMC, BMC, TM, TN, KT, BM, BN, true>(As, Bs, 0, tx, ty, acc);
+      kk0 = 1;
     }
+    for (int kk = kk0; kk < kt; ++kk) step<T, NC, AMC, BMC, TM, TN, KT, BM, BN, false>(As, Bs, kk, tx, ty, acc);
     __syncthreads();
   }
 
@@ -123,14 +197,14 @@ __global__ __launch_bounds__(MM_THREADS) void mm_kernel(const T *__restrict__ A,
         for (int c = 0; c < NC; ++c) r[c] = acc[0][i][j][c];
         // MC x MC: combine the per-component products left to right
 #pragma unroll
-        for (int p = 1; p < NP; ++p) add_mcn<T, NC>(r, acc[p][i][j], r);
+        for (int p = 1; p < NP; ++p) mm_add<T, NC>(r, acc[p][i][j], r);
       }
       if (gm < M && gn < N) {
         if (bias != nullptr) {
           T bv[NC];
 #pragma unroll
           for (int c = 0; c < NC; ++c) bv[c] = bias[c * N + gn];
-          add_mcn<T, NC>(r, bv, r);
+          mm_add<T, NC>(r, bv, r);
         }
 #pragma unroll
         for (int c = 0; c < NC; ++c) C[c * M * N + gm * N + gn] = r[c];
