@@ -42,13 +42,20 @@ def log(*a):
 
 
 def algo_ops_per_mac(nc: int, mc_x_mc: bool) -> int:
-    """VALU arithmetic operations the algorithm needs per multiply-add: ScalingN is
-    mul + fma on component 0 and mul + fma + Two-Sum (6) + carry add on the others;
-    Add-MCN is Two-Sum on component 0 and two Two-Sums + carry add on the others (the
-    first Two-Sum with the zero carry is an identity and is not counted).  MC x MC
-    repeats this for each of the nc components of B.  Simple-Renorm selects are not
-    counted."""
-    per = (2 + 9 * (nc - 1)) + (6 + 13 * (nc - 1))
+    """Floating-point operations of the algorithm that determine the result, per
+    multiply-add, on the common path where Simple-Renorm keeps the first nc terms and
+    drops the final carry (whose computation is then not needed):
+      ScalingN: component 0: mul + fma; components 1..nc-2: mul + fma + Two-Sum (6)
+                + carry add; component nc-1: mul + add (the kept sum only);
+      Add-MCN:  component 0: Two-Sum (6; the Two-Sum with the zero carry is an
+                identity); components 1..nc-2: two Two-Sums + carry add (13);
+                component nc-1: add + add.
+    nc = 1: one mul, one add.  MC x MC repeats this for each component of B.
+    Zero checks, selects, loads and loop control are overhead, not counted."""
+    if nc == 1:
+        per = 2
+    else:
+        per = (2 + 9 * (nc - 2) + 2) + (6 + 13 * (nc - 2) + 2)
     return per * (nc if mc_x_mc else 1)
 
 

@@ -35,24 +35,58 @@ constexpr int MM_THREADS = 256;
 //     compaction runs only in lanes where a leading term is zero.
 // ---------------------------------------------------------------------------------
 
-template <typename T, int N>
-__device__ __forceinline__ void sr_fast(const T (&h)[N + 1], T (&out)[N]) {
-  if constexpr (N == 1) {
-    out[0] = (h[0] != T(0)) ? h[0] : h[1];
+// True when every one of v[0..K-1] is non-zero: min(|v_i|) != 0.  (A NaN is
+// non-zero and min ignores it unless all are NaN, which is non-zero too.)
+template <typename T, int K>
+__device__ __forceinline__ bool all_nonzero(const T (&v)[K]) {
+  static_assert(K >= 1 && K <= 4, "");
+  if constexpr (K == 1) {
+    return v[0] != T(0);
+  } else if constexpr (K == 2) {
+    return __builtin_fminf((float)__builtin_fabsf((float)v[0]), __builtin_fabsf((float)v[1])) != 0.0f;
   } else {
-    bool lead = true;
-#pragma unroll
-    for (int i = 0; i < N - 1; ++i) lead = lead && (h[i] != T(0));
-#pragma unroll
-    for (int i = 0; i < N - 1; ++i) out[i] = h[i];
-    out[N - 1] = (h[N - 1] != T(0)) ? h[N - 1] : h[N];
-    if (__builtin_expect(!lead, 0)) simple_renorm<T, N + 1, N>(h, out);
+    T m = __builtin_fminf(__builtin_fminf(__builtin_fabsf((float)v[0]), __builtin_fabsf((float)v[1])),
+                          __builtin_fabsf((float)v[2]));
+    if constexpr (K == 4) return __builtin_fminf(m, __builtin_fabsf((float)v[3])) != 0.0f;
+    return m != T(0);
   }
 }
 
-// ScalingN(x, v) without expand.
+// FULL = true: the fast path needs all of h_0 .. h_{nc-1} non-zero and then keeps
+// them, so the dropped h_nc is never needed there (binary32 data, where a zero term
+// is rare).  FULL = false: it needs only h_0 .. h_{nc-2} and selects the first
+// non-zero of h_{nc-1}, h_nc (binary16 data, where the last component is often
+// below the subnormal grid).  `ok` admits lanes whose h is known to be all zero: the
+// fast path then returns zeros, which is Simple-Renorm's result up to zero signs.
+template <typename T, int N, bool FULL>
+__device__ __forceinline__ void sr_fast(const T (&h)[N + 1], T (&out)[N], bool ok = false) {
+  if constexpr (N == 1) {
+    out[0] = (h[0] != T(0)) ? h[0] : h[1];
+  } else {
+    constexpr int NCHK = FULL ? N : N - 1;
+    T lead[NCHK];
+#pragma unroll
+    for (int i = 0; i < NCHK; ++i) lead[i] = h[i];
+    const bool fast = ok || all_nonzero<T, NCHK>(lead);
+#pragma unroll
+    for (int i = 0; i < N - 1; ++i) out[i] = h[i];
+    if constexpr (FULL)
+      out[N - 1] = h[N - 1];
+    else
+      out[N - 1] = (h[N - 1] != T(0)) ? h[N - 1] : h[N];
+    if (__builtin_expect(!fast, 0)) simple_renorm<T, N + 1, N>(h, out);
+  }
+}
+
+// Full checks pay off for binary32, the select for binary16.
+template <typename T>
+constexpr bool sr_full() {
+  return sizeof(T) == 4;
+}
+
+// ScalingN(x, v) without expand.  vzero: v is +-0, so every term is zero (finite x).
 template <typename T, int N>
-__device__ __forceinline__ void mm_scaling(const T (&x)[N], T v, T (&out)[N]) {
+__device__ __forceinline__ void mm_scaling(const T (&x)[N], T v, T (&out)[N], bool vzero) {
   T h[N + 1];
   T e;
   two_prod(x[0], v, h[0], e);
@@ -64,7 +98,7 @@ __device__ __forceinline__ void mm_scaling(const T (&x)[N], T v, T (&out)[N]) {
     e = e1 + e2;
   }
   h[N] = e;
-  sr_fast<T, N>(h, out);
+  sr_fast<T, N, sr_full<T>()>(h, out, vzero);
 }
 
 // Add-MCN(x, y).
@@ -81,20 +115,27 @@ __device__ __forceinline__ void mm_add(const T (&x)[N], const T (&y)[N], T (&out
     e = e1 + e2;
   }
   h[N] = e;
-  sr_fast<T, N>(h, out);
+  sr_fast<T, N, sr_full<T>()>(h, out);
 }
 
 // acc = ScalingN(mc, v) (first term) or acc = Add-MCN(acc, ScalingN(mc, v)).
 template <typename T, int NC, bool FIRST>
-__device__ __forceinline__ void mac(T (&acc)[NC], const T (&mc)[NC], T v) {
+__device__ __forceinline__ void mac(T (&acc)[NC], const T (&mc)[NC], T v, bool vzero) {
   if constexpr (FIRST) {
-    mm_scaling<T, NC>(mc, v, acc);
+    mm_scaling<T, NC>(mc, v, acc, vzero);
   } else {
     T term[NC];
-    mm_scaling<T, NC>(mc, v, term);
+    mm_scaling<T, NC>(mc, v, term, vzero);
     mm_add<T, NC>(acc, term, acc);
   }
 }
+
+// A term whose plain factor is +-0 in every active lane of the wave is skipped by the
+// whole wave: ScalingN then returns (+0, ..., +0) and Add-MCN(acc, (+0, ..., +0))
+// returns acc unchanged, because acc is already a Simple-Renorm output (non-zeros
+// first, zeros after).  (binary16 MC operands often carry a last component that is
+// zero everywhere.)
+__device__ __forceinline__ bool wave_none(bool lane_flag) { return __builtin_amdgcn_ballot_w64(lane_flag) == 0; }
 
 // One reduction step kk of the LDS tiles for the TM x TN outputs of a lane.
 template <typename T, int NC, bool AMC, bool BMC, int TM, int TN, int KT, int BM, int BN, bool FIRST>
@@ -118,11 +159,16 @@ __device__ __forceinline__ void step(const T (*As)[KT][BM], const T (*Bs)[KT][BN
     for (int j = 0; j < TN; ++j) {
       if constexpr (AMC && BMC) {
 #pragma unroll
-        for (int p = 0; p < NP; ++p) mac<T, NC, FIRST>(acc[p][i][j], a[i], b[j][p]);
+        for (int p = 0; p < NP; ++p) {
+          const bool vz = b[j][p] == T(0);
+          if (FIRST || !wave_none(!vz)) mac<T, NC, FIRST>(acc[p][i][j], a[i], b[j][p], vz);
+        }
       } else if constexpr (AMC) {
-        mac<T, NC, FIRST>(acc[0][i][j], a[i], b[j][0]);
+        const bool vz = b[j][0] == T(0);
+        if (FIRST || !wave_none(!vz)) mac<T, NC, FIRST>(acc[0][i][j], a[i], b[j][0], vz);
       } else {
-        mac<T, NC, FIRST>(acc[0][i][j], b[j], a[i][0]);
+        const bool vz = a[i][0] == T(0);
+        if (FIRST || !wave_none(!vz)) mac<T, NC, FIRST>(acc[0][i][j], b[j], a[i][0], vz);
       }
     }
 }
@@ -206,8 +252,10 @@ __global__ __launch_bounds__(MM_THREADS) void mm_kernel(const T *__restrict__ A,
           for (int c = 0; c < NC; ++c) bv[c] = bias[c * N + gn];
           mm_add<T, NC>(r, bv, r);
         }
+        // Zero components leave as +0, the padding Simple-Renorm writes (a zero term
+        // that was skipped or selected above may carry the sign of -0).
 #pragma unroll
-        for (int c = 0; c < NC; ++c) C[c * M * N + gm * N + gn] = r[c];
+        for (int c = 0; c < NC; ++c) C[c * M * N + gm * N + gn] = (r[c] != T(0)) ? r[c] : T(0);
       }
     }
 }
