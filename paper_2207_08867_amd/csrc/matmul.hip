@@ -26,14 +26,35 @@ constexpr int MM_THREADS = 256;
 // The two steps of one MM-MCN term, in the form the product kernel executes them.
 //
 // They compute exactly what scaling_n / add_mcn of mcf_arith.hpp compute on finite,
-// non-overflowing data, with two shortcuts that change nothing but the sign of a
-// zero term, and zero terms are all dropped by Simple-Renorm (which pads with +0):
+// non-overflowing data.  The shortcuts below change nothing but the sign of zero
+// terms, and zero terms are all dropped by Simple-Renorm; the kernel writes every
+// zero output component as +0, Simple-Renorm's padding, so the results are
+// bit-identical:
 //   * the first Two-Sum of each step adds the initial carry +0: Two-Sum(h, +0) =
 //     (h + 0, +0), so h_0 is the first product (resp. sum) and the carry its error;
-//   * Simple-Renorm of nc+1 terms keeps h_0 .. h_{nc-2} unchanged when they are all
-//     non-zero and then only chooses between h_{nc-1} and h_nc; the general
-//     compaction runs only in lanes where a leading term is zero.
+//   * Simple-Renorm of the nc+1 terms takes a fast path chosen by a policy (below);
+//     lanes that miss it run the general compaction in a divergent block shared by
+//     all the terms of a reduction step, so the arithmetic of the independent terms
+//     stays in one straight-line block the compiler can interleave.
 // ---------------------------------------------------------------------------------
+
+// First R non-zero entries of v[0..M-1], in order; the remaining slots hold zeros
+// of either sign.  Built back to front: after visiting v[i..M-1], out is the
+// compaction of that suffix, and prepending a non-zero v[i] shifts it by one slot.
+template <typename T, int M, int R>
+__device__ __forceinline__ void compact_nz(const T (&v)[M], T (&out)[R]) {
+  out[0] = v[M - 1];
+#pragma unroll
+  for (int r = 1; r < R; ++r) out[r] = T(0);
+#pragma unroll
+  for (int i = M - 2; i >= 0; --i) {
+    const bool nz = v[i] != T(0);
+    const int top = (M - 1 - i) < R - 1 ? (M - 1 - i) : R - 1;  // slots that can hold a value
+#pragma unroll
+    for (int r = top; r >= 1; --r) out[r] = nz ? out[r - 1] : out[r];
+    out[0] = nz ? v[i] : out[0];
+  }
+}
 
 // True when every one of v[0..K-1] is non-zero: min(|v_i|) != 0.  (A NaN is
 // non-zero and min ignores it unless all are NaN, which is non-zero too.)
@@ -43,7 +64,7 @@ __device__ __forceinline__ bool all_nonzero(const T (&v)[K]) {
   if constexpr (K == 1) {
     return v[0] != T(0);
   } else if constexpr (K == 2) {
-    return __builtin_fminf((float)__builtin_fabsf((float)v[0]), __builtin_fabsf((float)v[1])) != 0.0f;
+    return __builtin_fminf(__builtin_fabsf((float)v[0]), __builtin_fabsf((float)v[1])) != 0.0f;
   } else {
     T m = __builtin_fminf(__builtin_fminf(__builtin_fabsf((float)v[0]), __builtin_fabsf((float)v[1])),
                           __builtin_fabsf((float)v[2]));
@@ -52,42 +73,55 @@ __device__ __forceinline__ bool all_nonzero(const T (&v)[K]) {
   }
 }
 
-// FULL = true: the fast path needs all of h_0 .. h_{nc-1} non-zero and then keeps
-// them, so the dropped h_nc is never needed there (binary32 data, where a zero term
-// is rare).  FULL = false: it needs only h_0 .. h_{nc-2} and selects the first
-// non-zero of h_{nc-1}, h_nc (binary16 data, where the last component is often
-// below the subnormal grid).  `ok` admits lanes whose h is known to be all zero: the
-// fast path then returns zeros, which is Simple-Renorm's result up to zero signs.
-template <typename T, int N, bool FULL>
-__device__ __forceinline__ void sr_fast(const T (&h)[N + 1], T (&out)[N], bool ok = false) {
+// Simple-Renorm fast paths for the nc+1 terms h of a step:
+//   SR_FULL:   valid when h_0 .. h_{nc-1} are all non-zero: keep them; the dropped h_nc
+//              is then never needed (binary32 data, where a zero term is rare);
+//   SR_SELECT: valid when h_0 .. h_{nc-2} are non-zero: keep them and take the first
+//              non-zero of h_{nc-1}, h_nc;
+//   SR_HEAD:   valid when h_0 is non-zero: keep it and compact h_1 .. h_nc into the
+//              other nc-1 slots without branching (binary16 data, where the low terms
+//              of a step often fall below the subnormal grid);
+//   SR_NET:    always valid: the general compaction without a branch.
+// sr_try writes the fast-path result and returns true when the lane needs the general
+// compaction instead.  `ok` marks lanes whose terms are known to be all zero: any
+// fast-path result is then correct up to zero signs.
+enum SrPolicy { SR_FULL = 0, SR_SELECT = 1, SR_HEAD = 2, SR_NET = 3 };
+
+template <typename T, int N, int POL>
+__device__ __forceinline__ bool sr_try(const T (&h)[N + 1], T (&out)[N], bool ok = false) {
   if constexpr (N == 1) {
     out[0] = (h[0] != T(0)) ? h[0] : h[1];
+    return false;
+  } else if constexpr (POL == SR_NET) {
+    compact_nz<T, N + 1, N>(h, out);
+    return false;
+  } else if constexpr (POL == SR_HEAD) {
+    out[0] = h[0];
+    T tail_in[N], tail_out[N - 1];
+#pragma unroll
+    for (int i = 0; i < N; ++i) tail_in[i] = h[i + 1];
+    compact_nz<T, N, N - 1>(tail_in, tail_out);
+#pragma unroll
+    for (int i = 1; i < N; ++i) out[i] = tail_out[i - 1];
+    return !(ok || h[0] != T(0));
   } else {
-    constexpr int NCHK = FULL ? N : N - 1;
+    constexpr int NCHK = (POL == SR_FULL) ? N : N - 1;
     T lead[NCHK];
 #pragma unroll
     for (int i = 0; i < NCHK; ++i) lead[i] = h[i];
-    const bool fast = ok || all_nonzero<T, NCHK>(lead);
 #pragma unroll
     for (int i = 0; i < N - 1; ++i) out[i] = h[i];
-    if constexpr (FULL)
+    if constexpr (POL == SR_FULL)
       out[N - 1] = h[N - 1];
     else
       out[N - 1] = (h[N - 1] != T(0)) ? h[N - 1] : h[N];
-    if (__builtin_expect(!fast, 0)) simple_renorm<T, N + 1, N>(h, out);
+    return !(ok || all_nonzero<T, NCHK>(lead));
   }
 }
 
-// Full checks pay off for binary32, the select for binary16.
-template <typename T>
-constexpr bool sr_full() {
-  return sizeof(T) == 4;
-}
-
-// ScalingN(x, v) without expand.  vzero: v is +-0, so every term is zero (finite x).
+// The nc+1 terms of ScalingN(x, v) (before Simple-Renorm).
 template <typename T, int N>
-__device__ __forceinline__ void mm_scaling(const T (&x)[N], T v, T (&out)[N], bool vzero) {
-  T h[N + 1];
+__device__ __forceinline__ void scaling_terms(const T (&x)[N], T v, T (&h)[N + 1]) {
   T e;
   two_prod(x[0], v, h[0], e);
 #pragma unroll
@@ -98,13 +132,11 @@ __device__ __forceinline__ void mm_scaling(const T (&x)[N], T v, T (&out)[N], bo
     e = e1 + e2;
   }
   h[N] = e;
-  sr_fast<T, N, sr_full<T>()>(h, out, vzero);
 }
 
-// Add-MCN(x, y).
+// The nc+1 terms of Add-MCN(x, y) (before Simple-Renorm).
 template <typename T, int N>
-__device__ __forceinline__ void mm_add(const T (&x)[N], const T (&y)[N], T (&out)[N]) {
-  T h[N + 1];
+__device__ __forceinline__ void add_terms(const T (&x)[N], const T (&y)[N], T (&h)[N + 1]) {
   T e;
   two_sum(x[0], y[0], h[0], e);
 #pragma unroll
@@ -115,67 +147,168 @@ __device__ __forceinline__ void mm_add(const T (&x)[N], const T (&y)[N], T (&out
     e = e1 + e2;
   }
   h[N] = e;
-  sr_fast<T, N, sr_full<T>()>(h, out);
 }
 
-// acc = ScalingN(mc, v) (first term) or acc = Add-MCN(acc, ScalingN(mc, v)).
-template <typename T, int NC, bool FIRST>
-__device__ __forceinline__ void mac(T (&acc)[NC], const T (&mc)[NC], T v, bool vzero) {
-  if constexpr (FIRST) {
-    mm_scaling<T, NC>(mc, v, acc, vzero);
-  } else {
-    T term[NC];
-    mm_scaling<T, NC>(mc, v, term, vzero);
-    mm_add<T, NC>(acc, term, acc);
-  }
+// out = Add-MCN(x, y) for one value (the epilogue's combinations).
+template <typename T, int N, int POL>
+__device__ __forceinline__ void mm_add(const T (&x)[N], const T (&y)[N], T (&out)[N]) {
+  T h[N + 1];
+  add_terms<T, N>(x, y, h);
+  if (sr_try<T, N, POL>(h, out)) compact_nz<T, N + 1, N>(h, out);
 }
 
-// A term whose plain factor is +-0 in every active lane of the wave is skipped by the
-// whole wave: ScalingN then returns (+0, ..., +0) and Add-MCN(acc, (+0, ..., +0))
-// returns acc unchanged, because acc is already a Simple-Renorm output (non-zeros
-// first, zeros after).  (binary16 MC operands often carry a last component that is
-// zero everywhere.)
-__device__ __forceinline__ bool wave_none(bool lane_flag) { return __builtin_amdgcn_ballot_w64(lane_flag) == 0; }
-
-// One reduction step kk of the LDS tiles for the TM x TN outputs of a lane.
-template <typename T, int NC, bool AMC, bool BMC, int TM, int TN, int KT, int BM, int BN, bool FIRST>
-__device__ __forceinline__ void step(const T (*As)[KT][BM], const T (*Bs)[KT][BN], int kk, int tx, int ty,
-                                     T (&acc)[(AMC && BMC) ? NC : 1][TM][TN][NC]) {
-  constexpr int NA = AMC ? NC : 1;
-  constexpr int NB = BMC ? NC : 1;
-  constexpr int NP = (AMC && BMC) ? NC : 1;
+// The operands of reduction step kk of the LDS tiles for the TM x TN outputs of a
+// lane: the A values of its rows, the B values of its columns (all components).
+template <typename T, int NA, int NB, int TM, int TN, int KT, int BM, int BN>
+struct Operands {
   T a[TM][NA], b[TN][NB];
+  __device__ __forceinline__ void load(const T (*As)[KT][BM], const T (*Bs)[KT][BN], int kk, int tx, int ty) {
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int c = 0; c < NA; ++c) a[i][c] = As[c][kk][ty * TM + i];
+      for (int c = 0; c < NA; ++c) a[i][c] = As[c][kk][ty * TM + i];
 #pragma unroll
-  for (int j = 0; j < TN; ++j)
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
-    for (int c = 0; c < NB; ++c) b[j][c] = Bs[c][kk][tx * TN + j];
+      for (int c = 0; c < NB; ++c) b[j][c] = Bs[c][kk][tx * TN + j];
+  }
+};
+
+// Per-lane state of the product: the accumulators of every (component p of B, row i,
+// column j) the lane owns.  PMASK selects the components p of B that take part
+// (MC x MC; bit p clear: B^(p) is zero across the whole tile, so the term is skipped
+// -- ScalingN gives zeros and Add-MCN(acc, zeros) returns acc, a Simple-Renorm output,
+// unchanged).  GROUP = false: each term's general-compaction branch follows its own
+// arithmetic; GROUP = true: the arithmetic of all terms of a step shares one
+// straight-line block and one (rarely taken) compaction branch.
+template <typename T, int NC, bool AMC, bool BMC, int TM, int TN, int KT, int BM, int BN, int SPOL, int APOL,
+          bool GROUP>
+struct Lane {
+  static constexpr int NA = AMC ? NC : 1;
+  static constexpr int NB = BMC ? NC : 1;
+  static constexpr int NP = (AMC && BMC) ? NC : 1;
+  using Ops = Operands<T, NA, NB, TM, TN, KT, BM, BN>;
+  T acc[NP][TM][TN][NC];
+
+  // dst = ScalingN terms of step o (FIRST: into acc)
+  template <int PMASK>
+  __device__ __forceinline__ void scale(const Ops &o, T (&dst)[NP][TM][TN][NC]) {
+    T hs[NP][TM][TN][NC + 1];
+    bool slow[NP][TM][TN];
+    bool any = false;
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
+    for (int p = 0; p < NP; ++p) {
+      if (!((PMASK >> p) & 1)) continue;
 #pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      if constexpr (AMC && BMC) {
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const T v = AMC ? o.b[j][p] : o.a[i][0];
+          if constexpr (AMC)
+            scaling_terms<T, NC>(o.a[i], v, hs[p][i][j]);
+          else
+            scaling_terms<T, NC>(o.b[j], v, hs[p][i][j]);
+          slow[p][i][j] = sr_try<T, NC, SPOL>(hs[p][i][j], dst[p][i][j], v == T(0));
+          if constexpr (GROUP)
+            any = any || slow[p][i][j];
+          else if (__builtin_expect(slow[p][i][j], 0))
+            compact_nz<T, NC + 1, NC>(hs[p][i][j], dst[p][i][j]);
+        }
+    }
+    if constexpr (GROUP) {
+      if (__builtin_expect(any, 0)) {
 #pragma unroll
         for (int p = 0; p < NP; ++p) {
-          const bool vz = b[j][p] == T(0);
-          if (FIRST || !wave_none(!vz)) mac<T, NC, FIRST>(acc[p][i][j], a[i], b[j][p], vz);
+          if (!((PMASK >> p) & 1)) continue;
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+              if (slow[p][i][j]) compact_nz<T, NC + 1, NC>(hs[p][i][j], dst[p][i][j]);
         }
-      } else if constexpr (AMC) {
-        const bool vz = b[j][0] == T(0);
-        if (FIRST || !wave_none(!vz)) mac<T, NC, FIRST>(acc[0][i][j], a[i], b[j][0], vz);
-      } else {
-        const bool vz = a[i][0] == T(0);
-        if (FIRST || !wave_none(!vz)) mac<T, NC, FIRST>(acc[0][i][j], b[j], a[i][0], vz);
       }
     }
-}
+  }
+
+  // acc = Add-MCN(acc, term) for every term
+  template <int PMASK>
+  __device__ __forceinline__ void add(const T (&term)[NP][TM][TN][NC]) {
+    T ha[NP][TM][TN][NC + 1];
+    bool slow[NP][TM][TN];
+    bool any = false;
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      if (!((PMASK >> p) & 1)) continue;
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          add_terms<T, NC>(acc[p][i][j], term[p][i][j], ha[p][i][j]);
+          slow[p][i][j] = sr_try<T, NC, APOL>(ha[p][i][j], acc[p][i][j]);
+          if constexpr (GROUP)
+            any = any || slow[p][i][j];
+          else if (__builtin_expect(slow[p][i][j], 0))
+            compact_nz<T, NC + 1, NC>(ha[p][i][j], acc[p][i][j]);
+        }
+    }
+    if constexpr (GROUP) {
+      if (__builtin_expect(any, 0)) {
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+          if (!((PMASK >> p) & 1)) continue;
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+              if (slow[p][i][j]) compact_nz<T, NC + 1, NC>(ha[p][i][j], acc[p][i][j]);
+        }
+      }
+    }
+  }
+
+  // term k = 0 initialises the accumulators
+  __device__ __forceinline__ void first(const Ops &o) { scale<(1 << NP) - 1>(o, acc); }
+
+  // steps kk0 .. kt-1 of a tile.  GROUP = false: each term's ScalingN and Add-MCN run
+  // back to back, so only one term is live at a time.
+  template <int PMASK>
+  __device__ __forceinline__ void run(const T (*As)[KT][BM], const T (*Bs)[KT][BN], int kk0, int kt, int tx,
+                                      int ty) {
+    for (int kk = kk0; kk < kt; ++kk) {
+      Ops o;
+      o.load(As, Bs, kk, tx, ty);
+      if constexpr (GROUP) {
+        T term[NP][TM][TN][NC];
+        scale<PMASK>(o, term);
+        add<PMASK>(term);
+      } else {
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+          if (!((PMASK >> p) & 1)) continue;
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+              const T v = AMC ? o.b[j][p] : o.a[i][0];
+              T h[NC + 1], term[NC];
+              if constexpr (AMC)
+                scaling_terms<T, NC>(o.a[i], v, h);
+              else
+                scaling_terms<T, NC>(o.b[j], v, h);
+              if (__builtin_expect(sr_try<T, NC, SPOL>(h, term, v == T(0)), 0)) compact_nz<T, NC + 1, NC>(h, term);
+              add_terms<T, NC>(acc[p][i][j], term, h);
+              if (__builtin_expect(sr_try<T, NC, APOL>(h, acc[p][i][j]), 0)) compact_nz<T, NC + 1, NC>(h, acc[p][i][j]);
+            }
+        }
+      }
+    }
+  }
+};
 
 // A: [NA][M][K] row-major planes.  B: [NB][K][N] (BT = false) or [NB][N][K] (BT =
 // true).  NA = NC when A is MC else 1, likewise NB.
-template <typename T, int NC, bool AMC, bool BMC, bool BT, int TM, int TN, int KT>
+template <typename T, int NC, bool AMC, bool BMC, bool BT, int TM, int TN, int KT, int SPOL, int APOL,
+          bool GROUP>
 __global__ __launch_bounds__(MM_THREADS) void mm_kernel(const T *__restrict__ A, const T *__restrict__ B,
                                                         const T *__restrict__ bias, T *__restrict__ C, int64_t M,
                                                         int64_t N, int64_t K) {
@@ -183,14 +316,16 @@ __global__ __launch_bounds__(MM_THREADS) void mm_kernel(const T *__restrict__ A,
   constexpr int NB = BMC ? NC : 1;
   constexpr int TX = 16, TY = 16;  // lanes along N and along M
   constexpr int BM = TY * TM, BN = TX * TN;
-  constexpr int NP = (AMC && BMC) ? NC : 1;  // plain components to sweep (MC x MC)
+  constexpr int NP = (AMC && BMC) ? NC : 1;  // components of B swept (MC x MC)
+  constexpr int ALL = (1 << NP) - 1;
   __shared__ T As[NA][KT][BM];
   __shared__ T Bs[NB][KT][BN];
 
   const int tx = threadIdx.x % TX, ty = threadIdx.x / TX;
   const int64_t m0 = (int64_t)blockIdx.y * BM, n0 = (int64_t)blockIdx.x * BN;
 
-  T acc[NP][TM][TN][NC];
+  Lane<T, NC, AMC, BMC, TM, TN, KT, BM, BN, SPOL, APOL, GROUP> lane;
+  auto &acc = lane.acc;
 
   for (int64_t k0 = 0; k0 < K; k0 += KT) {
     const int kt = (int)((K - k0) < KT ? (K - k0) : KT);
@@ -202,6 +337,8 @@ __global__ __launch_bounds__(MM_THREADS) void mm_kernel(const T *__restrict__ A,
 #pragma unroll
       for (int c = 0; c < NA; ++c) As[c][kk][r] = ok ? A[c * M * K + gm * K + gk] : T(0);
     }
+    // stage B tile, noting which of its component planes hold a non-zero value
+    int nonzero_planes = 0;
     for (int idx = threadIdx.x; idx < BN * KT; idx += MM_THREADS) {
       int col, kk;
       if constexpr (BT) {
@@ -216,16 +353,29 @@ __global__ __launch_bounds__(MM_THREADS) void mm_kernel(const T *__restrict__ A,
 #pragma unroll
       for (int c = 0; c < NB; ++c) {
         const int64_t off = BT ? (c * N * K + gn * K + gk) : (c * K * N + gk * N + gn);
-        Bs[c][kk][col] = ok ? B[off] : T(0);
+        const T v = ok ? B[off] : T(0);
+        Bs[c][kk][col] = v;
+        if (v != T(0)) nonzero_planes |= 1 << c;
       }
     }
-    __syncthreads();
+    int pmask = ALL;
+    if constexpr (AMC && BMC) {
+      // the last component plane of B is often zero throughout a tile (binary16)
+      pmask = __syncthreads_or(nonzero_planes & (1 << (NP - 1))) ? ALL : (ALL >> 1);
+    } else {
+      __syncthreads();
+    }
     int kk0 = 0;
     if (k0 == 0) {  // term k = 0 initialises the accumulators
-      step<T, NC, AMC, BMC, TM, TN, KT, BM, BN, true>(As, Bs, 0, tx, ty, acc);
+      typename decltype(lane)::Ops o;
+      o.load(As, Bs, 0, tx, ty);
+      lane.first(o);
       kk0 = 1;
     }
-    for (int kk = kk0; kk < kt; ++kk) step<T, NC, AMC, BMC, TM, TN, KT, BM, BN, false>(As, Bs, kk, tx, ty, acc);
+    if (NP > 1 && pmask != ALL)
+      lane.template run<(ALL >> 1)>(As, Bs, kk0, kt, tx, ty);
+    else
+      lane.template run<ALL>(As, Bs, kk0, kt, tx, ty);
     __syncthreads();
   }
 
@@ -243,14 +393,14 @@ __global__ __launch_bounds__(MM_THREADS) void mm_kernel(const T *__restrict__ A,
         for (int c = 0; c < NC; ++c) r[c] = acc[0][i][j][c];
         // MC x MC: combine the per-component products left to right
 #pragma unroll
-        for (int p = 1; p < NP; ++p) mm_add<T, NC>(r, acc[p][i][j], r);
+        for (int p = 1; p < NP; ++p) mm_add<T, NC, APOL>(r, acc[p][i][j], r);
       }
       if (gm < M && gn < N) {
         if (bias != nullptr) {
           T bv[NC];
 #pragma unroll
           for (int c = 0; c < NC; ++c) bv[c] = bias[c * N + gn];
-          mm_add<T, NC>(r, bv, r);
+          mm_add<T, NC, APOL>(r, bv, r);
         }
         // Zero components leave as +0, the padding Simple-Renorm writes (a zero term
         // that was skipped or selected above may carry the sign of -0).
@@ -260,15 +410,33 @@ __global__ __launch_bounds__(MM_THREADS) void mm_kernel(const T *__restrict__ A,
     }
 }
 
+template <typename T, int NC, bool AMC, bool BMC, bool BT, int TM, int TN, int SPOL, int APOL>
+static hipError_t mm_launch_tile(int64_t M, int64_t N, int64_t K, const void *A, const void *B, const void *bias,
+                                 void *C, hipStream_t s) {
+  constexpr int KT = 16;
+  constexpr int BM = 16 * TM, BN = 16 * TN;
+  dim3 grid((unsigned)((N + BN - 1) / BN), (unsigned)((M + BM - 1) / BM));
+  hipLaunchKernelGGL((mm_kernel<T, NC, AMC, BMC, BT, TM, TN, KT, SPOL, APOL, false>), grid, dim3(MM_THREADS), 0, s,
+                     (const T *)A, (const T *)B, (const T *)bias, (T *)C, M, N, K);
+  return hipGetLastError();
+}
+
+// Launch shape and Simple-Renorm policies (measured on the product workloads):
+//   binary32: every kept term is non-zero almost always -> SR_FULL for both steps;
+//             two outputs per lane once the output has 2^25 entries or more, else one;
+//   binary16: one output per lane; ScalingN terms of low components underflow often ->
+//             SR_HEAD (nc >= 3) or the branch-free network (nc = 2); Add-MCN -> SR_SELECT.
 template <typename T, int NC, bool AMC, bool BMC, bool BT>
 static hipError_t mm_launch(int64_t M, int64_t N, int64_t K, const void *A, const void *B, const void *bias,
                             void *C, hipStream_t s) {
-  constexpr int TM = 2, TN = 2, KT = 16;
-  constexpr int BM = 16 * TM, BN = 16 * TN;
-  dim3 grid((unsigned)((N + BN - 1) / BN), (unsigned)((M + BM - 1) / BM));
-  hipLaunchKernelGGL((mm_kernel<T, NC, AMC, BMC, BT, TM, TN, KT>), grid, dim3(MM_THREADS), 0, s, (const T *)A,
-                     (const T *)B, (const T *)bias, (T *)C, M, N, K);
-  return hipGetLastError();
+  if constexpr (sizeof(T) == 4) {
+    if (M * N >= ((int64_t)1 << 25))
+      return mm_launch_tile<T, NC, AMC, BMC, BT, 1, 2, SR_FULL, SR_FULL>(M, N, K, A, B, bias, C, s);
+    return mm_launch_tile<T, NC, AMC, BMC, BT, 1, 1, SR_FULL, SR_FULL>(M, N, K, A, B, bias, C, s);
+  } else {
+    constexpr int SPOL = NC == 2 ? SR_NET : SR_HEAD;
+    return mm_launch_tile<T, NC, AMC, BMC, BT, 1, 1, SPOL, SR_SELECT>(M, N, K, A, B, bias, C, s);
+  }
 }
 
 template <typename T, int NC>
