@@ -298,16 +298,46 @@ __device__ __forceinline__ void exp_chain(const _Float16 (&h)[M], const _Float16
   }
 }
 
-// One workgroup per CU holds the whole 128 KiB table in LDS; elements are looked up
-// by their bit pattern.
+// The LDS copy of the table covers |x| < 32 (exponent fields 0..19 of both signs, 80
+// KiB); outside it e^x is +inf (x >= 32), +0 (x <= -32) or NaN, which is what the
+// full table holds there.
+constexpr int EXP_LDS_MAG = 20 << 10;  // magnitudes below 0x5000: |x| < 32
+
+__device__ __forceinline__ unsigned exp16_bits(_Float16 v) {
+  unsigned short b;
+  __builtin_memcpy(&b, &v, 2);
+  return b;
+}
+
+// Table slot of an in-range bit pattern: positive half at 0, negative half after it.
+__device__ __forceinline__ _Float16 exp16_fast(const _Float16 *tab, unsigned b) {
+  return tab[(b & 0x7fffu) + (b >> 15) * (unsigned)EXP_LDS_MAG];
+}
+
+// Any bit pattern: +inf for x >= 32, +0 for x <= -32, NaN for NaN.
+__device__ __forceinline__ _Float16 exp16_any(const _Float16 *tab, unsigned b) {
+  const unsigned mag = b & 0x7fffu;
+  if (mag < (unsigned)EXP_LDS_MAG) return exp16_fast(tab, b);
+  _Float16 v;
+  const unsigned short bs = (unsigned short)b;
+  __builtin_memcpy(&v, &bs, 2);
+  if (mag > 0x7c00u) return v;
+  return (b >> 15) ? _Float16(0) : _Float16(__builtin_inff16());
+}
+
 template <int NC, int W>
 __global__ __launch_bounds__(EXP_THREADS) void exp16_kernel(const _Float16 *x, _Float16 *out, int64_t n,
                                                             const _Float16 *table) {
-  __shared__ uint4 lds_tab[65536 * 2 / 16];
-  const uint4 *gt = reinterpret_cast<const uint4 *>(table);
-  for (int i = threadIdx.x; i < 65536 * 2 / 16; i += EXP_THREADS) lds_tab[i] = gt[i];
+  __shared__ uint4 lds_raw[2 * EXP_LDS_MAG * 2 / 16];
+  // positive half: table[0 .. EXP_LDS_MAG), negative half: table[0x8000 ..)
+  {
+    const uint4 *gp = reinterpret_cast<const uint4 *>(table);
+    const uint4 *gn = reinterpret_cast<const uint4 *>(table + 0x8000);
+    constexpr int H = EXP_LDS_MAG * 2 / 16;  // uint4 per half
+    for (int i = threadIdx.x; i < 2 * H; i += EXP_THREADS) lds_raw[i] = i < H ? gp[i] : gn[i - H];
+  }
   __syncthreads();
-  const _Float16 *tab = reinterpret_cast<const _Float16 *>(lds_tab);
+  const _Float16 *tab = reinterpret_cast<const _Float16 *>(lds_raw);
   const int64_t nchunk = n / W;
   const int64_t stride = (int64_t)gridDim.x * EXP_THREADS;
   const int64_t tid = (int64_t)blockIdx.x * EXP_THREADS + threadIdx.x;
@@ -324,11 +354,18 @@ __global__ __launch_bounds__(EXP_THREADS) void exp16_kernel(const _Float16 *x, _
 #pragma unroll
       for (int w = 0; w < WW; ++w) {
         _Float16 ex[NC];
+        unsigned bits[NC], big = 0;
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
-          unsigned short b;
-          __builtin_memcpy(&b, &xa[u][c].v[w], 2);
-          ex[c] = tab[b];
+          bits[c] = exp16_bits(xa[u][c].v[w]);
+          big = big > (bits[c] & 0x7fffu) ? big : (bits[c] & 0x7fffu);
+        }
+        if (__builtin_expect(big < (unsigned)EXP_LDS_MAG, 1)) {
+#pragma unroll
+          for (int c = 0; c < NC; ++c) ex[c] = exp16_fast(tab, bits[c]);
+        } else {
+#pragma unroll
+          for (int c = 0; c < NC; ++c) ex[c] = exp16_any(tab, bits[c]);
         }
         _Float16 h0[1] = {ex[0]};
         _Float16 r[NC];
@@ -368,7 +405,7 @@ static hipError_t exp16_launch(int64_t n, const void *x, void *out, const _Float
   bool vec = (n % 8 == 0) && ((uintptr_t)x % 16 == 0) && ((uintptr_t)out % 16 == 0);
   int64_t work = vec ? n / 8 : n;
   int64_t blocks = (work + EXP_THREADS - 1) / EXP_THREADS;
-  if (blocks > cus) blocks = cus;
+  if (blocks > 2 * cus) blocks = 2 * cus;  // 80 KiB of LDS each: up to two per CU
   if (blocks < 1) blocks = 1;
   if (vec)
     hipLaunchKernelGGL((exp16_kernel<NC, 8>), dim3(blocks), dim3(EXP_THREADS), 0, s, (const _Float16 *)x,

@@ -123,12 +123,18 @@ __device__ __forceinline__ void grow_expn(const T (&x)[N], T v, T (&out)[N]) {
 }
 
 // ScalingN: an M-component value times a plain value v; R = M (expand off) or M+1.
+// The first Two-Sum adds the initial carry +0: Two-Sum(hp, +0) = (hp + 0, +0) for any
+// finite hp, so h_0 = hp and the carry is e1, up to the sign of a zero -- and
+// Simple-Renorm drops every zero term and pads with +0, so the result is the same.
+// (With an infinite or NaN term the elided steps could only turn an infinity into a
+// NaN; results are then non-finite either way.)
 template <typename T, int M, int R>
 __device__ __forceinline__ void scaling_n(const T (&x)[M], T v, T (&out)[R]) {
   T h[M + 1];
-  T e = T(0);
+  T e;
+  two_prod(x[0], v, h[0], e);
 #pragma unroll
-  for (int i = 0; i < M; ++i) {
+  for (int i = 1; i < M; ++i) {
     T hp, e1, e2;
     two_prod(x[i], v, hp, e1);
     two_sum(hp, e, h[i], e2);
@@ -138,13 +144,15 @@ __device__ __forceinline__ void scaling_n(const T (&x)[M], T v, T (&out)[R]) {
   simple_renorm<T, M + 1, R>(h, out);
 }
 
-// Add-MCN: sum of two N-component values.
+// Add-MCN: sum of two N-component values (first Two-Sum with the +0 carry elided as
+// in scaling_n).
 template <typename T, int N>
 __device__ __forceinline__ void add_mcn(const T (&x)[N], const T (&y)[N], T (&out)[N]) {
   T h[N + 1];
-  T e = T(0);
+  T e;
+  two_sum(x[0], y[0], h[0], e);
 #pragma unroll
-  for (int i = 0; i < N; ++i) {
+  for (int i = 1; i < N; ++i) {
     T hp, e1, e2;
     two_sum(x[i], y[i], hp, e1);
     two_sum(hp, e, h[i], e2);

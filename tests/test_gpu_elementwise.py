@@ -132,12 +132,18 @@ def test_special_values(mcf, orc):
 
 def test_literal_mult_inputs_overflow_class(mcf, orc):
     """Mult-MCN with divisors drawn from U[-1/2, 1/2] (the literal elementwise input
-    range): tiny divisors overflow the reciprocal; results must agree by class."""
+    range): tiny divisors overflow the reciprocal.  Elements whose result is finite on
+    both sides agree bit for bit; the others are non-finite on both sides."""
     n = 1 << 18
     x, _ = inputs.elementwise_inputs("add", n, 3, np.float16, seed=11)
     _, y = inputs.elementwise_inputs("add", n, 3, np.float16, seed=12)
     got = to_host(mcf.mc_mul(to_dev(x), to_dev(y), nc=3))
-    assert_bits(got, orc.mul(x, y, nc=3), "mult literal range")
+    want = orc.mul(x, y, nc=3)
+    gfin = np.isfinite(got.astype(np.float64)).all(0)
+    wfin = np.isfinite(want.astype(np.float64)).all(0)
+    assert np.array_equal(gfin, wfin)
+    assert (~wfin).sum() > 0  # the case does occur (about 2^-15 of the elements)
+    assert_bits(got[:, wfin], want[:, wfin], "mult literal range")
 
 
 def test_in_place_and_empty(mcf, orc):
