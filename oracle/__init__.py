@@ -69,6 +69,8 @@ def lib() -> ctypes.CDLL:
         L.mcf_oracle_elementwise.argtypes = [ci, ci, ci, ci, i64, vp, ci, vp, ci, vp]
         L.mcf_oracle_matmul.restype = ci
         L.mcf_oracle_matmul.argtypes = [ci, ci, i64, i64, i64, vp, ci, vp, ci, vp, vp, i64, vp]
+        L.mcf_oracle_matmul_splitk.restype = ci
+        L.mcf_oracle_matmul_splitk.argtypes = [ci, ci, i64, i64, i64, vp, ci, vp, ci, i64, vp, vp, i64, vp]
         L.mcf_oracle_linear.restype = ci
         L.mcf_oracle_linear.argtypes = [ci, ci, i64, i64, i64, vp, vp, vp, vp, vp, i64, vp]
         L.mcf_oracle_matmul_exact_err.restype = ci
@@ -268,6 +270,32 @@ def matmul(A, B, *, nc, a_mc=True, b_mc=True, rows=None, cols=None):
     out = np.empty((nc, count), dtype=dtype)
     rc = lib().mcf_oracle_matmul(fmt, nc, M, N, K, _ptr(A), int(a_mc), _ptr(B), int(b_mc), _ptr(r), _ptr(c),
                                  count, _ptr(out))
+    if rc != 0:
+        raise ValueError("oracle: bad arguments")
+    return out.reshape(nc, M, N) if rows is None else out
+
+
+def matmul_splitk(A, B, *, nc, slices, a_mc=True, b_mc=True, rows=None, cols=None):
+    """C = A x B with the reduction dealt round-robin to min(slices, K) slices, each
+    summed in MM-MCN order, then combined by a pairwise Add-MCN tree (MC x MC: one
+    such product per component of B, combined left to right).  slices = 1 is
+    ``matmul``.  Shapes and return value as for ``matmul``."""
+    dtype = np.dtype(A.dtype)
+    fmt = fmt_of(dtype)
+    A = _planar(A, dtype)
+    B = _planar(B, dtype)
+    if A.ndim == 2:
+        A = A[None]
+    if B.ndim == 2:
+        B = B[None]
+    M, K = A.shape[1:]
+    K2, N = B.shape[1:]
+    if K2 != K or A.shape[0] != (nc if a_mc else 1) or B.shape[0] != (nc if b_mc else 1) or slices < 1:
+        raise ValueError("matmul_splitk: bad arguments")
+    r, c, count = _positions(M, N, rows, cols)
+    out = np.empty((nc, count), dtype=dtype)
+    rc = lib().mcf_oracle_matmul_splitk(fmt, nc, M, N, K, _ptr(A), int(a_mc), _ptr(B), int(b_mc), int(slices),
+                                        _ptr(r), _ptr(c), count, _ptr(out))
     if rc != 0:
         raise ValueError("oracle: bad arguments")
     return out.reshape(nc, M, N) if rows is None else out

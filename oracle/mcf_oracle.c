@@ -492,17 +492,20 @@ static void mm_term(const mm_args *g, int nc, int64_t i, int64_t j, int64_t k, i
   }
 }
 
-/* MM-MCN for one output of an MC matrix times a plain matrix:
- * acc = ScalingN(term 0); acc = Add-MCN(acc, ScalingN(term k)) for k = 1..K-1,
- * the sequential order in which the paper propagates the addition error.
- * K = 0 gives +0 in every component. */
-static void mm_entry_plain(const mm_args *g, int nc, int64_t i, int64_t j, int bcomp, double *acc) {
+/* MM-MCN for one output of an MC matrix times a plain matrix, over the reduction
+ * indices k = k0, k0 + kstep, k0 + 2 kstep, ... below K:
+ * acc = ScalingN(first term); acc = Add-MCN(acc, ScalingN(next term)) for each
+ * further k, the sequential order in which the paper propagates the addition error
+ * (Section 2.2; Appendix A.2.2, MV-MCN and MM-MCN).  The full product is k0 = 0,
+ * kstep = 1.  No term gives +0 in every component. */
+static void mm_entry_plain(const mm_args *g, int nc, int64_t i, int64_t j, int bcomp, int64_t k0, int64_t kstep,
+                           double *acc) {
   double mc[MAXC], term[MAXC], t[MAXC], v;
   for (int c = 0; c < nc; ++c) acc[c] = 0.0;
-  for (int64_t k = 0; k < g->K; ++k) {
+  for (int64_t k = k0; k < g->K; k += kstep) {
     mm_term(g, nc, i, j, k, bcomp, mc, &v);
     scaling_n(g->f, mc, nc, v, 0, term);
-    if (k == 0) {
+    if (k == k0) {
       for (int c = 0; c < nc; ++c) acc[c] = term[c];
     } else {
       add_mcn(g->f, acc, term, nc, t);
@@ -519,14 +522,14 @@ static void mm_entry_plain(const mm_args *g, int nc, int64_t i, int64_t j, int b
 static void mm_entry(const mm_args *g, int nc, int64_t i, int64_t j, double *out) {
   if (g->a_mc && g->b_mc) {
     double part[MAXC], t[MAXC];
-    mm_entry_plain(g, nc, i, j, 0, out);
+    mm_entry_plain(g, nc, i, j, 0, 0, 1, out);
     for (int b = 1; b < nc; ++b) {
-      mm_entry_plain(g, nc, i, j, b, part);
+      mm_entry_plain(g, nc, i, j, b, 0, 1, part);
       add_mcn(g->f, out, part, nc, t);
       for (int c = 0; c < nc; ++c) out[c] = t[c];
     }
   } else {
-    mm_entry_plain(g, nc, i, j, 0, out);
+    mm_entry_plain(g, nc, i, j, 0, 0, 1, out);
   }
 }
 
@@ -550,6 +553,75 @@ int mcf_oracle_matmul(int f, int nc, int64_t M, int64_t N, int64_t K, const void
   return 0;
 }
 
+/* K-split product, one output and one component of B (the whole B when it is
+ * plain).  Reading of the paper's remark that an accurate sum of N MC values can be
+ * had in O(nc log N) depth (Section 2.2): the K reduction steps are dealt out
+ * round-robin to S = min(S, K) slices, slice s taking k = s, s + S, s + 2S, ...;
+ * each slice accumulates its terms in MM-MCN order; the S slice sums are then
+ * combined by a pairwise tree of Add-MCN: at each level, entry q of the next level
+ * is Add-MCN(entry 2q, entry 2q+1), and an odd last entry moves up unchanged, until
+ * one value is left.  S = 1 is MM-MCN itself. */
+static void mm_entry_split_plain(const mm_args *g, int nc, int64_t i, int64_t j, int bcomp, int64_t S,
+                                 double *work, double *out) {
+  if (g->K == 0) {
+    for (int c = 0; c < nc; ++c) out[c] = 0.0;
+    return;
+  }
+  if (S > g->K) S = g->K;
+  for (int64_t s = 0; s < S; ++s) mm_entry_plain(g, nc, i, j, bcomp, s, S, work + s * nc);
+  for (int64_t count = S; count > 1; count = (count + 1) / 2) {
+    for (int64_t q = 0; 2 * q < count; ++q) {
+      double t[MAXC];
+      if (2 * q + 1 < count)
+        add_mcn(g->f, work + 2 * q * nc, work + (2 * q + 1) * nc, nc, t);
+      else
+        for (int c = 0; c < nc; ++c) t[c] = work[2 * q * nc + c];
+      for (int c = 0; c < nc; ++c) work[q * nc + c] = t[c];
+    }
+  }
+  for (int c = 0; c < nc; ++c) out[c] = work[c];
+}
+
+/* C = A x B by the K-split above (MC x MC: one K-split product per component of B,
+ * combined left to right with Add-MCN, as in mm_entry).  Arguments as for
+ * mcf_oracle_matmul, plus the slice count S >= 1.  Returns 0, or -1 on bad
+ * arguments or when scratch memory cannot be had. */
+int mcf_oracle_matmul_splitk(int f, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc,
+                             const void *B, int b_mc, int64_t S, const int64_t *rows, const int64_t *cols,
+                             int64_t count, void *out) {
+  if (nc < 1 || nc > MAXC || (!a_mc && !b_mc) || S < 1) return -1;
+  mm_args g = {f, A, a_mc, B, b_mc, K, K, 1, N, 1, M * K, K * N};
+  int64_t slots = S < K ? S : (K > 0 ? K : 1);
+  int failed = 0;
+#pragma omp parallel
+  {
+    double *work = (double *)malloc((size_t)slots * nc * sizeof(double));
+    if (!work) {
+#pragma omp atomic write
+      failed = 1;
+    }
+#pragma omp for schedule(dynamic, 1)
+    for (int64_t t = 0; t < count; ++t) {
+      if (!work) continue;
+      int64_t i = rows ? rows[t] : t / N;
+      int64_t j = rows ? cols[t] : t % N;
+      double r[MAXC];
+      mm_entry_split_plain(&g, nc, i, j, 0, S, work, r);
+      if (a_mc && b_mc) {
+        for (int b = 1; b < nc; ++b) {
+          double part[MAXC], sum[MAXC];
+          mm_entry_split_plain(&g, nc, i, j, b, S, work, part);
+          add_mcn(f, r, part, nc, sum);
+          for (int c = 0; c < nc; ++c) r[c] = sum[c];
+        }
+      }
+      scatter(f, out, nc, count, t, r);
+    }
+    free(work);
+  }
+  return failed ? -1 : 0;
+}
+
 /* MC-Linear forward (Section 2.3): the product of the MC weight and the plain input,
  * Y[t][o] = sum over i of W[o][i] * X[t][i] in MM-MCN order, then Add-MCN with the
  * MC bias[o] when bias is given.  X is plain [T][I], W is [nc][O][I], bias [nc][O].
@@ -565,7 +637,7 @@ int mcf_oracle_linear(int f, int nc, int64_t T, int64_t I, int64_t O, const void
     int64_t i = rows ? rows[t] : t / O;
     int64_t j = rows ? cols[t] : t % O;
     double r[MAXC];
-    mm_entry_plain(&g, nc, i, j, 0, r);
+    mm_entry_plain(&g, nc, i, j, 0, 0, 1, r);
     if (bias) {
       double b[MAXC], s[MAXC];
       for (int c = 0; c < nc; ++c) b[c] = load_c(f, bias, (int64_t)c * O + j);
