@@ -121,7 +121,7 @@ def cpu_baseline(oracle, A, B, nc, target_s=12.0):
     t0 = time.perf_counter()
     oracle.matmul(A, B, nc=nc, rows=g.integers(0, M, probe), cols=g.integers(0, N, probe))
     dt = time.perf_counter() - t0
-    count = int(max(probe, min(4096, probe * target_s / max(dt, 1e-3))))
+    count = int(max(probe, min(16384, probe * target_s / max(dt, 1e-3))))
     threads = oracle.threads()
     count = max(threads, (count // threads) * threads)
     rows = g.integers(0, M, count)
@@ -161,6 +161,39 @@ def bench_elementwise(torch, mcf, inputs, steps=10):
                      "Gelem/s": round(n / (ms * 1e-3) / 1e9, 2)}
         log(f"  elementwise {name}: {ms * 1e3:.1f} us, {gbs:.0f} GB/s")
     return {"workload": "2^26 elements, binary16, nc = 3", "ops": res}
+
+
+def bench_splitk(torch, mcf, inputs, steps=20):
+    """K-split products on the shapes they are for, with their HBM bandwidth:
+    Dot-MCN of two binary32 nc = 2 MC vectors of 2^24 entries, and MV-MCN of an
+    8192 x 8192 binary32 nc = 3 MC matrix by a plain vector (default slice counts)."""
+    res = {}
+    cases = (("dot_2^24_f32_nc2", 1, 1, 1 << 24, 2, True, True),
+             ("mv_8192x8192_f32_nc3", 8192, 1, 8192, 3, True, False))
+    for name, M, N, K, nc, a_mc, b_mc in cases:
+        A, B = inputs.matmul_normal(M, N, K, nc, np.float32, seed=0)
+        tA = torch.from_numpy(A if a_mc else A[:1]).cuda()
+        tB = torch.from_numpy(B if b_mc else B[:1]).cuda()
+        del A, B
+        out = torch.empty((nc, M, N), dtype=torch.float32, device="cuda")
+        S = mcf.mc_matmul_splitk_slices(M, N, K)
+        wb = mcf.mc_matmul_splitk_workspace(1, nc, M, N, K, a_mc, b_mc, S)
+        ws = torch.empty(max(wb, 1), dtype=torch.uint8, device="cuda")
+        fn = lambda: mcf.mc_matmul_splitk(tA, tB, nc=nc, a_mc=a_mc, b_mc=b_mc, out=out, workspace=ws)
+        for _ in range(3):
+            fn()
+        tm = Timer(torch)
+        for _ in range(steps):
+            tm.run(fn)
+        ms = float(np.median(tm.ms()))
+        nbytes = (tA.numel() + tB.numel() + out.numel()) * 4
+        gbs = nbytes / (ms * 1e-3) / 1e9
+        res[name] = {"us": round(ms * 1e3, 1), "slices": S, "GB/s": round(gbs, 1),
+                     "hbm_frac": round(gbs * 1e9 / HBM_PEAK, 3),
+                     "MC-GFLOP/s": round(2 * M * N * K / (ms * 1e-3) / 1e9, 1)}
+        log(f"  splitk {name}: {ms * 1e3:.1f} us, {gbs:.0f} GB/s (S = {S})")
+        del tA, tB, out, ws
+    return res
 
 
 def bench_linear(torch, mcf, inputs, layers=100):
@@ -277,6 +310,8 @@ def main():
         extra["linear_4096x1024x1024_f16_nc3"] = bench_linear(torch, mcf, inputs)
         log("elementwise")
         extra["elementwise"] = bench_elementwise(torch, mcf, inputs)
+        log("K-split products")
+        extra["splitk"] = bench_splitk(torch, mcf, inputs)
         line["extra"] = extra
     if not args.no_cpu:
         log("cpu baseline (oracle)")

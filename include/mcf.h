@@ -10,7 +10,8 @@
  * ---------------------------------------
  * Memory.  All tensor pointers are DEVICE pointers owned by the caller; the library
  *   allocates nothing per call and keeps no state besides a per-device binary16
- *   exponential table (128 KiB, built on the first mc_exp call on a device).
+ *   exponential table (128 KiB, built on the first mc_exp call on a device).  Calls
+ *   that need scratch memory (mc_matmul_splitk) take a caller-owned workspace.
  * Layout.  Dense, component-major ("planar"): component c of element i of an MC
  *   array of n elements is at element offset c*n + i.  A plain tensor is one plane.
  *   Matrices are row-major inside each plane.  The paper's interleaved layout
@@ -113,6 +114,41 @@ int mc_renorm(int dtype, int nc_in, int nc_out, int64_t n, const void *x, void *
  * A: [nc or 1][M][K], B: [nc or 1][K][N], C: [nc][M][N]. */
 int mc_matmul(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B,
               int b_mc, void *C, void *stream);
+
+/* K-split matrix product, for reductions that are long compared with the number of
+ * outputs (Dot-MCN, MV-MCN, small products).  Section 2.2 of the paper notes that an
+ * accurate sum of N MC values can be had in O(nc log N) depth; this entry point
+ * computes the following log-depth variant of MM-MCN, fixed by the slice count S
+ * alone (never by the device or the launch):
+ *   the reduction steps are dealt round-robin to S slices, slice s taking
+ *   k = s, s + S, s + 2S, ...; each slice is summed in MM-MCN order; the S slice
+ *   sums are combined by a pairwise Add-MCN tree -- at each level entry q of the
+ *   next level is Add-MCN(entry 2q, entry 2q+1), an odd last entry moves up
+ *   unchanged.  With both operands MC, one such product per component of B,
+ *   combined left to right with Add-MCN (as mc_matmul).
+ * S = 1 gives exactly mc_matmul's result.  Other S give a result of the same
+ * accuracy class (the error bound of MM-MCN holds) but not the same bits.
+ * slices: S, at most 65536 (else MCF_E_ARG); values above K are taken as K;
+ *   slices <= 0 selects mc_matmul_splitk_slices(M, N, K).
+ * workspace: device memory of at least mc_matmul_splitk_workspace(...) bytes, owned
+ *   by the caller, not overlapping A, B or C; may be NULL when that size is 0.  Its
+ *   contents on entry do not matter; calls sharing a workspace must not overlap
+ *   in time.  Too small: MCF_E_ARG; NULL when needed: MCF_E_NULL.
+ * A: [nc or 1][M][K], B: [nc or 1][K][N], C: [nc][M][N] (C must not overlap A or B);
+ * M * N below 2^31. */
+int mc_matmul_splitk(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B,
+                     int b_mc, int64_t slices, void *workspace, int64_t workspace_bytes, void *C, void *stream);
+
+/* Default slice count of mc_matmul_splitk, a function of the shape only: enough
+ * slices for about 2^18 lanes in total (ceil(2^18 / (M N))), at most K / 8 (so a
+ * slice holds at least 8 terms when K allows), at most 65536, at least 1.
+ * Negative sizes: MCF_E_SHAPE. */
+int64_t mc_matmul_splitk_slices(int64_t M, int64_t N, int64_t K);
+
+/* Workspace bytes mc_matmul_splitk needs for these arguments (0 when none), or a
+ * negative mcf_status for arguments mc_matmul_splitk would reject. */
+int64_t mc_matmul_splitk_workspace(int dtype, int nc, int64_t M, int64_t N, int64_t K, int a_mc, int b_mc,
+                                   int64_t slices);
 
 /* MC-Linear forward (Section 2.3): y = x W^T (+ b).  The weight and bias are MC,
  * the input is a plain tensor; each output accumulates ScalingN(W[o][i], x[t][i])

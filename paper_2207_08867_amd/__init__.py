@@ -18,7 +18,8 @@ import ctypes
 import os
 
 __all__ = [
-    "mc_add", "mc_mul", "mc_div", "mc_exp", "mc_renorm", "mc_matmul", "mc_linear_fwd", "mc_status_str",
+    "mc_add", "mc_mul", "mc_div", "mc_exp", "mc_renorm", "mc_matmul", "mc_matmul_splitk",
+    "mc_matmul_splitk_slices", "mc_matmul_splitk_workspace", "mc_linear_fwd", "mc_status_str",
     "lib", "LIB_PATH", "MCFError",
 ]
 
@@ -51,6 +52,12 @@ def lib() -> ctypes.CDLL:
         L.mc_renorm.argtypes = [ci, ci, ci, i64, vp, vp, ci, vp]
         L.mc_matmul.restype = ci
         L.mc_matmul.argtypes = [ci, ci, i64, i64, i64, vp, ci, vp, ci, vp, vp]
+        L.mc_matmul_splitk.restype = ci
+        L.mc_matmul_splitk.argtypes = [ci, ci, i64, i64, i64, vp, ci, vp, ci, i64, vp, i64, vp, vp]
+        L.mc_matmul_splitk_slices.restype = i64
+        L.mc_matmul_splitk_slices.argtypes = [i64, i64, i64]
+        L.mc_matmul_splitk_workspace.restype = i64
+        L.mc_matmul_splitk_workspace.argtypes = [ci, ci, i64, i64, i64, ci, ci, i64]
         L.mc_linear_fwd.restype = ci
         L.mc_linear_fwd.argtypes = [ci, ci, i64, i64, i64, vp, vp, vp, vp, vp]
         L.mc_status_str.restype = ctypes.c_char_p
@@ -177,8 +184,7 @@ def mc_renorm(x, *, nc_out: int | None = None, mode: int = 0, out=None):
     return out
 
 
-def mc_matmul(A, B, *, nc: int, a_mc: bool = True, b_mc: bool = True, out=None):
-    """C = A B in MM-MCN order.  A: (nc|1, M, K), B: (nc|1, K, N) -> (nc, M, N)."""
+def _mm_operands(A, B, nc, a_mc, b_mc, out):
     torch = _torch()
     if A.dtype != B.dtype or A.device != B.device:
         raise ValueError("operands must share dtype and device")
@@ -194,9 +200,50 @@ def mc_matmul(A, B, *, nc: int, a_mc: bool = True, b_mc: bool = True, out=None):
         out = torch.empty((nc, M, N), dtype=A.dtype, device=A.device)
     elif out.shape != (nc, M, N) or out.dtype != A.dtype:
         raise ValueError("out has the wrong shape or dtype")
+    return A3, B3, M, N, K, out
+
+
+def mc_matmul(A, B, *, nc: int, a_mc: bool = True, b_mc: bool = True, out=None):
+    """C = A B in MM-MCN order.  A: (nc|1, M, K), B: (nc|1, K, N) -> (nc, M, N)."""
+    A3, B3, M, N, K, out = _mm_operands(A, B, nc, a_mc, b_mc, out)
     st = lib().mc_matmul(_dtype_code(A), nc, M, N, K, _dev(A3, "A"), int(bool(a_mc)), _dev(B3, "B"),
                          int(bool(b_mc)), _dev(out, "out"), _stream(A))
     _check(st, "mc_matmul")
+    return out
+
+
+def mc_matmul_splitk_slices(M: int, N: int, K: int) -> int:
+    """Default slice count of the K-split product for this shape."""
+    s = lib().mc_matmul_splitk_slices(M, N, K)
+    _check(int(s) if s < 0 else 0, "mc_matmul_splitk_slices")
+    return int(s)
+
+
+def mc_matmul_splitk_workspace(dtype_code: int, nc: int, M: int, N: int, K: int, a_mc: bool, b_mc: bool,
+                               slices: int) -> int:
+    """Workspace bytes the K-split product needs."""
+    w = lib().mc_matmul_splitk_workspace(dtype_code, nc, M, N, K, int(bool(a_mc)), int(bool(b_mc)), slices)
+    _check(int(w) if w < 0 else 0, "mc_matmul_splitk_workspace")
+    return int(w)
+
+
+def mc_matmul_splitk(A, B, *, nc: int, a_mc: bool = True, b_mc: bool = True, slices: int = 0, out=None,
+                     workspace=None):
+    """C = A B with the reduction dealt round-robin to `slices` slices (0: the default
+    for the shape), each summed in MM-MCN order, the slice sums combined by a
+    pairwise Add-MCN tree.  Shapes as for mc_matmul.  `workspace`: an optional
+    device byte tensor; one is allocated here when needed and not given."""
+    torch = _torch()
+    A3, B3, M, N, K, out = _mm_operands(A, B, nc, a_mc, b_mc, out)
+    code = _dtype_code(A)
+    wb = mc_matmul_splitk_workspace(code, nc, M, N, K, a_mc, b_mc, slices)
+    if wb > 0 and workspace is None:
+        workspace = torch.empty(wb, dtype=torch.uint8, device=A.device)
+    wp = _dev(workspace, "workspace") if workspace is not None else None
+    wn = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    st = lib().mc_matmul_splitk(code, nc, M, N, K, _dev(A3, "A"), int(bool(a_mc)), _dev(B3, "B"), int(bool(b_mc)),
+                                int(slices), wp, wn, _dev(out, "out"), _stream(A))
+    _check(st, "mc_matmul_splitk")
     return out
 
 

@@ -25,6 +25,10 @@ bool bad_alias(const void *out, int64_t obytes, const void *in, int64_t ibytes) 
   return overlap(out, obytes, in, ibytes);
 }
 
+// The sequential product launches one workgroup per 16 x 16 (or larger) tile of C in
+// a 1-D grid, which must stay below 2^31 workgroups.
+bool grid_fits(int64_t M, int64_t N) { return ((M + 15) / 16) * ((N + 15) / 16) < ((int64_t)1 << 31); }
+
 int hip_status(hipError_t e) { return e == hipSuccess ? MCF_OK : MCF_E_HIP; }
 
 int check_common(int dtype, int nc, int64_t n) {
@@ -47,6 +51,32 @@ int binary_op(int op, int dtype, int nc, int64_t n, const void *x, int x_mc, con
   const int64_t ob = nc * n * es, xb = (x_mc ? nc : 1) * n * es, yb = (y_mc ? nc : 1) * n * es;
   if (bad_alias(out, ob, x, xb) || bad_alias(out, ob, y, yb)) return MCF_E_ALIAS;
   return hip_status(mcf::launch_elementwise(dtype, op, nc, nc, n, x, x_mc, y, y_mc, out, (hipStream_t)stream));
+}
+
+// Shared validation of the K-split product; *S receives the slice count used
+// (the default for slices <= 0, capped at K).
+int splitk_check(int dtype, int nc, int64_t M, int64_t N, int64_t K, int a_mc, int b_mc, int64_t slices,
+                 int64_t *S) {
+  if (dtype != MCF_F16 && dtype != MCF_F32) return MCF_E_DTYPE;
+  if (nc < 1 || nc > MAX_NC) return MCF_E_NC;
+  if ((a_mc != 0 && a_mc != 1) || (b_mc != 0 && b_mc != 1) || (!a_mc && !b_mc)) return MCF_E_ARG;
+  if (M < 0 || N < 0 || K < 0) return MCF_E_SHAPE;
+  if (M > ((int64_t)1 << 40) || N > ((int64_t)1 << 40) || K > ((int64_t)1 << 40)) return MCF_E_SHAPE;
+  if (M > 0 && N > (((int64_t)1 << 31) - 1) / M) return MCF_E_SHAPE;  // grid of up to M*N workgroups
+  if (slices > mcf::SPLITK_MAX_SLICES) return MCF_E_ARG;
+  int64_t s = slices <= 0 ? mcf::splitk_default_slices(M, N, K) : slices;
+  if (K > 0 && s > K) s = K;
+  *S = s < 1 ? 1 : s;
+  return MCF_OK;
+}
+
+int64_t splitk_workspace_bytes(int dtype, int nc, int64_t M, int64_t N, int64_t K, int a_mc, int b_mc, int64_t S) {
+  if (M == 0 || N == 0 || K == 0) return 0;
+  int KS, G;
+  mcf::splitk_shape(S, &KS, &G);
+  if (G == 1) return 0;
+  const int64_t np = (a_mc && b_mc) ? nc : 1;
+  return (int64_t)G * np * nc * M * N * elem_size(dtype);
 }
 
 }  // namespace
@@ -98,8 +128,8 @@ int mc_matmul(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A,
   if (nc < 1 || nc > MAX_NC) return MCF_E_NC;
   if ((a_mc != 0 && a_mc != 1) || (b_mc != 0 && b_mc != 1) || (!a_mc && !b_mc)) return MCF_E_ARG;
   if (M < 0 || N < 0 || K < 0) return MCF_E_SHAPE;
-  // grid limits: M / 32 workgroup rows, N / 32 columns
   if (M > ((int64_t)1 << 20) || N > ((int64_t)1 << 30) || K > ((int64_t)1 << 40)) return MCF_E_SHAPE;
+  if (!grid_fits(M, N)) return MCF_E_SHAPE;
   if (M == 0 || N == 0) return MCF_OK;
   if (!C || (K > 0 && (!A || !B))) return MCF_E_NULL;
   const int64_t es = elem_size(dtype);
@@ -109,12 +139,49 @@ int mc_matmul(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A,
   return hip_status(mcf::launch_matmul(dtype, nc, M, N, K, A, a_mc, B, b_mc, 0, nullptr, C, (hipStream_t)stream));
 }
 
+int64_t mc_matmul_splitk_slices(int64_t M, int64_t N, int64_t K) {
+  if (M < 0 || N < 0 || K < 0) return MCF_E_SHAPE;
+  return mcf::splitk_default_slices(M, N, K);
+}
+
+int64_t mc_matmul_splitk_workspace(int dtype, int nc, int64_t M, int64_t N, int64_t K, int a_mc, int b_mc,
+                                   int64_t slices) {
+  int64_t S = 0;
+  int st = splitk_check(dtype, nc, M, N, K, a_mc, b_mc, slices, &S);
+  if (st != MCF_OK) return st;
+  return splitk_workspace_bytes(dtype, nc, M, N, K, a_mc, b_mc, S);
+}
+
+int mc_matmul_splitk(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B,
+                     int b_mc, int64_t slices, void *workspace, int64_t workspace_bytes, void *C, void *stream) {
+  int64_t S = 0;
+  int st = splitk_check(dtype, nc, M, N, K, a_mc, b_mc, slices, &S);
+  if (st != MCF_OK) return st;
+  if (M == 0 || N == 0) return MCF_OK;
+  if (!C || (K > 0 && (!A || !B))) return MCF_E_NULL;
+  const int64_t es = elem_size(dtype);
+  const int64_t cb = nc * M * N * es, ab = (a_mc ? nc : 1) * M * K * es, bb = (b_mc ? nc : 1) * K * N * es;
+  if (overlap(C, cb, A, ab) || overlap(C, cb, B, bb)) return MCF_E_ALIAS;
+  if (K == 0)  // every output is +0
+    return hip_status(mcf::launch_matmul(dtype, nc, M, N, 0, A, a_mc, B, b_mc, 0, nullptr, C, (hipStream_t)stream));
+  const int64_t wb = splitk_workspace_bytes(dtype, nc, M, N, K, a_mc, b_mc, S);
+  if (wb > 0) {
+    if (!workspace) return MCF_E_NULL;
+    if (workspace_bytes < wb) return MCF_E_ARG;
+    if (overlap(workspace, wb, A, ab) || overlap(workspace, wb, B, bb) || overlap(workspace, wb, C, cb))
+      return MCF_E_ALIAS;
+  }
+  return hip_status(
+      mcf::launch_matmul_splitk(dtype, nc, M, N, K, A, a_mc, B, b_mc, S, workspace, C, (hipStream_t)stream));
+}
+
 int mc_linear_fwd(int dtype, int nc, int64_t batch, int64_t in, int64_t out, const void *x, const void *W,
                   const void *b, void *y, void *stream) {
   if (dtype != MCF_F16 && dtype != MCF_F32) return MCF_E_DTYPE;
   if (nc < 1 || nc > MAX_NC) return MCF_E_NC;
   if (batch < 0 || in < 0 || out < 0) return MCF_E_SHAPE;
   if (batch > ((int64_t)1 << 20) || out > ((int64_t)1 << 30) || in > ((int64_t)1 << 40)) return MCF_E_SHAPE;
+  if (!grid_fits(batch, out)) return MCF_E_SHAPE;
   if (batch == 0 || out == 0) return MCF_OK;
   if (!y || (in > 0 && (!x || !W))) return MCF_E_NULL;
   const int64_t es = elem_size(dtype);

@@ -25,4 +25,14 @@ hipError_t launch_exp_f16(int nc, int64_t n, const void *x, void *out, hipStream
 hipError_t launch_matmul(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc,
                          const void *B, int b_mc, int b_trans, const void *bias, void *C, hipStream_t stream);
 
+// K-split product (splitk.hip).  S slices (1 <= S <= min(K, SPLITK_MAX_SLICES)); W is
+// a workspace of splitk_workspace_elems(...) components when S exceeds one
+// workgroup's slice group, else unused.
+constexpr int64_t SPLITK_TARGET_LANES = (int64_t)1 << 18;
+constexpr int64_t SPLITK_MAX_SLICES = 65536;
+int64_t splitk_default_slices(int64_t M, int64_t N, int64_t K);
+void splitk_shape(int64_t S, int *KS, int *G);
+hipError_t launch_matmul_splitk(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc,
+                                const void *B, int b_mc, int64_t S, void *W, void *C, hipStream_t stream);
+
 }  // namespace mcf

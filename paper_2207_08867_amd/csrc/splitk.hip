@@ -1,0 +1,274 @@
+// splitk.hip -- K-split MC matrix product on gfx950 VALU, for reductions that are
+// long compared with the number of outputs (Dot-MCN, MV-MCN, small products).
+//
+// The function computed (fixed by the slice count S alone, not by the launch):
+// the reduction steps are dealt round-robin to S slices, slice s taking
+// k = s, s + S, s + 2S, ...; each slice is summed in MM-MCN order (ScalingN of its
+// first term, then Add-MCN of each further ScalingN term); the S slice sums are then
+// combined by a pairwise Add-MCN tree -- at each level entry q of the next level is
+// Add-MCN(entry 2q, entry 2q+1) and an odd last entry moves up unchanged.  This is
+// the log-depth accumulation that Section 2.2 of the paper names as the cost of an
+// accurate N-term MC sum.  MC x MC products are taken by linearity over B's
+// components, one K-split product per component, combined left to right.
+//
+// Launch: a 256-lane workgroup holds 256/KS outputs x KS consecutive slices (KS a
+// power of two); lane (output o, slice s) reads A[i][k] and B[k][j] for its own k,
+// so the lanes of a slice group read consecutive k.  The first log2(KS) tree levels
+// run inside the workgroup (strides < 64 by lane exchange inside a wavefront, 64 and
+// 128 through LDS); when S > KS the G = ceil(S/KS) group results go to a workspace
+// and a second kernel runs the remaining levels the same way.  Because slice groups
+// are aligned blocks of KS leaves, the split between the two kernels never pairs
+// entries across groups: the result equals the tree's definition for every KS.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "mcf_arith.hpp"
+#include "mcf_internal.hpp"
+#include "mm_steps.hpp"
+
+namespace mcf {
+
+constexpr int SK_THREADS = 256;
+constexpr int SK_UNROLL = 4;
+
+// Lane exchange inside a wavefront: the value of lane (l + d), for d < 64.  binary16
+// values travel as binary32 (exact both ways).
+__device__ __forceinline__ float lane_down(float v, int d) { return __shfl_down(v, (unsigned)d, 64); }
+__device__ __forceinline__ _Float16 lane_down(_Float16 v, int d) {
+  return (_Float16)__shfl_down((float)v, (unsigned)d, 64);
+}
+
+// Pairwise Add-MCN tree over groups of W lanes (W a power of two, W <= 256): lane q
+// of a group holds leaf q, and leaves q >= count are absent.  At stride d the entry of
+// lane q (q a multiple of 2d) becomes Add-MCN(entry q, entry q + d) when q + d <
+// count, and is unchanged otherwise.  Afterwards lane 0 of each group holds the root.
+// Every lane of the workgroup must call this (it contains barriers and exchanges).
+template <typename T, int NC, int NP, int APOL>
+__device__ __forceinline__ void group_tree(T (&acc)[NP][NC], int q, int W, int count, T (*lds)[NP * NC]) {
+  for (int d = 1; d < W; d <<= 1) {
+    T other[NP][NC];
+    if (d < 64) {
+#pragma unroll
+      for (int p = 0; p < NP; ++p)
+#pragma unroll
+        for (int c = 0; c < NC; ++c) other[p][c] = lane_down(acc[p][c], d);
+    } else {
+      if ((q & (2 * d - 1)) == d) {
+#pragma unroll
+        for (int p = 0; p < NP; ++p)
+#pragma unroll
+          for (int c = 0; c < NC; ++c) lds[threadIdx.x][p * NC + c] = acc[p][c];
+      }
+      __syncthreads();
+      if ((q & (2 * d - 1)) == 0 && q + d < count) {
+#pragma unroll
+        for (int p = 0; p < NP; ++p)
+#pragma unroll
+          for (int c = 0; c < NC; ++c) other[p][c] = lds[threadIdx.x + d][p * NC + c];
+      }
+      __syncthreads();
+    }
+    if ((q & (2 * d - 1)) == 0 && q + d < count) {
+#pragma unroll
+      for (int p = 0; p < NP; ++p) mm_add<T, NC, APOL>(acc[p], other[p], acc[p]);
+    }
+  }
+}
+
+// Combine the per-component products of B left to right and store one output
+// (zero components as +0, Simple-Renorm's padding).
+template <typename T, int NC, int NP, int APOL>
+__device__ __forceinline__ void sk_store(const T (&acc)[NP][NC], T *__restrict__ C, int64_t MN, int64_t o) {
+  T r[NC];
+#pragma unroll
+  for (int c = 0; c < NC; ++c) r[c] = acc[0][c];
+#pragma unroll
+  for (int p = 1; p < NP; ++p) mm_add<T, NC, APOL>(r, acc[p], r);
+#pragma unroll
+  for (int c = 0; c < NC; ++c) C[c * MN + o] = (r[c] != T(0)) ? r[c] : T(0);
+}
+
+// One MM-MCN term into the accumulators: acc[p] = Add-MCN(acc[p], ScalingN(mc, v_p)).
+// FIRST: acc[p] = ScalingN(mc, v_p).
+template <typename T, int NC, bool AMC, bool BMC, int SPOL, int APOL, bool FIRST>
+__device__ __forceinline__ void sk_term(T (&acc)[(AMC && BMC) ? NC : 1][NC], const T (&a)[AMC ? NC : 1],
+                                        const T (&b)[BMC ? NC : 1]) {
+  constexpr int NP = (AMC && BMC) ? NC : 1;
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    const T v = AMC ? b[BMC ? p : 0] : a[0];
+    T h[NC + 1];
+    if constexpr (AMC)
+      scaling_terms<T, NC>(a, v, h);
+    else
+      scaling_terms<T, NC>(b, v, h);
+    if constexpr (FIRST) {
+      if (__builtin_expect(sr_try<T, NC, SPOL>(h, acc[p], v == T(0)), 0)) compact_nz<T, NC + 1, NC>(h, acc[p]);
+    } else {
+      T term[NC];
+      if (__builtin_expect(sr_try<T, NC, SPOL>(h, term, v == T(0)), 0)) compact_nz<T, NC + 1, NC>(h, term);
+      add_terms<T, NC>(acc[p], term, h);
+      if (__builtin_expect(sr_try<T, NC, APOL>(h, acc[p]), 0)) compact_nz<T, NC + 1, NC>(h, acc[p]);
+    }
+  }
+}
+
+// Phase 1: slice sums and the in-workgroup tree levels.  A: [NA][M][K], B: [NB][K][N].
+// G == 1: the result goes to C [NC][M*N].  G > 1: the group roots go to
+// W [G][NP][NC][M*N].
+template <typename T, int NC, bool AMC, bool BMC, int SPOL, int APOL>
+__global__ __launch_bounds__(SK_THREADS) void sk_kernel(const T *__restrict__ A, const T *__restrict__ B,
+                                                        T *__restrict__ C, T *__restrict__ W, int64_t M, int64_t N,
+                                                        int64_t K, int64_t S, int KS, int G) {
+  constexpr int NA = AMC ? NC : 1;
+  constexpr int NB = BMC ? NC : 1;
+  constexpr int NP = (AMC && BMC) ? NC : 1;
+  __shared__ T lds[SK_THREADS][NP * NC];
+
+  const int64_t MN = M * N;
+  const int q = threadIdx.x & (KS - 1);
+  const int64_t o = (int64_t)blockIdx.x * (SK_THREADS / KS) + threadIdx.x / KS;
+  const int64_t s = (int64_t)blockIdx.y * KS + q;
+  const int64_t i = o / N, j = o % N;
+
+  T acc[NP][NC];
+#pragma unroll
+  for (int p = 0; p < NP; ++p)
+#pragma unroll
+    for (int c = 0; c < NC; ++c) acc[p][c] = T(0);
+
+  if (o < MN && s < S) {
+    const T *Ai = A + i * K;
+    const T *Bj = B + j;
+    auto load = [&](int64_t k, T (&a)[NA], T (&b)[NB]) {
+#pragma unroll
+      for (int c = 0; c < NA; ++c) a[c] = Ai[c * M * K + k];
+#pragma unroll
+      for (int c = 0; c < NB; ++c) b[c] = Bj[c * K * N + k * N];
+    };
+    int64_t k = s;
+    {
+      T a[NA], b[NB];
+      load(k, a, b);
+      sk_term<T, NC, AMC, BMC, SPOL, APOL, true>(acc, a, b);
+      k += S;
+    }
+    // Loads of SK_UNROLL steps are issued before their arithmetic.
+    for (; k + (SK_UNROLL - 1) * S < K; k += SK_UNROLL * S) {
+      T a[SK_UNROLL][NA], b[SK_UNROLL][NB];
+#pragma unroll
+      for (int u = 0; u < SK_UNROLL; ++u) load(k + u * S, a[u], b[u]);
+#pragma unroll
+      for (int u = 0; u < SK_UNROLL; ++u) sk_term<T, NC, AMC, BMC, SPOL, APOL, false>(acc, a[u], b[u]);
+    }
+    for (; k < K; k += S) {
+      T a[NA], b[NB];
+      load(k, a, b);
+      sk_term<T, NC, AMC, BMC, SPOL, APOL, false>(acc, a, b);
+    }
+  }
+
+  const int64_t left = S - (int64_t)blockIdx.y * KS;
+  const int count = left < KS ? (int)left : KS;
+  group_tree<T, NC, NP, APOL>(acc, q, KS, count, lds);
+
+  if (q == 0 && o < MN) {
+    if (G == 1) {
+      sk_store<T, NC, NP, APOL>(acc, C, MN, o);
+    } else {
+#pragma unroll
+      for (int p = 0; p < NP; ++p)
+#pragma unroll
+        for (int c = 0; c < NC; ++c) W[(((int64_t)blockIdx.y * NP + p) * NC + c) * MN + o] = acc[p][c];
+    }
+  }
+}
+
+// Phase 2: the remaining tree levels over the G group roots of each output, GW lanes
+// (GW = G rounded up to a power of two) per output.
+template <typename T, int NC, int NP, int APOL>
+__global__ __launch_bounds__(SK_THREADS) void sk_reduce_kernel(const T *__restrict__ W, T *__restrict__ C,
+                                                               int64_t MN, int G, int GW) {
+  __shared__ T lds[SK_THREADS][NP * NC];
+  const int q = threadIdx.x & (GW - 1);
+  const int64_t o = (int64_t)blockIdx.x * (SK_THREADS / GW) + threadIdx.x / GW;
+  T acc[NP][NC];
+#pragma unroll
+  for (int p = 0; p < NP; ++p)
+#pragma unroll
+    for (int c = 0; c < NC; ++c) acc[p][c] = (o < MN && q < G) ? W[(((int64_t)q * NP + p) * NC + c) * MN + o] : T(0);
+  group_tree<T, NC, NP, APOL>(acc, q, GW, G, lds);
+  if (q == 0 && o < MN) sk_store<T, NC, NP, APOL>(acc, C, MN, o);
+}
+
+static int pow2_at_least(int64_t v) {
+  int p = 1;
+  while (p < v) p <<= 1;
+  return p;
+}
+
+int64_t splitk_default_slices(int64_t M, int64_t N, int64_t K) {
+  const int64_t MN = M * N;
+  if (MN <= 0 || K <= 0) return 1;
+  int64_t s = ((int64_t)SPLITK_TARGET_LANES + MN - 1) / MN;
+  const int64_t by_k = K / 8 > 1 ? K / 8 : 1;
+  if (s > by_k) s = by_k;
+  if (s > SPLITK_MAX_SLICES) s = SPLITK_MAX_SLICES;
+  return s < 1 ? 1 : s;
+}
+
+void splitk_shape(int64_t S, int *KS, int *G) {
+  const int ks = pow2_at_least(S < SK_THREADS ? S : SK_THREADS);
+  *KS = ks;
+  *G = (int)((S + ks - 1) / ks);
+}
+
+template <typename T, int NC, bool AMC, bool BMC>
+static hipError_t sk_launch(int64_t M, int64_t N, int64_t K, const void *A, const void *B, int64_t S, void *W, void *C,
+                            hipStream_t s) {
+  constexpr int NP = (AMC && BMC) ? NC : 1;
+  // Simple-Renorm fast-path policies as in the sequential product (they change speed only)
+  constexpr int SPOL = sizeof(T) == 4 ? SR_FULL : (NC == 2 ? SR_NET : SR_HEAD);
+  constexpr int APOL = sizeof(T) == 4 ? SR_FULL : SR_SELECT;
+  const int64_t MN = M * N;
+  int KS, G;
+  splitk_shape(S, &KS, &G);
+  dim3 grid((unsigned)((MN + (SK_THREADS / KS) - 1) / (SK_THREADS / KS)), (unsigned)G);
+  hipLaunchKernelGGL((sk_kernel<T, NC, AMC, BMC, SPOL, APOL>), grid, dim3(SK_THREADS), 0, s, (const T *)A,
+                     (const T *)B, (T *)C, (T *)W, M, N, K, S, KS, G);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || G == 1) return e;
+  const int GW = pow2_at_least(G);
+  dim3 grid2((unsigned)((MN + (SK_THREADS / GW) - 1) / (SK_THREADS / GW)));
+  hipLaunchKernelGGL((sk_reduce_kernel<T, NC, NP, APOL>), grid2, dim3(SK_THREADS), 0, s, (const T *)W, (T *)C, MN, G,
+                     GW);
+  return hipGetLastError();
+}
+
+template <typename T, int NC>
+static hipError_t sk_kinds(int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B, int b_mc,
+                           int64_t S, void *W, void *C, hipStream_t s) {
+  if (a_mc && b_mc) return sk_launch<T, NC, true, true>(M, N, K, A, B, S, W, C, s);
+  if (a_mc) return sk_launch<T, NC, true, false>(M, N, K, A, B, S, W, C, s);
+  return sk_launch<T, NC, false, true>(M, N, K, A, B, S, W, C, s);
+}
+
+template <typename T>
+static hipError_t sk_dispatch(int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B,
+                              int b_mc, int64_t S, void *W, void *C, hipStream_t s) {
+  switch (nc) {
+    case 1: return sk_kinds<T, 1>(M, N, K, A, a_mc, B, b_mc, S, W, C, s);
+    case 2: return sk_kinds<T, 2>(M, N, K, A, a_mc, B, b_mc, S, W, C, s);
+    case 3: return sk_kinds<T, 3>(M, N, K, A, a_mc, B, b_mc, S, W, C, s);
+    case 4: return sk_kinds<T, 4>(M, N, K, A, a_mc, B, b_mc, S, W, C, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_matmul_splitk(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc,
+                                const void *B, int b_mc, int64_t S, void *W, void *C, hipStream_t stream) {
+  if (dtype == 0) return sk_dispatch<_Float16>(nc, M, N, K, A, a_mc, B, b_mc, S, W, C, stream);
+  return sk_dispatch<float>(nc, M, N, K, A, a_mc, B, b_mc, S, W, C, stream);
+}
+
+}  // namespace mcf

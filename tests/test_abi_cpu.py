@@ -79,3 +79,43 @@ def test_validation_matrix(L):
     assert L.mc_linear_fwd(0, 3, 4, 4, 4, None, b, None, c, None) == MCF_E_NULL
     assert L.mc_linear_fwd(0, 3, 4, 4, 4, a, b, P(0x300000), c, None) == MCF_E_ALIAS
     assert L.mc_linear_fwd(0, 3, 0, 4, 4, None, None, None, None, None) == MCF_OK
+
+
+def test_validation_splitk(L):
+    a, b, c, w = P(0x100000), P(0x200000), P(0x300000), P(0x400000)
+    f = L.mc_matmul_splitk
+    f.restype = ctypes.c_int
+    f.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, P, ctypes.c_int, P,
+                  ctypes.c_int, ctypes.c_int64, P, ctypes.c_int64, P, P]
+    ws = L.mc_matmul_splitk_workspace
+    ws.restype = ctypes.c_int64
+    ws.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
+                   ctypes.c_int, ctypes.c_int64]
+    sl = L.mc_matmul_splitk_slices
+    sl.restype = ctypes.c_int64
+    sl.argtypes = [ctypes.c_int64] * 3
+    # default slice count: about 2^18 lanes, at most K / 8, at most 65536, at least 1
+    assert sl(64, 64, 64) == 8
+    assert sl(4096, 1, 4096) == 64
+    assert sl(1, 1, 1 << 24) == 65536
+    assert sl(1, 1, 100) == 12
+    assert sl(1024, 1024, 1024) == 1
+    assert sl(1, 1, 3) == 1
+    assert sl(-1, 1, 3) == MCF_E_SHAPE
+    # workspace: none while the slices fit one workgroup (<= 256), else G x planes
+    assert ws(1, 3, 4, 4, 4096, 1, 0, 256) == 0
+    assert ws(1, 3, 4, 4, 4096, 1, 0, 257) == 2 * 1 * 3 * 16 * 4
+    assert ws(0, 2, 4, 4, 4096, 1, 1, 1024) == 4 * 2 * 2 * 16 * 2
+    assert ws(1, 3, 4, 4, 4096, 1, 0, 1 << 17) == MCF_E_ARG
+    assert ws(1, 3, 4, 4, 100, 1, 0, 1000) == 0  # capped at K = 100 slices
+    assert f(1, 3, 4, 4, 4096, a, 0, b, 0, 16, None, 0, c, None) == MCF_E_ARG
+    assert f(1, 7, 4, 4, 4096, a, 1, b, 0, 16, None, 0, c, None) == MCF_E_NC
+    assert f(1, 3, 4, 4, -1, a, 1, b, 0, 16, None, 0, c, None) == MCF_E_SHAPE
+    assert f(1, 3, 1 << 16, 1 << 16, 4, a, 1, b, 0, 16, None, 0, c, None) == MCF_E_SHAPE  # M N > 2^31
+    assert f(1, 3, 0, 4, 4096, None, 1, None, 0, 16, None, 0, None, None) == MCF_OK
+    assert f(1, 3, 4, 4, 4096, a, 1, b, 0, 1024, None, 0, c, None) == MCF_E_NULL  # workspace needed
+    need = ws(1, 3, 4, 4, 4096, 1, 0, 1024)
+    assert f(1, 3, 4, 4, 4096, a, 1, b, 0, 1024, w, need - 1, c, None) == MCF_E_ARG
+    assert f(1, 3, 4, 4, 4096, a, 1, b, 0, 1024, P(0x300000 + 4), need, c, None) == MCF_E_ALIAS
+    assert f(1, 3, 4, 4, 4096, a, 1, b, 0, 1024, a, need, c, None) == MCF_E_ALIAS
+    assert f(1, 3, 4, 4, 4096, a, 1, b, 0, 16, None, 0, P(0x100000 + 8), None) == MCF_E_ALIAS
