@@ -90,8 +90,10 @@ int mc_div(int dtype, int nc, int64_t n, const void *x, int x_mc, const void *y,
 
 /* Exponential, Exp-MCN (Appendix A.2.1): h = exp(x_0) (one component), then for
  * i = 1 .. nc-1, h = ScalingN(h, exp(x_i), expand) growing h by one component per
- * step.  The component exponential is correctly rounded.  Provided for MCF_F16
- * (MCF_F32 returns MCF_E_DTYPE).  x, out: [nc][n]. */
+ * step.  The component exponential is correctly rounded in both formats (binary16
+ * by table lookup; binary32 from a binary64 evaluation, with a double-double one
+ * where that lies too close to a rounding boundary).  x, out: [nc][n]; out == x
+ * allowed. */
 int mc_exp(int dtype, int nc, int64_t n, const void *x, void *out, void *stream);
 
 /* Renormalization (Appendix A.2.1).

@@ -63,6 +63,8 @@ def lib() -> ctypes.CDLL:
         L.mcf_oracle_f16_encode.argtypes = [dbl]
         L.mcf_oracle_binop_array.restype = None
         L.mcf_oracle_binop_array.argtypes = [ci, ci, i64, vp, vp, vp]
+        L.mcf_oracle_exp32_near_ties.restype = i64
+        L.mcf_oracle_exp32_near_ties.argtypes = [dbl, vp, i64]
         L.mcf_oracle_eft_array.restype = None
         L.mcf_oracle_eft_array.argtypes = [ci, ci, i64, vp, vp, vp, vp]
         L.mcf_oracle_elementwise.restype = ci
@@ -146,6 +148,15 @@ def two_prod_err(fmt, a, b):
 def fl_exp(fmt, a):
     """Correctly rounded component exponential."""
     return _binop(fmt, 5, a)
+
+
+def exp32_near_ties(rel_margin: float, max_out: int = 4096):
+    """binary32 inputs x (as uint32 bit patterns) whose long double e^x lies within
+    rel_margin (relative) of a binary32 rounding boundary; scans every input with
+    2^-30 <= |x| <= 105.  Returns (count, patterns[:min(count, max_out)])."""
+    out = np.zeros(max_out, dtype=np.uint32)
+    n = int(lib().mcf_oracle_exp32_near_ties(float(rel_margin), _ptr(out), max_out))
+    return n, out[:min(n, max_out)]
 
 
 def two_sum(fmt, a, b):

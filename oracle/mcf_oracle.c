@@ -366,6 +366,40 @@ void mcf_oracle_binop_array(int f, int op, int64_t n, const double *a, const dou
   }
 }
 
+/* Pinning aid for the binary32 exponential.  fl_exp rounds the long double e^x of
+ * expl to binary32; that is the correctly rounded result unless e^x lies closer to a
+ * binary32 rounding boundary than expl's error.  This scans every binary32 x with
+ * 2^-30 <= |x| <= 105 (outside that range e^x rounds to 1, or to 0 or infinity, far
+ * from any boundary) and reports the x whose expl value, moved by the relative amount
+ * rel_margin either way, rounds to two different binary32 values.  Up to max_out bit
+ * patterns go to out; the return value is how many there are. */
+static double round_ld_f32(long double v) {
+  double hi = (double)v;
+  long double lo = v - (long double)hi;
+  return round_to(FMT_F32, hi, lo > 0 ? 1 : (lo < 0 ? -1 : 0));
+}
+
+int64_t mcf_oracle_exp32_near_ties(double rel_margin, uint32_t *out, int64_t max_out) {
+  int64_t count = 0;
+#pragma omp parallel for schedule(dynamic, 1 << 16) reduction(+ : count)
+  for (int64_t b = 0; b < ((int64_t)1 << 32); ++b) {
+    uint32_t bits = (uint32_t)b;
+    float xf;
+    memcpy(&xf, &bits, 4);
+    double ax = fabs((double)xf);
+    if (!(ax >= 0x1p-30 && ax <= 105.0)) continue;
+    long double e = expl((long double)xf);
+    long double m = (long double)rel_margin;
+    if (round_ld_f32(e * (1.0L - m)) != round_ld_f32(e * (1.0L + m))) {
+      int64_t slot;
+#pragma omp atomic capture
+      slot = count++;
+      if (slot < max_out) out[slot] = bits;
+    }
+  }
+  return count;
+}
+
 /* Two-Sum / Two-Prod on arrays of doubles: outputs s (or p) and e. */
 void mcf_oracle_eft_array(int f, int prod, int64_t n, const double *a, const double *b, double *s, double *e) {
 #pragma omp parallel for schedule(static)

@@ -101,12 +101,12 @@ int mc_div(int dtype, int nc, int64_t n, const void *x, int x_mc, const void *y,
 int mc_exp(int dtype, int nc, int64_t n, const void *x, void *out, void *stream) {
   int st = check_common(dtype, nc, n);
   if (st != MCF_OK) return st;
-  if (dtype != MCF_F16) return MCF_E_DTYPE;
   if (n == 0) return MCF_OK;
   if (!x || !out) return MCF_E_NULL;
   const int64_t b = nc * n * elem_size(dtype);
   if (bad_alias(out, b, x, b)) return MCF_E_ALIAS;
-  return hip_status(mcf::launch_exp_f16(nc, n, x, out, (hipStream_t)stream));
+  if (dtype == MCF_F16) return hip_status(mcf::launch_exp_f16(nc, n, x, out, (hipStream_t)stream));
+  return hip_status(mcf::launch_exp_f32(nc, n, x, out, (hipStream_t)stream));
 }
 
 int mc_renorm(int dtype, int nc_in, int nc_out, int64_t n, const void *x, void *out, int mode, void *stream) {

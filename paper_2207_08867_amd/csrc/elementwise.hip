@@ -1,5 +1,6 @@
 // elementwise.hip -- elementwise MC kernels: Add-MCN / Grow-ExpN, ScalingN /
-// Mult-MCN, Div-MCN / DivN, Renormalize / Simple-Renorm, and Exp-MCN (binary16).
+// Mult-MCN, Div-MCN / DivN, Renormalize / Simple-Renorm, and Exp-MCN (binary16 by
+// table lookup, binary32 by a correctly rounded evaluation).
 //
 // Data are component-major planes; each thread moves 16 bytes per plane per step
 // (8 binary16 or 4 binary32 elements) with dwordx4 loads and stores, so one wave
@@ -11,6 +12,7 @@
 #include <atomic>
 #include <mutex>
 
+#include "exp32.hpp"
 #include "mcf_arith.hpp"
 #include "mcf_internal.hpp"
 
@@ -53,6 +55,20 @@ __device__ __forceinline__ void store_pack(T *p, const Pack<T, W> &r) {
   }
 }
 
+// Exp-MCN for one element from the component exponentials ex[0..N-1]:
+// h = (ex_0), then h = ScalingN(h, ex_i) with expand, one component longer per step.
+template <typename T, int N, int M>
+__device__ __forceinline__ void exp_chain(const T (&h)[M], const T (&ex)[N], T (&out)[N]) {
+  if constexpr (M == N) {
+#pragma unroll
+    for (int c = 0; c < N; ++c) out[c] = h[c];
+  } else {
+    T g[M + 1];
+    scaling_n<T, M, M + 1>(h, ex[M], g);
+    exp_chain<T, N, M + 1>(g, ex, out);
+  }
+}
+
 // The algorithm applied to one element.  Plain operands arrive in slot 0 with the
 // other slots +0, which is exactly the zero padding DivN and (MC, T) division use.
 template <typename T, int NC, int OP, bool XMC, bool YMC, int NCOUT>
@@ -73,6 +89,13 @@ __device__ __forceinline__ void elem(const T (&a)[NC], const T (&b)[NC], T (&r)[
       scaling_n<T, NC, NC>(b, a[0], r);
   } else if constexpr (OP == EW_DIV) {
     div_mcn<T, NC>(a, b, r);
+  } else if constexpr (OP == EW_EXP) {
+    static_assert(sizeof(T) == 4, "binary16 Exp-MCN has its own kernel");
+    T ex[NC];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) ex[c] = exp32_cr(a[c]);
+    const T h0[1] = {ex[0]};
+    exp_chain<T, NC, 1>(h0, ex, r);
   } else if constexpr (OP == EW_RENORM) {
     renormalize<T, NC, NCOUT>(a, r);
   } else {
@@ -87,7 +110,7 @@ __device__ __forceinline__ void elem(const T (&a)[NC], const T (&b)[NC], T (&r)[
 template <typename T, int NC, int OP, bool XMC, bool YMC, int NCOUT, int W, int U>
 __device__ __forceinline__ void ew_chunks(const T *x, const T *y, T *out, int64_t n, const int64_t (&e0)[U]) {
   constexpr int XN = XMC ? NC : 1;
-  constexpr int YN = (OP == EW_RENORM || OP == EW_SIMPLE_RENORM) ? 0 : (YMC ? NC : 1);
+  constexpr int YN = (OP == EW_RENORM || OP == EW_SIMPLE_RENORM || OP == EW_EXP) ? 0 : (YMC ? NC : 1);
   Pack<T, W> xa[U][XN];
   Pack<T, W> ya[U][YN > 0 ? YN : 1];
 #pragma unroll
@@ -284,19 +307,6 @@ static hipError_t exp_table(_Float16 **tab, hipStream_t s) {
 
 constexpr int EXP_THREADS = 1024;
 
-// Exp-MCN for one element from the component exponentials ex[0..N-1]:
-// h = (ex_0), then h = ScalingN(h, ex_i) with expand, one component longer per step.
-template <int N, int M>
-__device__ __forceinline__ void exp_chain(const _Float16 (&h)[M], const _Float16 (&ex)[N], _Float16 (&out)[N]) {
-  if constexpr (M == N) {
-#pragma unroll
-    for (int c = 0; c < N; ++c) out[c] = h[c];
-  } else {
-    _Float16 g[M + 1];
-    scaling_n<_Float16, M, M + 1>(h, ex[M], g);
-    exp_chain<N, M + 1>(g, ex, out);
-  }
-}
 
 // The LDS copy of the table covers |x| < 32 (exponent fields 0..19 of both signs, 80
 // KiB); outside it e^x is +inf (x >= 32), +0 (x <= -32) or NaN, which is what the
@@ -369,7 +379,7 @@ __global__ __launch_bounds__(EXP_THREADS) void exp16_kernel(const _Float16 *x, _
         }
         _Float16 h0[1] = {ex[0]};
         _Float16 r[NC];
-        exp_chain<NC, 1>(h0, ex, r);
+        exp_chain<_Float16, NC, 1>(h0, ex, r);
 #pragma unroll
         for (int c = 0; c < NC; ++c) res[u][c].v[w] = r[c];
       }
@@ -414,6 +424,16 @@ static hipError_t exp16_launch(int64_t n, const void *x, void *out, const _Float
     hipLaunchKernelGGL((exp16_kernel<NC, 1>), dim3(blocks), dim3(EXP_THREADS), 0, s, (const _Float16 *)x,
                        (_Float16 *)out, n, tab);
   return hipGetLastError();
+}
+
+hipError_t launch_exp_f32(int nc, int64_t n, const void *x, void *out, hipStream_t stream) {
+  switch (nc) {
+    case 1: return ew_launch<float, 1, EW_EXP, true, false, 1>(n, x, nullptr, out, stream);
+    case 2: return ew_launch<float, 2, EW_EXP, true, false, 2>(n, x, nullptr, out, stream);
+    case 3: return ew_launch<float, 3, EW_EXP, true, false, 3>(n, x, nullptr, out, stream);
+    case 4: return ew_launch<float, 4, EW_EXP, true, false, 4>(n, x, nullptr, out, stream);
+  }
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_exp_f16(int nc, int64_t n, const void *x, void *out, hipStream_t stream) {

@@ -8,7 +8,7 @@
 
 namespace mcf {
 
-enum EwOp { EW_ADD = 0, EW_MUL = 1, EW_DIV = 2, EW_RENORM = 3, EW_SIMPLE_RENORM = 4 };
+enum EwOp { EW_ADD = 0, EW_MUL = 1, EW_DIV = 2, EW_RENORM = 3, EW_SIMPLE_RENORM = 4, EW_EXP = 5 };
 
 // Elementwise binary (add/mul/div) and renormalization launchers.  dtype 0 = binary16,
 // 1 = binary32.  For renormalization y is unused, nc is nc_in.
@@ -18,6 +18,9 @@ hipError_t launch_elementwise(int dtype, int op, int nc, int nc_out, int64_t n, 
 // Exp-MCN over binary16 components; builds the per-device exponential table on the
 // first call on a device.
 hipError_t launch_exp_f16(int nc, int64_t n, const void *x, void *out, hipStream_t stream);
+
+// Exp-MCN over binary32 components (correctly rounded component exponential).
+hipError_t launch_exp_f32(int nc, int64_t n, const void *x, void *out, hipStream_t stream);
 
 // C[nc][M][N] = A x B.  b_trans: B is stored as [planes][N][K] (a linear layer's
 // weight) instead of [planes][K][N].  bias: [nc][N] MC bias added with Add-MCN, or

@@ -89,12 +89,35 @@ def test_renorm_parity(mcf, orc, dt, nc, mode):
         assert_bits(got, want, f"renorm mode={mode} {dt.__name__} {nc}->{nc_out}")
 
 
+@pytest.mark.parametrize("dt", DTS)
 @pytest.mark.parametrize("nc", [1, 2, 3, 4])
-def test_exp_parity(mcf, orc, nc):
+def test_exp_parity(mcf, orc, dt, nc):
     n = 50_001
-    x, _ = inputs.elementwise_inputs("exp", n, nc, np.float16, seed=300 + nc)
+    x, _ = inputs.elementwise_inputs("exp", n, nc, dt, seed=300 + nc)
     got = to_host(mcf.mc_exp(to_dev(x), nc=nc))
-    assert_bits(got, orc.exp(x, nc=nc), f"exp nc={nc}")
+    assert_bits(got, orc.exp(x, nc=nc), f"exp {dt.__name__} nc={nc}")
+
+
+def test_exp32_component_exhaustive(mcf, orc):
+    """The binary32 component exponential (Exp-MCN at nc = 1) on every binary32 input
+    with 2^-30 <= |x| <= 105 -- the range where e^x is neither 1, 0 nor infinite
+    after rounding, and where inputs whose binary64 e^x lies close to a rounding
+    boundary take the double-double path -- in chunks of 2^26, plus every 997th bit
+    pattern over the whole encoding space (zeros, subnormals, huge, infinities,
+    NaNs)."""
+    lo, hi = 0x30800000, 0x42D20001  # 2^-30 .. 105.0
+    chunk = 1 << 26
+    for sign in (0, 0x80000000):
+        for start in range(lo, hi, chunk):
+            bits = np.arange(start, min(start + chunk, hi), dtype=np.uint32) | np.uint32(sign)
+            x = bits.view(np.float32)[None]
+            print(f"exp32 exhaustive: sign {sign >> 31} patterns {start:#x}..", flush=True)
+            got = to_host(mcf.mc_exp(to_dev(x), nc=1))
+            assert_bits(got, orc.exp(x, nc=1), f"exp32 from {start | sign:#x}")
+    bits = np.arange(0, 1 << 32, 997, dtype=np.uint64).astype(np.uint32)
+    x = bits.view(np.float32)[None]
+    got = to_host(mcf.mc_exp(to_dev(x), nc=1))
+    assert_bits(got, orc.exp(x, nc=1), "exp32 strided")
 
 
 def test_exp_component_exhaustive(mcf, orc):

@@ -139,3 +139,30 @@ def test_exp_f32_sample_correctly_rounded(orc):
             cands = [Fraction(float(v)) for v in (f, np.nextafter(f, np.float32(np.inf)), np.nextafter(f, np.float32(0)))]
             best = min(cands, key=lambda c: abs(c - E))
             assert Fraction(gi) == best, xi
+
+
+def test_exp_f32_exhaustive(orc):
+    """Every binary32 input with 2^-30 <= |x| <= 105 (outside that range e^x rounds
+    to 1, 0 or infinity far from any rounding boundary): the oracle rounds expl's
+    long double e^x, whose error (a few long double ulps, about 2^-62 relative) can
+    only matter where e^x lies that close to a binary32 rounding boundary.  The scan
+    lists every input whose expl value is within 2^-44 of one; all other inputs
+    round correctly, and the listed ones are checked against a 60-digit decimal
+    exponential, which also shows none lies within 2^-58."""
+    n, pats = orc.exp32_near_ties(2.0 ** -44, max_out=8192)
+    assert 0 < n <= 8192
+    x = pats.view(np.float32).astype(np.float64)
+    got = orc.fl_exp(F32, x)
+    closest = 1.0
+    with decimal.localcontext() as ctx:
+        ctx.prec = 60
+        for xi, gi in zip(x, got):
+            E = Fraction(decimal.Decimal(float(xi)).exp())
+            f = np.float32(float(E))
+            cands = sorted({Fraction(float(v)) for v in (np.nextafter(f, np.float32(0)), f,
+                                                         np.nextafter(f, np.float32(np.inf)))})
+            best = min(cands, key=lambda c: abs(c - E))
+            assert Fraction(gi) == best, xi
+            mids = [(a + b) / 2 for a, b in zip(cands, cands[1:])]
+            closest = min(closest, float(min(abs(m - E) for m in mids) / E))
+    assert closest > 2.0 ** -58
