@@ -140,6 +140,9 @@ struct Lane {
   template <int PMASK>
   __device__ __forceinline__ void run(const T (*As)[KT][BM], const T (*Bs)[KT][BN], int kk0, int kt, int tx,
                                       int ty) {
+    // two steps per loop iteration, so the accumulators keep their registers across
+    // the back edge instead of being copied
+#pragma unroll 2
     for (int kk = kk0; kk < kt; ++kk) {
       Ops o;
       o.load(As, Bs, kk, tx, ty);
