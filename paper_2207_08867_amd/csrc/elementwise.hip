@@ -319,6 +319,11 @@ __device__ __forceinline__ unsigned exp16_bits(_Float16 v) {
   return b;
 }
 
+// |x| <= 2^-12 (binary16 magnitude bits <= 0x0C00): e^x lies in
+// [1 - 2^-12 + 2^-26, 1 + 2^-12 + 2^-24], inside the interval (1 - 2^-12, 1 + 2^-11)
+// of reals that round to 1, so its binary16 exponential is exactly 1.
+constexpr unsigned EXP16_ONE_MAG = 0x0C00u;
+
 // Table slot of an in-range bit pattern: positive half at 0, negative half after it.
 __device__ __forceinline__ _Float16 exp16_fast(const _Float16 *tab, unsigned b) {
   return tab[(b & 0x7fffu) + (b >> 15) * (unsigned)EXP_LDS_MAG];
@@ -359,30 +364,67 @@ __global__ __launch_bounds__(EXP_THREADS) void exp16_kernel(const _Float16 *x, _
     for (int u = 0; u < UU; ++u)
 #pragma unroll
       for (int c = 0; c < NC; ++c) xa[u][c] = load_pack<_Float16, WW>(x + c * n + e0[u]);
+    if constexpr (NC == 1) {
 #pragma unroll
-    for (int u = 0; u < UU; ++u)
+      for (int u = 0; u < UU; ++u)
 #pragma unroll
-      for (int w = 0; w < WW; ++w) {
-        _Float16 ex[NC];
-        unsigned bits[NC], big = 0;
-#pragma unroll
-        for (int c = 0; c < NC; ++c) {
-          bits[c] = exp16_bits(xa[u][c].v[w]);
-          big = big > (bits[c] & 0x7fffu) ? big : (bits[c] & 0x7fffu);
+        for (int w = 0; w < WW; ++w) {
+          const unsigned b = exp16_bits(xa[u][0].v[w]);
+          res[u][0].v[w] = (b & 0x7fffu) < (unsigned)EXP_LDS_MAG ? exp16_fast(tab, b) : exp16_any(tab, b);
         }
-        if (__builtin_expect(big < (unsigned)EXP_LDS_MAG, 1)) {
+    } else {
+      // All components but the last: h = (e^x_0), grown by ScalingN(expand) to nc-1
+      // components.  `last_one` stays set while every element of the lane has a last
+      // component with |x| <= 2^-12 (its exponential is exactly 1 in binary16) and a
+      // finite h: ScalingN of a compact h by exactly 1 with expand is h followed by +0.
+      _Float16 hh[UU][WW][NC - 1];
+      bool last_one = true;
 #pragma unroll
-          for (int c = 0; c < NC; ++c) ex[c] = exp16_fast(tab, bits[c]);
-        } else {
+      for (int u = 0; u < UU; ++u)
 #pragma unroll
-          for (int c = 0; c < NC; ++c) ex[c] = exp16_any(tab, bits[c]);
+        for (int w = 0; w < WW; ++w) {
+          _Float16 ex[NC - 1];
+          unsigned bits[NC - 1], big = 0;
+#pragma unroll
+          for (int c = 0; c < NC - 1; ++c) {
+            bits[c] = exp16_bits(xa[u][c].v[w]);
+            big = big > (bits[c] & 0x7fffu) ? big : (bits[c] & 0x7fffu);
+          }
+          if (__builtin_expect(big < (unsigned)EXP_LDS_MAG, 1)) {
+#pragma unroll
+            for (int c = 0; c < NC - 1; ++c) ex[c] = exp16_fast(tab, bits[c]);
+          } else {
+#pragma unroll
+            for (int c = 0; c < NC - 1; ++c) ex[c] = exp16_any(tab, bits[c]);
+          }
+          const _Float16 h0[1] = {ex[0]};
+          exp_chain<_Float16, NC - 1, 1>(h0, ex, hh[u][w]);
+          const unsigned lastmag = exp16_bits(xa[u][NC - 1].v[w]) & 0x7fffu;
+          last_one = last_one && lastmag <= EXP16_ONE_MAG && __builtin_isfinite((float)hh[u][w][0]);
         }
-        _Float16 h0[1] = {ex[0]};
-        _Float16 r[NC];
-        exp_chain<_Float16, NC, 1>(h0, ex, r);
+      if (__all(last_one)) {
 #pragma unroll
-        for (int c = 0; c < NC; ++c) res[u][c].v[w] = r[c];
+        for (int u = 0; u < UU; ++u)
+#pragma unroll
+          for (int w = 0; w < WW; ++w) {
+#pragma unroll
+            for (int c = 0; c < NC - 1; ++c) res[u][c].v[w] = hh[u][w][c];
+            res[u][NC - 1].v[w] = _Float16(0);
+          }
+      } else {
+#pragma unroll
+        for (int u = 0; u < UU; ++u)
+#pragma unroll
+          for (int w = 0; w < WW; ++w) {
+            const unsigned b = exp16_bits(xa[u][NC - 1].v[w]);
+            const _Float16 e = (b & 0x7fffu) < (unsigned)EXP_LDS_MAG ? exp16_fast(tab, b) : exp16_any(tab, b);
+            _Float16 g[NC];
+            scaling_n<_Float16, NC - 1, NC>(hh[u][w], e, g);
+#pragma unroll
+            for (int c = 0; c < NC; ++c) res[u][c].v[w] = g[c];
+          }
       }
+    }
 #pragma unroll
     for (int u = 0; u < UU; ++u)
 #pragma unroll

@@ -221,19 +221,26 @@ __global__ __launch_bounds__(MM_THREADS) void mm_kernel(const T *__restrict__ A,
   Lane<T, NC, AMC, BMC, TM, TN, KT, BM, BN, SPOL, APOL, GROUP> lane;
   auto &acc = lane.acc;
 
-  for (int64_t k0 = 0; k0 < K; k0 += KT) {
-    const int kt = (int)((K - k0) < KT ? (K - k0) : KT);
-    // stage A tile: rows m0..m0+BM-1, reduction steps k0..k0+KT-1
-    for (int idx = threadIdx.x; idx < BM * KT; idx += MM_THREADS) {
+  // Each thread stages A_PER elements of the A tile and B_PER of the B tile per
+  // component plane.  The next tile's global loads are issued into registers before
+  // the current tile's arithmetic, so their latency hides behind it; the registers
+  // go to LDS at the top of the next iteration.
+  constexpr int A_PER = (BM * KT + MM_THREADS - 1) / MM_THREADS;
+  constexpr int B_PER = (BN * KT + MM_THREADS - 1) / MM_THREADS;
+  T ra[A_PER][NA], rb[B_PER][NB];
+  auto fetch = [&](int64_t k0) {
+#pragma unroll
+    for (int t = 0; t < A_PER; ++t) {
+      const int idx = threadIdx.x + t * MM_THREADS;
       const int r = idx / KT, kk = idx % KT;
       const int64_t gm = m0 + r, gk = k0 + kk;
-      const bool ok = gm < M && gk < K;
+      const bool ok = idx < BM * KT && gm < M && gk < K;
 #pragma unroll
-      for (int c = 0; c < NA; ++c) As[c][kk][r] = ok ? A[c * M * K + gm * K + gk] : T(0);
+      for (int c = 0; c < NA; ++c) ra[t][c] = ok ? A[c * M * K + gm * K + gk] : T(0);
     }
-    // stage B tile, noting which of its component planes hold a non-zero value
-    int nonzero_planes = 0;
-    for (int idx = threadIdx.x; idx < BN * KT; idx += MM_THREADS) {
+#pragma unroll
+    for (int t = 0; t < B_PER; ++t) {
+      const int idx = threadIdx.x + t * MM_THREADS;
       int col, kk;
       if constexpr (BT) {
         col = idx / KT;
@@ -243,13 +250,38 @@ __global__ __launch_bounds__(MM_THREADS) void mm_kernel(const T *__restrict__ A,
         col = idx % BN;
       }
       const int64_t gn = n0 + col, gk = k0 + kk;
-      const bool ok = gn < N && gk < K;
+      const bool ok = idx < BN * KT && gn < N && gk < K;
 #pragma unroll
       for (int c = 0; c < NB; ++c) {
         const int64_t off = BT ? (c * N * K + gn * K + gk) : (c * K * N + gk * N + gn);
-        const T v = ok ? B[off] : T(0);
-        Bs[c][kk][col] = v;
-        if (v != T(0)) nonzero_planes |= 1 << c;
+        rb[t][c] = ok ? B[off] : T(0);
+      }
+    }
+  };
+
+  if (K > 0) fetch(0);
+  for (int64_t k0 = 0; k0 < K; k0 += KT) {
+    const int kt = (int)((K - k0) < KT ? (K - k0) : KT);
+    // registers -> LDS: A transposed to [k][m]; note which planes of B hold a non-zero
+    int nonzero_planes = 0;
+#pragma unroll
+    for (int t = 0; t < A_PER; ++t) {
+      const int idx = threadIdx.x + t * MM_THREADS;
+      if (idx < BM * KT) {
+#pragma unroll
+        for (int c = 0; c < NA; ++c) As[c][idx % KT][idx / KT] = ra[t][c];
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < B_PER; ++t) {
+      const int idx = threadIdx.x + t * MM_THREADS;
+      if (idx < BN * KT) {
+        const int col = BT ? idx / KT : idx % BN, kk = BT ? idx % KT : idx / BN;
+#pragma unroll
+        for (int c = 0; c < NB; ++c) {
+          Bs[c][kk][col] = rb[t][c];
+          if (rb[t][c] != T(0)) nonzero_planes |= 1 << c;
+        }
       }
     }
     int pmask = ALL;
@@ -259,6 +291,7 @@ __global__ __launch_bounds__(MM_THREADS) void mm_kernel(const T *__restrict__ A,
     } else {
       __syncthreads();
     }
+    if (k0 + KT < K) fetch(k0 + KT);  // next tile, in flight during this one
     int kk0 = 0;
     if (k0 == 0) {  // term k = 0 initialises the accumulators
       typename decltype(lane)::Ops o;

@@ -91,6 +91,38 @@ def test_config_1024_fp16(mcf, orc, nc):
     check_bound(orc, A, B, np.ascontiguousarray(got[:, rows, cols]), nc, n, np.float16, rows=rows, cols=cols)
 
 
+@pytest.mark.parametrize("kinds", [(True, True), (True, False), (False, True)])
+def test_large_output_tile_path(mcf, orc, kinds):
+    """Products with 2^25 or more outputs take the two-outputs-per-lane tile (the
+    binary32 launch of the headline workload): 6001 x 5603 x 37, binary32, nc = 3,
+    ragged in every dimension, checked on sampled outputs and the four corners."""
+    a_mc, b_mc = kinds
+    M, N, K, nc = 6001, 5603, 37, 3
+    g = np.random.default_rng(45)
+    A = inputs.split(g.normal(0, 1 / np.sqrt(K), (M, K)), nc if a_mc else 1, np.float32)
+    B = inputs.split(g.normal(0, 1 / np.sqrt(K), (K, N)), nc if b_mc else 1, np.float32)
+    got = to_host(mcf.mc_matmul(to_dev(A), to_dev(B), nc=nc, a_mc=a_mc, b_mc=b_mc))
+    rows = np.concatenate([g.integers(0, M, 2000), [0, 0, M - 1, M - 1], np.full(16, M - 1)])
+    cols = np.concatenate([g.integers(0, N, 2000), [0, N - 1, 0, N - 1], np.arange(N - 16, N)])
+    want = orc.matmul(A, B, nc=nc, a_mc=a_mc, b_mc=b_mc, rows=rows, cols=cols)
+    assert_bits(got[:, rows, cols], want, f"large tile {kinds}")
+
+
+def test_config_8192_fp32_nc3_sampled(mcf, orc):
+    """The 8192^3 binary32 nc = 3 MC x MC workload in the benchmark's launch
+    configuration: 192 sampled outputs bitwise against the oracle and within
+    4 K u^3 of the exact product."""
+    n, nc = 8192, 3
+    A, B = inputs.matmul_normal(n, n, n, nc, np.float32, seed=0)
+    got = to_host(mcf.mc_matmul(to_dev(A), to_dev(B), nc=nc))
+    g = np.random.default_rng(46)
+    rows = np.concatenate([g.integers(0, n, 188), [0, 0, n - 1, n - 1]])
+    cols = np.concatenate([g.integers(0, n, 188), [0, n - 1, 0, n - 1]])
+    want = orc.matmul(A, B, nc=nc, rows=rows, cols=cols)
+    assert_bits(got[:, rows, cols], want, "8192^3")
+    check_bound(orc, A, B, np.ascontiguousarray(got[:, rows, cols]), nc, n, np.float32, rows=rows, cols=cols)
+
+
 @pytest.mark.parametrize("bias", [True, False])
 def test_linear_small(mcf, orc, bias):
     for dt in (np.float16, np.float32):

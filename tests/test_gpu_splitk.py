@@ -77,7 +77,7 @@ def test_dot_max_slices(mcf, orc):
 
 @pytest.mark.parametrize("dt", [np.float16, np.float32])
 def test_mv(mcf, orc, dt):
-    """MV-MCN (N = 1), M = 1000, K = 4099, default slices (262)."""
+    """MV-MCN (N = 1), M = 1000, K = 4099, default slice count."""
     M, K, nc = 1000, 4099, 3
     A, B = inputs.matmul_normal(M, 1, K, nc, dt, seed=98)
     S = mcf.mc_matmul_splitk_slices(M, 1, K)
@@ -118,3 +118,27 @@ def test_workspace_reuse_and_degenerate(mcf, orc):
     assert Z.shape == (3, 5, 6) and (Z == 0).all() and not np.signbit(Z).any()
     E = mcf.mc_matmul_splitk(to_dev(np.zeros((3, 0, 9), np.float32)), to_dev(np.zeros((3, 9, 6), np.float32)), nc=3)
     assert tuple(E.shape) == (3, 0, 6)
+
+
+def test_bench_shapes(mcf, orc):
+    """The K-split launch configurations the benchmark times (default slice counts):
+    Dot of two binary32 nc = 2 MC vectors at the maximum of 65536 slices (256
+    workgroups of 256 slices, a 256-lane second-level tree) with K = 2^22 + 5 (the
+    benchmark's 2^24 takes the same launch; the one-output oracle is sequential),
+    bitwise and within the bound; MV of an 8192 x 8192 binary32 nc = 3 MC matrix by a
+    plain vector, in full on the GPU, on 48 sampled rows."""
+    K = (1 << 22) + 5
+    A, B = inputs.matmul_normal(1, 1, K, 2, np.float32, seed=0)
+    got = to_host(mcf.mc_matmul_splitk(to_dev(A), to_dev(B), nc=2))
+    S = mcf.mc_matmul_splitk_slices(1, 1, K)
+    assert_bits(got, orc.matmul_splitk(A, B, nc=2, slices=S), "dot 2^24")
+    check_bound(orc, A, B, got, 2, K, np.float32)
+    n = 8192
+    A, B = inputs.matmul_normal(n, 1, n, 3, np.float32, seed=0)
+    got = to_host(mcf.mc_matmul_splitk(to_dev(A), to_dev(B[:1]), nc=3, b_mc=False))
+    S = mcf.mc_matmul_splitk_slices(n, 1, n)
+    g = np.random.default_rng(47)
+    rows = np.concatenate([g.integers(0, n, 46), [0, n - 1]])
+    cols = np.zeros_like(rows)
+    want = orc.matmul_splitk(A, B[:1], nc=3, b_mc=False, slices=S, rows=rows, cols=cols)
+    assert_bits(got[:, rows, cols], want, "mv 8192")
