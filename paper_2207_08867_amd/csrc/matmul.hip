@@ -15,6 +15,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "mcf_arith.hpp"
 #include "mcf_internal.hpp"
 #include "mm_steps.hpp"
@@ -132,12 +134,57 @@ struct Lane {
     }
   }
 
+  // ScalingN of term (x, v) in kept-terms form; lanes failing the test run the
+  // general step.  HEAD / TAIL: the products' errors are known to be zero (see mm_kernel).
+  template <bool HEAD, bool TAIL>
+  __device__ __forceinline__ void scale_kept(const T (&x)[NC], T v, T (&t)[NC]) {
+    T last;
+    scaling_kept<T, NC, HEAD, TAIL>(x, v, t, last);
+    if (__builtin_expect(kept_invalid<T, NC, TAIL>(t, last), 0)) {
+      T h[NC + 1];
+      scaling_terms<T, NC>(x, v, h);
+      compact_nz<T, NC + 1, NC>(h, t);
+    }
+  }
+
+  // a = Add-MCN(a, t) in kept-terms form
+  __device__ __forceinline__ void add_kept_into(T (&a)[NC], const T (&t)[NC]) {
+    T s[NC], last;
+    add_kept<T, NC>(a, t, s, last);
+    if (__builtin_expect(kept_invalid<T, NC, false>(s, last), 0)) {
+      T h[NC + 1];
+      add_terms<T, NC>(a, t, h);
+      compact_nz<T, NC + 1, NC>(h, s);
+    }
+#pragma unroll
+    for (int c = 0; c < NC; ++c) a[c] = s[c];
+  }
+
   // term k = 0 initialises the accumulators
-  __device__ __forceinline__ void first(const Ops &o) { scale<(1 << NP) - 1>(o, acc); }
+  template <bool TPS>
+  __device__ __forceinline__ void first(const Ops &o) {
+    if constexpr (SPOL == SR_SUFFIX) {
+#pragma unroll
+      for (int p = 0; p < NP; ++p)
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j) {
+            if constexpr (!AMC)
+              scale_kept<false, TPS>(o.b[j], o.a[i][0], acc[p][i][j]);
+            else if (TPS && p > 0)
+              scale_kept<true, true>(o.a[i], o.b[j][p], acc[p][i][j]);
+            else
+              scale_kept<false, TPS>(o.a[i], o.b[j][p], acc[p][i][j]);
+          }
+    } else {
+      scale<(1 << NP) - 1>(o, acc);
+    }
+  }
 
   // steps kk0 .. kt-1 of a tile.  GROUP = false: each term's ScalingN and Add-MCN run
   // back to back, so only one term is live at a time.
-  template <int PMASK>
+  template <int PMASK, bool TPS>
   __device__ __forceinline__ void run(const T (*As)[KT][BM], const T (*Bs)[KT][BN], int kk0, int kt, int tx,
                                       int ty) {
     // two steps per loop iteration, so the accumulators keep their registers across
@@ -146,7 +193,25 @@ struct Lane {
     for (int kk = kk0; kk < kt; ++kk) {
       Ops o;
       o.load(As, Bs, kk, tx, ty);
-      if constexpr (GROUP) {
+      if constexpr (SPOL == SR_SUFFIX) {
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+          if (!((PMASK >> p) & 1)) continue;
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+              T term[NC];
+              if constexpr (!AMC)
+                scale_kept<false, TPS>(o.b[j], o.a[i][0], term);
+              else if (TPS && p > 0)
+                scale_kept<true, true>(o.a[i], o.b[j][p], term);
+              else
+                scale_kept<false, TPS>(o.a[i], o.b[j][p], term);
+              add_kept_into(acc[p][i][j], term);
+            }
+        }
+      } else if constexpr (GROUP) {
         T term[NP][TM][TN][NC];
         scale<PMASK>(o, term);
         add<PMASK>(term);
@@ -209,6 +274,7 @@ __global__ __launch_bounds__(MM_THREADS) void mm_kernel(const T *__restrict__ A,
   constexpr int BM = TY * TM, BN = TX * TN;
   constexpr int NP = (AMC && BMC) ? NC : 1;  // components of B swept (MC x MC)
   constexpr int ALL = (1 << NP) - 1;
+  constexpr int EPOL = APOL == SR_SUFFIX ? SR_NET : APOL;  // the epilogue's Add-MCN
   __shared__ T As[NA][KT][BM];
   __shared__ T Bs[NB][KT][BN];
 
@@ -259,17 +325,39 @@ __global__ __launch_bounds__(MM_THREADS) void mm_kernel(const T *__restrict__ A,
     }
   };
 
+  // Kept-terms policy: the largest magnitude of each component plane of the A and B
+  // tiles (binary32 bit patterns of |value|, which order like the values; a NaN or an
+  // infinity is above every finite value), in LDS slots alternating between tiles.
+  // It decides per tile whether every product of a low component, x_c * v_p with
+  // c + p >= 1 (x the MC operand, v_p the other operand's components), is below
+  // exact_limit, so that its Two-Prod error is zero (a product's error is at most half
+  // the spacing of the format at the product, which below exact_limit is half the
+  // smallest subnormal, and that rounds to zero).
+  constexpr bool TRACK = SPOL == SR_SUFFIX && NC > 1;
+  __shared__ uint32_t mx[2][NA + NB];
+  if constexpr (TRACK) {
+    if (threadIdx.x < 2 * (NA + NB)) (&mx[0][0])[threadIdx.x] = 0;
+    __syncthreads();
+  }
+
   if (K > 0) fetch(0);
-  for (int64_t k0 = 0; k0 < K; k0 += KT) {
+  int tile = 0;
+  for (int64_t k0 = 0; k0 < K; k0 += KT, ++tile) {
     const int kt = (int)((K - k0) < KT ? (K - k0) : KT);
     // registers -> LDS: A transposed to [k][m]; note which planes of B hold a non-zero
     int nonzero_planes = 0;
+    uint32_t lmax[NA + NB];
+#pragma unroll
+    for (int c = 0; c < NA + NB; ++c) lmax[c] = 0;
 #pragma unroll
     for (int t = 0; t < A_PER; ++t) {
       const int idx = threadIdx.x + t * MM_THREADS;
       if (idx < BM * KT) {
 #pragma unroll
-        for (int c = 0; c < NA; ++c) As[c][idx % KT][idx / KT] = ra[t][c];
+        for (int c = 0; c < NA; ++c) {
+          As[c][idx % KT][idx / KT] = ra[t][c];
+          if constexpr (TRACK) lmax[c] = max(lmax[c], __float_as_uint(__builtin_fabsf((float)ra[t][c])));
+        }
       }
     }
 #pragma unroll
@@ -281,7 +369,16 @@ __global__ __launch_bounds__(MM_THREADS) void mm_kernel(const T *__restrict__ A,
         for (int c = 0; c < NB; ++c) {
           Bs[c][kk][col] = rb[t][c];
           if (rb[t][c] != T(0)) nonzero_planes |= 1 << c;
+          if constexpr (TRACK) lmax[NA + c] = max(lmax[NA + c], __float_as_uint(__builtin_fabsf((float)rb[t][c])));
         }
+      }
+    }
+    if constexpr (TRACK) {
+      // wavefront maximum (DPP), then one LDS atomic per wavefront and plane
+#pragma unroll
+      for (int c = 0; c < NA + NB; ++c) {
+        const uint32_t w = __ockl_wfred_max_u32(lmax[c]);
+        if (threadIdx.x % warpSize == 0) atomicMax(&mx[tile & 1][c], w);
       }
     }
     int pmask = ALL;
@@ -291,18 +388,42 @@ __global__ __launch_bounds__(MM_THREADS) void mm_kernel(const T *__restrict__ A,
     } else {
       __syncthreads();
     }
-    if (k0 + KT < K) fetch(k0 + KT);  // next tile, in flight during this one
-    int kk0 = 0;
-    if (k0 == 0) {  // term k = 0 initialises the accumulators
-      typename decltype(lane)::Ops o;
-      o.load(As, Bs, 0, tx, ty);
-      lane.first(o);
-      kk0 = 1;
+    bool tps = false;
+    if constexpr (TRACK) {
+      // X: the MC operand's planes, V: the other operand's planes
+      constexpr int X0 = AMC ? 0 : NA, NX = AMC ? NA : NB;
+      constexpr int V0 = AMC ? NA : 0, NV = AMC ? NB : NA;
+      tps = true;
+#pragma unroll
+      for (int c = 0; c < NX; ++c)
+#pragma unroll
+        for (int p = 0; p < NV; ++p)
+          if (c + p >= 1)
+            tps = tps && __uint_as_float(mx[tile & 1][X0 + c]) * __uint_as_float(mx[tile & 1][V0 + p]) <
+                             exact_limit<T>();
+      // the other slot set was last read during the previous tile, before its final
+      // barrier, and is next written by the next tile, after this tile's final barrier
+      if (threadIdx.x < NA + NB) mx[(tile & 1) ^ 1][threadIdx.x] = 0;
     }
-    if (NP > 1 && pmask != ALL)
-      lane.template run<(ALL >> 1)>(As, Bs, kk0, kt, tx, ty);
+    if (k0 + KT < K) fetch(k0 + KT);  // next tile, in flight during this one
+    auto steps = [&](auto tps_c) {
+      constexpr bool TPS = decltype(tps_c)::value;
+      int kk0 = 0;
+      if (k0 == 0) {  // term k = 0 initialises the accumulators
+        typename decltype(lane)::Ops o;
+        o.load(As, Bs, 0, tx, ty);
+        lane.template first<TPS>(o);
+        kk0 = 1;
+      }
+      if (NP > 1 && pmask != ALL)
+        lane.template run<(ALL >> 1), TPS>(As, Bs, kk0, kt, tx, ty);
+      else
+        lane.template run<ALL, TPS>(As, Bs, kk0, kt, tx, ty);
+    };
+    if (TRACK && tps)
+      steps(std::integral_constant<bool, TRACK>{});
     else
-      lane.template run<ALL>(As, Bs, kk0, kt, tx, ty);
+      steps(std::integral_constant<bool, false>{});
     __syncthreads();
   }
 
@@ -320,14 +441,14 @@ __global__ __launch_bounds__(MM_THREADS) void mm_kernel(const T *__restrict__ A,
         for (int c = 0; c < NC; ++c) r[c] = acc[0][i][j][c];
         // MC x MC: combine the per-component products left to right
 #pragma unroll
-        for (int p = 1; p < NP; ++p) mm_add<T, NC, APOL>(r, acc[p][i][j], r);
+        for (int p = 1; p < NP; ++p) mm_add<T, NC, EPOL>(r, acc[p][i][j], r);
       }
       if (gm < M && gn < N) {
         if (bias != nullptr) {
           T bv[NC];
 #pragma unroll
           for (int c = 0; c < NC; ++c) bv[c] = bias[c * N + gn];
-          mm_add<T, NC, APOL>(r, bv, r);
+          mm_add<T, NC, EPOL>(r, bv, r);
         }
         // Zero components leave as +0, the padding Simple-Renorm writes (a zero term
         // that was skipped or selected above may carry the sign of -0).
@@ -351,8 +472,9 @@ static hipError_t mm_launch_tile(int64_t M, int64_t N, int64_t K, const void *A,
 // Launch shape and Simple-Renorm policies (measured on the product workloads):
 //   binary32: every kept term is non-zero almost always -> SR_FULL for both steps;
 //             two outputs per lane once the output has 2^25 entries or more, else one;
-//   binary16: one output per lane; ScalingN terms of low components underflow often ->
-//             SR_HEAD (nc >= 3) or the branch-free network (nc = 2); Add-MCN -> SR_SELECT.
+//   binary16: one output per lane; the low terms of a step are often zero (they fall
+//             below the subnormal grid), almost always as a trailing run, so both steps
+//             use the kept-terms form (SR_SUFFIX), which skips the final carry.
 template <typename T, int NC, bool AMC, bool BMC, bool BT>
 static hipError_t mm_launch(int64_t M, int64_t N, int64_t K, const void *A, const void *B, const void *bias,
                             void *C, hipStream_t s) {
@@ -361,8 +483,7 @@ static hipError_t mm_launch(int64_t M, int64_t N, int64_t K, const void *A, cons
       return mm_launch_tile<T, NC, AMC, BMC, BT, 1, 2, SR_FULL, SR_FULL>(M, N, K, A, B, bias, C, s);
     return mm_launch_tile<T, NC, AMC, BMC, BT, 1, 1, SR_FULL, SR_FULL>(M, N, K, A, B, bias, C, s);
   } else {
-    constexpr int SPOL = NC == 2 ? SR_NET : SR_HEAD;
-    return mm_launch_tile<T, NC, AMC, BMC, BT, 1, 1, SPOL, SR_SELECT>(M, N, K, A, B, bias, C, s);
+    return mm_launch_tile<T, NC, AMC, BMC, BT, 1, 1, SR_SUFFIX, SR_SUFFIX>(M, N, K, A, B, bias, C, s);
   }
 }
 

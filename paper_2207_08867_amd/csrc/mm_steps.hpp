@@ -73,7 +73,9 @@ __device__ __forceinline__ bool all_nonzero(const T (&v)[K]) {
 // sr_try writes the fast-path result and returns true when the lane needs the general
 // compaction instead.  `ok` marks lanes whose terms are known to be all zero: any
 // fast-path result is then correct up to zero signs.
-enum SrPolicy { SR_FULL = 0, SR_SELECT = 1, SR_HEAD = 2, SR_NET = 3 };
+//   SR_SUFFIX: the kept-terms form below (scaling_kept / add_kept / kept_invalid); the
+//              final carry is computed only by lanes that fail its test.
+enum SrPolicy { SR_FULL = 0, SR_SELECT = 1, SR_HEAD = 2, SR_NET = 3, SR_SUFFIX = 4 };
 
 template <typename T, int N, int POL>
 __device__ __forceinline__ bool sr_try(const T (&h)[N + 1], T (&out)[N], bool ok = false) {
@@ -135,6 +137,114 @@ __device__ __forceinline__ void add_terms(const T (&x)[N], const T (&y)[N], T (&
     e = e1 + e2;
   }
   h[N] = e;
+}
+
+// ---------------------------------------------------------------------------------
+// Kept-terms form of a step (policy SR_SUFFIX, used for binary16).
+//
+// Simple-Renorm of the nc+1 terms h keeps h_0 .. h_{nc-1} unchanged (up to zero
+// signs) exactly when
+//   (a) the zero terms among h_0 .. h_{nc-1} form a suffix, and
+//   (b) h_nc = 0 whenever one of them is zero.
+// If h_{nc-1} = fl(hp + e) is zero, hp + e is exactly zero (a sum of two floats that
+// is not zero is at least the smallest subnormal), so the last Two-Sum's error is
+// zero and h_nc equals the error of the last component's own operation
+// (fl(x_{nc-1} * v) for ScalingN, fl(x_{nc-1} + y_{nc-1}) for Add-MCN).  That error
+// is zero when |hp| < 2^(emin+1): below that magnitude consecutive floats are one
+// smallest subnormal apart, so a sum of two floats is exact and a product's error is
+// at most half a subnormal spacing, which rounds to zero (a tie rounds to the even
+// neighbour, zero).  The kernels therefore compute only the kept terms, test (a) and
+// |hp| < 2^(emin+1), and run the general step for a lane that fails the test.
+// ---------------------------------------------------------------------------------
+
+// 2^(emin+1): below it the spacing of the format is its smallest subnormal.
+template <typename T>
+__device__ __forceinline__ constexpr float exact_limit();
+template <>
+__device__ __forceinline__ constexpr float exact_limit<_Float16>() {
+  return 0x1p-13f;
+}
+template <>
+__device__ __forceinline__ constexpr float exact_limit<float>() {
+  return 0x1p-125f;
+}
+
+// |x| < lim, compared in the component format (one compare with an abs modifier).
+__device__ __forceinline__ bool abs_below(float x, float lim) { return __builtin_fabsf(x) < lim; }
+__device__ __forceinline__ bool abs_below(_Float16 x, _Float16 lim) { return __builtin_fabsf16(x) < lim; }
+
+// h_0 .. h_{N-1} of ScalingN(x, v) and the last product hp = fl(x_{N-1} v).
+// HEAD_EXACT: the error of x_0 v is known to be zero; TAIL_EXACT: so are the errors
+// of x_i v, i >= 1 (both follow from |product| < exact_limit, established per tile).
+// A carry known to be zero is not added (Two-Sum(hp, 0) = (hp, 0)).
+template <typename T, int N, bool HEAD_EXACT, bool TAIL_EXACT>
+__device__ __forceinline__ void scaling_kept(const T (&x)[N], T v, T (&h)[N], T &last) {
+  h[0] = x[0] * v;
+  last = h[0];
+  if constexpr (N == 1) return;
+  T e = HEAD_EXACT ? T(0) : fma_(x[0], v, -h[0]);
+  bool carry_zero = HEAD_EXACT;
+#pragma unroll
+  for (int i = 1; i < N; ++i) {
+    const T hp = x[i] * v;
+    if (i == N - 1) {
+      h[i] = carry_zero ? hp : hp + e;
+      last = hp;
+    } else if (carry_zero && TAIL_EXACT) {
+      h[i] = hp;
+    } else {
+      T e2;
+      two_sum(hp, e, h[i], e2);
+      if constexpr (TAIL_EXACT) {
+        e = e2;
+      } else {
+        e = fma_(x[i], v, -hp) + e2;
+      }
+      carry_zero = false;
+    }
+  }
+}
+
+// h_0 .. h_{N-1} of Add-MCN(x, y) and the last component sum hp = fl(x_{N-1} + y_{N-1}).
+template <typename T, int N>
+__device__ __forceinline__ void add_kept(const T (&x)[N], const T (&y)[N], T (&h)[N], T &last) {
+  if constexpr (N == 1) {
+    h[0] = x[0] + y[0];
+    last = h[0];
+  } else {
+    T e;
+    two_sum(x[0], y[0], h[0], e);
+#pragma unroll
+    for (int i = 1; i < N - 1; ++i) {
+      T hp, e1, e2;
+      two_sum(x[i], y[i], hp, e1);
+      two_sum(hp, e, h[i], e2);
+      e = e1 + e2;
+    }
+    last = x[N - 1] + y[N - 1];
+    h[N - 1] = last + e;
+  }
+}
+
+// True when Simple-Renorm of the step's nc+1 terms could change h: a non-zero term
+// follows a zero one, or a term is zero and the last operation may have been inexact
+// (LAST_EXACT: known exact for the whole tile; else tested as |last| < exact_limit).
+// With N = 1 the single kept term is the result whenever it is non-zero, and when it
+// is zero the dropped term is zero too (a zero product or sum is exact).
+template <typename T, int N, bool LAST_EXACT>
+__device__ __forceinline__ bool kept_invalid(const T (&h)[N], T last) {
+  if constexpr (N == 1) {
+    return false;
+  } else {
+    bool z[N];
+#pragma unroll
+    for (int i = 0; i < N; ++i) z[i] = h[i] == T(0);
+    bool bad = false;
+#pragma unroll
+    for (int i = 0; i + 1 < N; ++i) bad = bad || (z[i] && !z[i + 1]);
+    if constexpr (LAST_EXACT) return bad;
+    return bad || (z[N - 1] && !abs_below(last, (T)exact_limit<T>()));
+  }
 }
 
 // out = Add-MCN(x, y) for one value (the epilogue's combinations).
