@@ -182,6 +182,85 @@ struct Lane {
     }
   }
 
+  // S consecutive reduction steps kk .. kk+S-1 in kept-terms form, all terms of all
+  // S steps behind one test: a lane whose test fails anywhere restores its
+  // accumulators and redoes the S steps with the general steps (full terms and the
+  // compaction network), so a wavefront takes one rarely-taken branch per S steps.
+  template <int PMASK, bool TPS, int S>
+  __device__ __forceinline__ void group_kept(const T (*As)[KT][BM], const T (*Bs)[KT][BN], int kk, int tx, int ty) {
+    T saved[NP][TM][TN][NC];
+#pragma unroll
+    for (int p = 0; p < NP; ++p)
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int c = 0; c < NC; ++c) saved[p][i][j][c] = acc[p][i][j][c];
+    bool bad = false;
+#pragma unroll
+    for (int st = 0; st < S; ++st) {
+      Ops o;
+      o.load(As, Bs, kk + st, tx, ty);
+#pragma unroll
+      for (int p = 0; p < NP; ++p) {
+        if (!((PMASK >> p) & 1)) continue;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j) {
+            T t[NC], sum[NC], last;
+            if constexpr (!AMC) {
+              scaling_kept<T, NC, false, TPS>(o.b[j], o.a[i][0], t, last);
+              bad |= kept_invalid<T, NC, TPS>(t, last);
+            } else if (TPS && p > 0) {
+              scaling_kept<T, NC, true, true>(o.a[i], o.b[j][p], t, last);
+              bad |= kept_invalid<T, NC, true>(t, last);
+            } else {
+              scaling_kept<T, NC, false, TPS>(o.a[i], o.b[j][p], t, last);
+              bad |= kept_invalid<T, NC, TPS>(t, last);
+            }
+            add_kept<T, NC>(acc[p][i][j], t, sum, last);
+            bad |= kept_invalid<T, NC, false>(sum, last);
+#pragma unroll
+            for (int c = 0; c < NC; ++c) acc[p][i][j][c] = sum[c];
+          }
+      }
+    }
+    if (__builtin_expect(bad, 0)) {
+#pragma unroll
+      for (int p = 0; p < NP; ++p)
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int c = 0; c < NC; ++c) acc[p][i][j][c] = saved[p][i][j][c];
+#pragma unroll
+      for (int st = 0; st < S; ++st) {
+        Ops o;
+        o.load(As, Bs, kk + st, tx, ty);
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+          if (!((PMASK >> p) & 1)) continue;
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+              T h[NC + 1], t[NC];
+              if constexpr (AMC)
+                scaling_terms<T, NC>(o.a[i], BMC ? o.b[j][p] : o.b[j][0], h);
+              else
+                scaling_terms<T, NC>(o.b[j], o.a[i][0], h);
+              compact_nz<T, NC + 1, NC>(h, t);
+              add_terms<T, NC>(acc[p][i][j], t, h);
+              compact_nz<T, NC + 1, NC>(h, acc[p][i][j]);
+            }
+        }
+      }
+    }
+  }
+
   // steps kk0 .. kt-1 of a tile.  GROUP = false: each term's ScalingN and Add-MCN run
   // back to back, so only one term is live at a time.
   template <int PMASK, bool TPS>
@@ -189,6 +268,15 @@ struct Lane {
                                       int ty) {
     // two steps per loop iteration, so the accumulators keep their registers across
     // the back edge instead of being copied
+    if constexpr (SPOL == SR_SUFFIX && NC == 2) {
+      // nc = 2: the tests of two steps share one branch.  (For nc >= 3 grouping keeps
+      // more temporaries live, lowers the wavefronts per SIMD and was measured
+      // slower; there each step tests and branches on its own, below.)
+      int kk = kk0;
+      for (; kk + 1 < kt; kk += 2) group_kept<PMASK, TPS, 2>(As, Bs, kk, tx, ty);
+      if (kk < kt) group_kept<PMASK, TPS, 1>(As, Bs, kk, tx, ty);
+      return;
+    }
 #pragma unroll 2
     for (int kk = kk0; kk < kt; ++kk) {
       Ops o;

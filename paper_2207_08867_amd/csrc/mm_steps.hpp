@@ -236,14 +236,16 @@ __device__ __forceinline__ bool kept_invalid(const T (&h)[N], T last) {
   if constexpr (N == 1) {
     return false;
   } else {
+    // bitwise operators, not short-circuit ones: the flags stay lane masks in
+    // scalar registers instead of being materialized per lane
     bool z[N];
 #pragma unroll
     for (int i = 0; i < N; ++i) z[i] = h[i] == T(0);
     bool bad = false;
 #pragma unroll
-    for (int i = 0; i + 1 < N; ++i) bad = bad || (z[i] && !z[i + 1]);
+    for (int i = 0; i + 1 < N; ++i) bad = bad | (z[i] & !z[i + 1]);
     if constexpr (LAST_EXACT) return bad;
-    return bad || (z[N - 1] && !abs_below(last, (T)exact_limit<T>()));
+    return bad | (z[N - 1] & !abs_below(last, (T)exact_limit<T>()));
   }
 }
 
