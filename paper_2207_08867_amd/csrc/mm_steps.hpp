@@ -226,6 +226,26 @@ __device__ __forceinline__ void add_kept(const T (&x)[N], const T (&y)[N], T (&h
   }
 }
 
+// Add-MCN(x, y) of two values whose component sums are all below exact_limit (the
+// accumulators of the low components of B in an MC x MC product, whose products the
+// tile flag shows to be below it): each sum x_i + y_i is then exact, every Two-Sum
+// error and carry is zero, and the final carry is zero, so the terms are the N sums
+// followed by zero.  Returns true when a lane does not meet that condition or when
+// Simple-Renorm would move a term (a zero before a non-zero); such a lane runs the
+// general step.
+template <typename T, int N>
+__device__ __forceinline__ bool add_tiny(const T (&x)[N], const T (&y)[N], T (&h)[N]) {
+  bool bad = false;
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    h[i] = x[i] + y[i];
+    bad = bad | !abs_below(h[i], (T)exact_limit<T>());
+  }
+#pragma unroll
+  for (int i = 0; i + 1 < N; ++i) bad = bad | ((h[i] == T(0)) & (h[i + 1] != T(0)));
+  return bad;
+}
+
 // True when Simple-Renorm of the step's nc+1 terms could change h: a non-zero term
 // follows a zero one, or a term is zero and the last operation may have been inexact
 // (LAST_EXACT: known exact for the whole tile; else tested as |last| < exact_limit).

@@ -149,3 +149,17 @@ def test_blocky_tiles(mcf, orc, nc, kinds):
     got = to_host(mcf.mc_matmul(to_dev(A), to_dev(B), nc=nc, a_mc=a_mc, b_mc=b_mc))
     want = orc.matmul(A, B, nc=nc, a_mc=a_mc, b_mc=b_mc)
     assert_bits(got, want, f"blocky nc={nc} {kinds}")
+
+
+@pytest.mark.parametrize("nc", [2, 3])
+def test_growing_low_accumulators(mcf, orc, nc):
+    """Positive A ~ 1/2 and B ~ 2^-5 (MC x MC): every product of a low component is
+    below 2^-13, so the tiles take the exact-low-products form, but the accumulators
+    of B's low components grow past 2^-13 after a few dozen steps, where their
+    tiny-sum form no longer applies and lanes fall back to the general step."""
+    M, N, K = 40, 48, 256
+    g = np.random.default_rng(990 + nc)
+    A = inputs.split(0.5 + g.uniform(0.0, 0.25, (M, K)), nc, np.float16)
+    B = inputs.split(2.0 ** -5 * (1.0 + g.uniform(0.0, 1.0, (K, N))), nc, np.float16)
+    got = to_host(mcf.mc_matmul(to_dev(A), to_dev(B), nc=nc))
+    assert_bits(got, orc.matmul(A, B, nc=nc), f"growing nc={nc}")
