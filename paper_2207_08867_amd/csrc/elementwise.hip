@@ -5,13 +5,15 @@
 // Data are component-major planes; each thread moves 16 bytes per plane per step
 // (8 binary16 or 4 binary32 elements) with dwordx4 loads and stores, so one wave
 // reads 1 KiB contiguous per plane: fully coalesced HBM streams.  The arithmetic of
-// each element is the per-element algorithm of mcf_arith.hpp.
+// each element is the per-element algorithm of mcf_arith.hpp (Div-MCN and Mult-MCN
+// through div_steps.hpp, which returns the same bits with fewer operations).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 #include <atomic>
 #include <mutex>
 
+#include "div_steps.hpp"
 #include "exp32.hpp"
 #include "mcf_arith.hpp"
 #include "mcf_internal.hpp"
@@ -82,13 +84,13 @@ __device__ __forceinline__ void elem(const T (&a)[NC], const T (&b)[NC], T (&r)[
       grow_expn<T, NC>(b, a[0], r);
   } else if constexpr (OP == EW_MUL) {
     if constexpr (XMC && YMC)
-      mult_mcn<T, NC>(a, b, r);
+      mult_mcn_fast<T, NC>(a, b, r);
     else if constexpr (XMC)
       scaling_n<T, NC, NC>(a, b[0], r);
     else
       scaling_n<T, NC, NC>(b, a[0], r);
   } else if constexpr (OP == EW_DIV) {
-    div_mcn<T, NC>(a, b, r);
+    div_mcn_fast<T, NC>(a, b, r);
   } else if constexpr (OP == EW_EXP) {
     static_assert(sizeof(T) == 4, "binary16 Exp-MCN has its own kernel");
     T ex[NC];

@@ -215,3 +215,28 @@ def test_deterministic(mcf):
     a = to_host(mcf.mc_mul(tx, ty, nc=3))
     b = to_host(mcf.mc_mul(tx, ty, nc=3))
     assert_bits(a, b, "repeat")
+
+
+@pytest.mark.parametrize("dt", DTS)
+@pytest.mark.parametrize("nc", [2, 3, 4])
+@pytest.mark.parametrize("op", ["mul", "div"])
+def test_div_mult_spread_and_zero_components(mcf, orc, dt, nc, op):
+    """Div-MCN and Mult-MCN on operands with magnitudes spread over 2^-20 .. 2^6 and
+    about a quarter of all components (leading ones included) set to +0 or -0, so
+    that ScalingN terms have zeros before non-zeros, quotient digits are zero and the
+    per-lane tests of the fast steps fail both ways.  Non-finite results (zero
+    divisors) compare by class, finite ones bit for bit."""
+    n = 20_011
+    g = np.random.default_rng(500 + nc + 10 * (op == "mul") + 20 * (dt == np.float32))
+    def operand():
+        v = g.normal(0.0, 1.0, n) * np.exp2(g.integers(-20, 7, n))
+        X = inputs.split(v, nc, dt)
+        kill = g.random(X.shape) < 0.25
+        X[kill] = np.where(g.random(kill.sum()) < 0.5, dt(0.0), dt(-0.0))
+        return X
+    x, y = operand(), operand()
+    fn = {"mul": (mcf.mc_mul, orc.mul), "div": (mcf.mc_div, orc.div)}[op]
+    with np.errstate(all="ignore"):
+        got = to_host(fn[0](to_dev(x), to_dev(y), nc=nc))
+        want = fn[1](x, y, nc=nc)
+    assert_bits(got, want, f"{op} spread {dt.__name__} nc={nc}")
