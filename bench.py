@@ -59,6 +59,23 @@ def algo_ops_per_mac(nc: int, mc_x_mc: bool) -> int:
     return per * (nc if mc_x_mc else 1)
 
 
+def ew_fp_ops(op: str, nc: int) -> int:
+    """Floating-point operations of the printed elementwise algorithm per element, for
+    the VALU-bound ones: Two-Sum = 6, Two-Prod = 2 (mul + fma), a carry addition = 1,
+    a component division = 1; negations and Simple-Renorm's compare/selects are not
+    counted, nor the Two-Sums and divisions the kernel can prove unnecessary.
+      ScalingN(nc):  2 nc + 7 (nc - 1);   Add-MCN(nc): 6 + 13 (nc - 1);
+      Div-MCN:       (nc + 1) divisions + nc (ScalingN + Add-MCN);
+      Renormalize:   (nc - 1) + nc Two-Sums;
+      Mult-MCN:      2 Div-MCN + 2 Renormalize."""
+    scal = 2 * nc + 7 * (nc - 1)
+    add = 6 + 13 * (nc - 1)
+    div = (nc + 1) + nc * (scal + add)
+    if op == "div":
+        return div
+    return 2 * div + 2 * 6 * (2 * nc - 1)
+
+
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "mm_kernel_f32_nc3_8192.traffic.txt")
 
 
@@ -187,6 +204,10 @@ def bench_elementwise(torch, mcf, inputs, steps=10):
         gbs = bpe * n / (ms * 1e-3) / 1e9
         res[name] = {"us": round(ms * 1e3, 1), "GB/s": round(gbs, 1), "hbm_frac": round(gbs * 1e9 / HBM_PEAK, 3),
                      "Gelem/s": round(n / (ms * 1e-3) / 1e9, 2)}
+        if name in ("mult_mcn", "div_mcn"):  # VALU-bound: their binding roofline
+            ops = ew_fp_ops("div" if name == "div_mcn" else "mult", nc)
+            res[name]["fp_ops_per_elem"] = ops
+            res[name]["valu_frac"] = round(ops * n / (ms * 1e-3) / VALU_PEAK, 3)
         log(f"  elementwise {name}: {ms * 1e3:.1f} us, {gbs:.0f} GB/s")
     return {"workload": "2^26 elements, binary16, nc = 3", "ops": res}
 
