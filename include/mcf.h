@@ -117,6 +117,32 @@ int mc_renorm(int dtype, int nc_in, int nc_out, int64_t n, const void *x, void *
 int mc_matmul(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B,
               int b_mc, void *C, void *stream);
 
+/* Batched and broadcast matrix products, BMM-MCN and 4DMM-MCN (Appendix A.2.2): for
+ * every batch index (i1, i2) in [0, B1) x [0, B2), the matrices of A and B at that
+ * index are multiplied exactly as mc_matmul multiplies its operands (MM-MCN order;
+ * both MC: by linearity over the components of B).  A batch dimension of size 1
+ * broadcast against a larger one (torch.matmul semantics) is a batch stride of 0.
+ * A: component plane c starts at A + c*a_plane (elements); the matrix of batch
+ *   (i1, i2) starts a_s1*i1 + a_s2*i2 elements into each plane and is [M][K]
+ *   row-major.  B likewise, [K][N], with b_plane, b_s1, b_s2.  Every stride is >= 0
+ *   and each plane must hold every batch's matrix: (B1-1)*s1 + (B2-1)*s2 + rows*cols
+ *   <= plane (else MCF_E_SHAPE); the caller provides planes * plane elements.
+ * C: dense [nc][B1][B2][M][N]; it must not overlap A or B.
+ * Sizes as mc_matmul; B1, B2 >= 0; B1 * B2 * M * N below 2^40. */
+int mc_matmul_batched(int dtype, int nc, int64_t B1, int64_t B2, int64_t M, int64_t N, int64_t K, const void *A,
+                      int a_mc, int64_t a_plane, int64_t a_s1, int64_t a_s2, const void *B, int b_mc,
+                      int64_t b_plane, int64_t b_s1, int64_t b_s2, void *C, void *stream);
+
+/* AddMM-MCN (Appendix A.2.2): C = Add-MCN(ScalingN(A B, alpha), ScalingN(Y, beta)),
+ * the product taken exactly as mc_matmul (any operand kinds), both ScalingN without
+ * expand (so the result has nc components).
+ * Y: MC, [nc][M][N] (y_rows = M) or [nc][N] added to every row (y_rows = 1).
+ * alpha, beta: plain scalars that must be exactly representable in the component
+ *   format (else MCF_E_ARG).
+ * A: [nc or 1][M][K], B: [nc or 1][K][N], C: [nc][M][N], not overlapping A, B or Y. */
+int mc_addmm(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B, int b_mc,
+             const void *Y, int64_t y_rows, double alpha, double beta, void *C, void *stream);
+
 /* K-split matrix product, for reductions that are long compared with the number of
  * outputs (Dot-MCN, MV-MCN, small products).  Section 2.2 of the paper notes that an
  * accurate sum of N MC values can be had in O(nc log N) depth; this entry point

@@ -312,6 +312,49 @@ def matmul_splitk(A, B, *, nc, slices, a_mc=True, b_mc=True, rows=None, cols=Non
     return out.reshape(nc, M, N) if rows is None else out
 
 
+def matmul_batched(A, B, *, nc, a_mc=True, b_mc=True):
+    """BMM-MCN / 4DMM-MCN (Appendix A.2.2): A (nc|1, *ba, M, K) and B (nc|1, *bb, K, N)
+    with batch dimensions broadcast as torch.matmul broadcasts them; every batch's
+    matrices are multiplied by ``matmul``.  Returns (nc, *batch, M, N)."""
+    dtype = np.dtype(A.dtype)
+    A = _planar(A, dtype)
+    B = _planar(B, dtype)
+    M, K = A.shape[-2:]
+    N = B.shape[-1]
+    batch = np.broadcast_shapes(A.shape[1:-2], B.shape[1:-2])
+    # missing batch dimensions go in front of the operand's own, after its planes
+    # axis (numpy would align the planes axis with a batch axis)
+    A = A.reshape((A.shape[0],) + (1,) * (len(batch) - (A.ndim - 3)) + A.shape[1:])
+    B = B.reshape((B.shape[0],) + (1,) * (len(batch) - (B.ndim - 3)) + B.shape[1:])
+    Ab = np.broadcast_to(A, (A.shape[0],) + batch + (M, K))
+    Bb = np.broadcast_to(B, (B.shape[0],) + batch + (K, N))
+    out = np.empty((nc,) + batch + (M, N), dtype=dtype)
+    for idx in np.ndindex(*batch):
+        sl = (slice(None),) + idx
+        out[sl] = matmul(np.ascontiguousarray(Ab[sl]), np.ascontiguousarray(Bb[sl]), nc=nc, a_mc=a_mc, b_mc=b_mc)
+    return out
+
+
+def addmm(A, B, Y, alpha, beta, *, nc, a_mc=True, b_mc=False):
+    """AddMM-MCN (Appendix A.2.2), step by step: h = ScalingN(MM-MCN(A, B), alpha);
+    bias = ScalingN(Y, beta); return Add-MCN(h, bias).  Y: (nc, M, N) or (nc, N) (one
+    row for all); alpha, beta: values of the component format."""
+    dtype = np.dtype(A.dtype)
+    P = matmul(A, B, nc=nc, a_mc=a_mc, b_mc=b_mc)
+    M, N = P.shape[1:]
+    Y = _planar(Y, dtype)
+    if Y.ndim == 2:  # one row for all: (nc, N) -> (nc, 1, N) before broadcasting
+        Y = Y[:, None, :]
+    Y = np.broadcast_to(Y, (nc, M, N))
+    a = np.full((M, N), alpha, dtype=dtype)
+    b = np.full((M, N), beta, dtype=dtype)
+    if a.flat[0] != alpha or b.flat[0] != beta:
+        raise ValueError("addmm: alpha and beta must be values of the component format")
+    h = mul(P, a[None], nc=nc, x_mc=True, y_mc=False)
+    bias = mul(np.ascontiguousarray(Y), b[None], nc=nc, x_mc=True, y_mc=False)
+    return add(h, bias, nc=nc)
+
+
 def linear(X, W, bias=None, *, nc, rows=None, cols=None):
     """MC-Linear forward: X plain (T, I), W (nc, O, I), bias (nc, O) or None."""
     dtype = np.dtype(W.dtype)

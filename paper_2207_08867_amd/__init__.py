@@ -20,6 +20,7 @@ import os
 __all__ = [
     "mc_add", "mc_mul", "mc_div", "mc_exp", "mc_renorm", "mc_matmul", "mc_matmul_splitk",
     "mc_matmul_splitk_slices", "mc_matmul_splitk_workspace", "mc_linear_fwd", "mc_status_str",
+    "mc_matmul_batched", "mc_bmm", "mc_addmm", "matmul_mcn",
     "lib", "LIB_PATH", "MCFError",
 ]
 
@@ -58,6 +59,12 @@ def lib() -> ctypes.CDLL:
         L.mc_matmul_splitk_slices.argtypes = [i64, i64, i64]
         L.mc_matmul_splitk_workspace.restype = i64
         L.mc_matmul_splitk_workspace.argtypes = [ci, ci, i64, i64, i64, ci, ci, i64]
+        L.mc_matmul_batched.restype = ci
+        L.mc_matmul_batched.argtypes = [ci, ci, i64, i64, i64, i64, i64, vp, ci, i64, i64, i64, vp, ci, i64, i64,
+                                        i64, vp, vp]
+        L.mc_addmm.restype = ci
+        L.mc_addmm.argtypes = [ci, ci, i64, i64, i64, vp, ci, vp, ci, vp, i64, ctypes.c_double, ctypes.c_double,
+                               vp, vp]
         L.mc_linear_fwd.restype = ci
         L.mc_linear_fwd.argtypes = [ci, ci, i64, i64, i64, vp, vp, vp, vp, vp]
         L.mc_status_str.restype = ctypes.c_char_p
@@ -265,4 +272,100 @@ def mc_linear_fwd(x, W, b=None, *, out=None):
     st = lib().mc_linear_fwd(_dtype_code(W), nc, T, I, O, _dev(x, "x"), _dev(W, "W"), bp, _dev(out, "out"),
                              _stream(W))
     _check(st, "mc_linear_fwd")
+    return out
+
+
+def _batch_strides(t, name, batch, rows, cols):
+    """(plane, s1, s2) of operand t = (planes, *b, rows, cols), len(b) <= 2, broadcast to
+    the two batch dimensions `batch` (size-1 or missing dimensions get stride 0)."""
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    b = tuple(t.shape[1:-2])
+    t5 = t.reshape((t.shape[0],) + (1,) * (2 - len(b)) + b + (rows, cols)).expand(
+        (t.shape[0],) + tuple(batch) + (rows, cols))
+    plane = t.stride(0) if t.shape[0] > 1 else t.numel()
+    return plane, t5.stride(1) if batch[0] > 1 else 0, t5.stride(2) if batch[1] > 1 else 0
+
+
+def mc_matmul_batched(A, B, *, nc: int, a_mc: bool = True, b_mc: bool = True, out=None):
+    """Batched / broadcast product (BMM-MCN, 4DMM-MCN): A (nc|1, *ba, M, K) times
+    B (nc|1, *bb, K, N), up to two batch dimensions each, broadcast as torch.matmul
+    broadcasts them -> (nc, *batch, M, N).  Each matrix product is taken as
+    mc_matmul takes it."""
+    torch = _torch()
+    if A.dtype != B.dtype or A.device != B.device:
+        raise ValueError("operands must share dtype and device")
+    if A.dim() < 3 or B.dim() < 3 or A.dim() > 5 or B.dim() > 5:
+        raise ValueError("operands must be (planes, [b1,] [b2,] rows, cols)")
+    if A.shape[0] != (nc if a_mc else 1) or B.shape[0] != (nc if b_mc else 1):
+        raise ValueError("operand plane count does not match nc / kind")
+    M, K = A.shape[-2:]
+    K2, N = B.shape[-2:]
+    if K != K2:
+        raise ValueError(f"inner dimensions differ: {K} vs {K2}")
+    try:
+        batch = tuple(torch.broadcast_shapes(tuple(A.shape[1:-2]), tuple(B.shape[1:-2])))
+    except RuntimeError as e:
+        raise ValueError(f"batch dimensions do not broadcast: {e}") from None
+    b2 = (1,) * (2 - len(batch)) + batch
+    if out is None:
+        out = torch.empty((nc,) + batch + (M, N), dtype=A.dtype, device=A.device)
+    elif tuple(out.shape) != (nc,) + batch + (M, N) or out.dtype != A.dtype:
+        raise ValueError("out has the wrong shape or dtype")
+    ap, as1, as2 = _batch_strides(A, "A", b2, M, K)
+    bp, bs1, bs2 = _batch_strides(B, "B", b2, K, N)
+    st = lib().mc_matmul_batched(_dtype_code(A), nc, b2[0], b2[1], M, N, K, _dev(A, "A"), int(bool(a_mc)), ap, as1,
+                                 as2, _dev(B, "B"), int(bool(b_mc)), bp, bs1, bs2, _dev(out, "out"), _stream(A))
+    _check(st, "mc_matmul_batched")
+    return out
+
+
+def mc_bmm(A, B, *, nc: int, a_mc: bool = True, b_mc: bool = True, out=None):
+    """BMM-MCN: A (nc|1, b, M, K), B (nc|1, b, K, N) -> (nc, b, M, N)."""
+    if A.dim() != 4 or B.dim() != 4:
+        raise ValueError("BMM operands are (planes, batch, rows, cols)")
+    return mc_matmul_batched(A, B, nc=nc, a_mc=a_mc, b_mc=b_mc, out=out)
+
+
+def mc_addmm(A, B, Y, *, nc: int, alpha: float = 1.0, beta: float = 1.0, a_mc: bool = True, b_mc: bool = False,
+             out=None):
+    """AddMM-MCN: Add-MCN(ScalingN(A B, alpha), ScalingN(Y, beta)).  A (nc|1, M, K),
+    B (nc|1, K, N), Y (nc, M, N) or (nc, N) (added to every row); alpha and beta must
+    be values of the component format.  The paper's AddMM multiplies an MC matrix by a
+    plain one (the defaults a_mc=True, b_mc=False)."""
+    A3, B3, M, N, K, out = _mm_operands(A, B, nc, a_mc, b_mc, out)
+    if Y.dtype != A.dtype or Y.device != A.device:
+        raise ValueError("Y must share dtype and device with A")
+    if tuple(Y.shape) == (nc, M, N):
+        y_rows = M
+    elif tuple(Y.shape) == (nc, N):
+        y_rows = 1
+    else:
+        raise ValueError(f"Y must be (nc, M, N) or (nc, N), got {tuple(Y.shape)}")
+    st = lib().mc_addmm(_dtype_code(A), nc, M, N, K, _dev(A3, "A"), int(bool(a_mc)), _dev(B3, "B"),
+                        int(bool(b_mc)), _dev(Y, "Y"), y_rows, float(alpha), float(beta), _dev(out, "out"),
+                        _stream(A))
+    _check(st, "mc_addmm")
+    return out
+
+
+def matmul_mcn(x, y, *, nc: int, x_mc: bool = True, y_mc: bool = False):
+    """Matmul-MCN: dispatch on the logical ranks of x and y (the planes dimension
+    excluded) as torch.matmul does -- Dot-MCN (1, 1), MV-MCN (2, 1), vector-matrix
+    (1, 2), MM-MCN (2, 2), batched (BMM-MCN / 4DMM-MCN) otherwise, with a 1-D operand
+    taken as a column (resp. row) that is dropped from the result."""
+    rx = x.dim() - 1
+    ry = y.dim() - 1
+    if rx < 1 or ry < 1:
+        raise ValueError("operands need at least one logical dimension")
+    xv = x.unsqueeze(-2) if rx == 1 else x  # (.., 1, K)
+    yv = y.unsqueeze(-1) if ry == 1 else y  # (.., K, 1)
+    if xv.dim() == 3 and yv.dim() == 3:
+        out = mc_matmul(xv, yv, nc=nc, a_mc=x_mc, b_mc=y_mc)
+    else:
+        out = mc_matmul_batched(xv.contiguous(), yv.contiguous(), nc=nc, a_mc=x_mc, b_mc=y_mc)
+    if rx == 1:
+        out = out.squeeze(-2)
+    if ry == 1:
+        out = out.squeeze(-1)
     return out

@@ -139,6 +139,94 @@ int mc_matmul(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A,
   return hip_status(mcf::launch_matmul(dtype, nc, M, N, K, A, a_mc, B, b_mc, 0, nullptr, C, (hipStream_t)stream));
 }
 
+int mc_matmul_batched(int dtype, int nc, int64_t B1, int64_t B2, int64_t M, int64_t N, int64_t K, const void *A,
+                      int a_mc, int64_t a_plane, int64_t a_s1, int64_t a_s2, const void *B, int b_mc,
+                      int64_t b_plane, int64_t b_s1, int64_t b_s2, void *C, void *stream) {
+  if (dtype != MCF_F16 && dtype != MCF_F32) return MCF_E_DTYPE;
+  if (nc < 1 || nc > MAX_NC) return MCF_E_NC;
+  if ((a_mc != 0 && a_mc != 1) || (b_mc != 0 && b_mc != 1) || (!a_mc && !b_mc)) return MCF_E_ARG;
+  if (M < 0 || N < 0 || K < 0 || B1 < 0 || B2 < 0) return MCF_E_SHAPE;
+  if (M > ((int64_t)1 << 20) || N > ((int64_t)1 << 30) || K > ((int64_t)1 << 40)) return MCF_E_SHAPE;
+  if (B1 > ((int64_t)1 << 40) || B2 > ((int64_t)1 << 40)) return MCF_E_SHAPE;
+  if (!grid_fits(M, N)) return MCF_E_SHAPE;
+  if (B1 == 0 || B2 == 0 || M == 0 || N == 0) return MCF_OK;
+  if (B1 > (((int64_t)1 << 40) / B2) / (M * N)) return MCF_E_SHAPE;
+  if (a_s1 < 0 || a_s2 < 0 || b_s1 < 0 || b_s2 < 0 || a_plane < 0 || b_plane < 0) return MCF_E_SHAPE;
+  const int64_t lim = (int64_t)1 << 50;
+  if (a_s1 > lim / B1 || a_s2 > lim / B2 || b_s1 > lim / B1 || b_s2 > lim / B2 || a_plane > lim || b_plane > lim)
+    return MCF_E_SHAPE;
+  // every batch's matrix lies inside its plane
+  if ((B1 - 1) * a_s1 + (B2 - 1) * a_s2 + M * K > a_plane) return MCF_E_SHAPE;
+  if ((B1 - 1) * b_s1 + (B2 - 1) * b_s2 + K * N > b_plane) return MCF_E_SHAPE;
+  if (!C || (K > 0 && (!A || !B))) return MCF_E_NULL;
+  const int64_t es = elem_size(dtype);
+  const int64_t cb = nc * B1 * B2 * M * N * es;
+  if (overlap(C, cb, A, (a_mc ? nc : 1) * a_plane * es) || overlap(C, cb, B, (b_mc ? nc : 1) * b_plane * es))
+    return MCF_E_ALIAS;
+  mcf::MmLaunch L;
+  L.dtype = dtype;
+  L.nc = nc;
+  L.M = M;
+  L.N = N;
+  L.K = K;
+  L.B1 = B1;
+  L.B2 = B2;
+  L.A = A;
+  L.a_mc = a_mc;
+  L.a_plane = a_plane;
+  L.a_s1 = a_s1;
+  L.a_s2 = a_s2;
+  L.B = B;
+  L.b_mc = b_mc;
+  L.b_plane = b_plane;
+  L.b_s1 = b_s1;
+  L.b_s2 = b_s2;
+  L.C = C;
+  return hip_status(mcf::launch_matmul_general(L, (hipStream_t)stream));
+}
+
+int mc_addmm(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B, int b_mc,
+             const void *Y, int64_t y_rows, double alpha, double beta, void *C, void *stream) {
+  if (dtype != MCF_F16 && dtype != MCF_F32) return MCF_E_DTYPE;
+  if (nc < 1 || nc > MAX_NC) return MCF_E_NC;
+  if ((a_mc != 0 && a_mc != 1) || (b_mc != 0 && b_mc != 1) || (!a_mc && !b_mc)) return MCF_E_ARG;
+  if (M < 0 || N < 0 || K < 0) return MCF_E_SHAPE;
+  if (M > ((int64_t)1 << 20) || N > ((int64_t)1 << 30) || K > ((int64_t)1 << 40)) return MCF_E_SHAPE;
+  if (!grid_fits(M, N)) return MCF_E_SHAPE;
+  if (y_rows != M && y_rows != 1) return MCF_E_SHAPE;
+  // the scalars must be values of the component format
+  const bool exact = dtype == MCF_F32 ? (double)(float)alpha == alpha && (double)(float)beta == beta
+                                      : (double)(_Float16)alpha == alpha && (double)(_Float16)beta == beta;
+  if (!exact) return MCF_E_ARG;
+  if (M == 0 || N == 0) return MCF_OK;
+  if (!C || !Y || (K > 0 && (!A || !B))) return MCF_E_NULL;
+  const int64_t es = elem_size(dtype);
+  const int64_t cb = nc * M * N * es;
+  if (overlap(C, cb, A, (a_mc ? nc : 1) * M * K * es) || overlap(C, cb, B, (b_mc ? nc : 1) * K * N * es) ||
+      overlap(C, cb, Y, nc * y_rows * N * es))
+    return MCF_E_ALIAS;
+  mcf::MmLaunch L;
+  L.dtype = dtype;
+  L.nc = nc;
+  L.M = M;
+  L.N = N;
+  L.K = K;
+  L.A = A;
+  L.a_mc = a_mc;
+  L.a_plane = M * K;
+  L.B = B;
+  L.b_mc = b_mc;
+  L.b_plane = K * N;
+  L.C = C;
+  L.mode = 2;
+  L.y = Y;
+  L.y_plane = y_rows * N;
+  L.y_ld = y_rows == 1 ? 0 : N;
+  L.alpha = alpha;
+  L.beta = beta;
+  return hip_status(mcf::launch_matmul_general(L, (hipStream_t)stream));
+}
+
 int64_t mc_matmul_splitk_slices(int64_t M, int64_t N, int64_t K) {
   if (M < 0 || N < 0 || K < 0) return MCF_E_SHAPE;
   return mcf::splitk_default_slices(M, N, K);

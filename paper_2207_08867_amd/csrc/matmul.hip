@@ -363,13 +363,43 @@ __device__ __forceinline__ void tile_of(uint32_t id, uint32_t total, uint32_t gx
   tn = local / rows;
 }
 
+// Shapes, strides and epilogue of one product launch.  Each batch index bb (grid y
+// plus bb0) is split into (bb / B2, bb % B2); operand planes start a_plane / b_plane
+// components apart and a batch at i1 * s1 + i2 * s2 components (a stride of 0
+// broadcasts the operand); C is dense: [nc][batches][M][N].
+template <typename T>
+struct MmArgs {
+  int64_t M, N, K;
+  int64_t a_plane, b_plane, c_plane;
+  int64_t B2, bb0;
+  int64_t a_s1, a_s2, b_s1, b_s2;
+  // epilogue: 0 none; 1 Add-MCN(acc, y) (MC-Linear bias); 2 AddMM:
+  // Add-MCN(ScalingN(acc, alpha), ScalingN(y, beta)).  y planes y_plane apart, rows
+  // y_ld apart (0: one row for every output row).
+  int mode;
+  const T *y;
+  int64_t y_plane, y_ld;
+  T alpha, beta;
+};
+
 // A: [NA][M][K] row-major planes.  B: [NB][K][N] (BT = false) or [NB][N][K] (BT =
 // true).  NA = NC when A is MC else 1, likewise NB.
+// nc <= 3: at least 5 wavefronts per SIMD (at most 96 VGPRs); the binary32 kernels
+// sit just under that bound (the 8192^3 one spills one 8-byte value outside its loop)
+// and one register more would drop them to 4.  nc = 4 needs more registers.
 template <typename T, int NC, bool AMC, bool BMC, bool BT, int TM, int TN, int KT, int SPOL, int APOL,
-          bool GROUP>
-__global__ __launch_bounds__(MM_THREADS) void mm_kernel(const T *__restrict__ A, const T *__restrict__ B,
-                                                        const T *__restrict__ bias, T *__restrict__ C, int64_t M,
-                                                        int64_t N, int64_t K) {
+          bool GROUP, bool ADDMM>
+__global__ __attribute__((amdgpu_flat_work_group_size(1, MM_THREADS), amdgpu_waves_per_eu(NC <= 3 ? 5 : 1))) void
+mm_kernel(const T *__restrict__ A, const T *__restrict__ B,
+                                                        T *__restrict__ C, const MmArgs<T> g) {
+  const int64_t M = g.M, N = g.N, K = g.K;
+  {
+    const int64_t bb = g.bb0 + blockIdx.y;
+    const int64_t i1 = bb / g.B2, i2 = bb - (bb / g.B2) * g.B2;
+    A += i1 * g.a_s1 + i2 * g.a_s2;
+    B += i1 * g.b_s1 + i2 * g.b_s2;
+    C += bb * M * N;
+  }
   constexpr int NA = AMC ? NC : 1;
   constexpr int NB = BMC ? NC : 1;
   constexpr int TX = 16, TY = 16;  // lanes along N and along M
@@ -404,7 +434,7 @@ __global__ __launch_bounds__(MM_THREADS) void mm_kernel(const T *__restrict__ A,
       const int64_t gm = m0 + r, gk = k0 + kk;
       const bool ok = idx < BM * KT && gm < M && gk < K;
 #pragma unroll
-      for (int c = 0; c < NA; ++c) ra[t][c] = ok ? A[c * M * K + gm * K + gk] : T(0);
+      for (int c = 0; c < NA; ++c) ra[t][c] = ok ? A[c * g.a_plane + gm * K + gk] : T(0);
     }
 #pragma unroll
     for (int t = 0; t < B_PER; ++t) {
@@ -421,7 +451,7 @@ __global__ __launch_bounds__(MM_THREADS) void mm_kernel(const T *__restrict__ A,
       const bool ok = idx < BN * KT && gn < N && gk < K;
 #pragma unroll
       for (int c = 0; c < NB; ++c) {
-        const int64_t off = BT ? (c * N * K + gn * K + gk) : (c * K * N + gk * N + gn);
+        const int64_t off = c * g.b_plane + (BT ? (gn * K + gk) : (gk * N + gn));
         rb[t][c] = ok ? B[off] : T(0);
       }
     }
@@ -546,28 +576,45 @@ __global__ __launch_bounds__(MM_THREADS) void mm_kernel(const T *__restrict__ A,
         for (int p = 1; p < NP; ++p) mm_add<T, NC, EPOL>(r, acc[p][i][j], r);
       }
       if (gm < M && gn < N) {
-        if (bias != nullptr) {
-          T bv[NC];
+        if (g.mode != 0) {
+          T yv[NC];
 #pragma unroll
-          for (int c = 0; c < NC; ++c) bv[c] = bias[c * N + gn];
-          mm_add<T, NC, EPOL>(r, bv, r);
+          for (int c = 0; c < NC; ++c) yv[c] = g.y[c * g.y_plane + gm * g.y_ld + gn];
+          if constexpr (ADDMM) {  // AddMM-MCN: both operands scaled first (ScalingN, expand off)
+            scaling_n<T, NC, NC>(r, g.alpha, r);
+            scaling_n<T, NC, NC>(yv, g.beta, yv);
+          }
+          mm_add<T, NC, EPOL>(r, yv, r);
         }
         // Zero components leave as +0, the padding Simple-Renorm writes (a zero term
         // that was skipped or selected above may carry the sign of -0).
 #pragma unroll
-        for (int c = 0; c < NC; ++c) C[c * M * N + gm * N + gn] = (r[c] != T(0)) ? r[c] : T(0);
+        for (int c = 0; c < NC; ++c) C[c * g.c_plane + gm * N + gn] = (r[c] != T(0)) ? r[c] : T(0);
       }
     }
 }
 
+// Batches go to grid y, at most MM_MAX_GRID_Y per launch.
+constexpr int64_t MM_MAX_GRID_Y = 65535;
+
 template <typename T, int NC, bool AMC, bool BMC, bool BT, int TM, int TN, int SPOL, int APOL, int KT = 16>
-static hipError_t mm_launch_tile(int64_t M, int64_t N, int64_t K, const void *A, const void *B, const void *bias,
-                                 void *C, hipStream_t s) {
+static hipError_t mm_launch_tile(MmArgs<T> g, int64_t batches, const void *A, const void *B, void *C,
+                                 hipStream_t s) {
   constexpr int BM = 16 * TM, BN = 16 * TN;
-  dim3 grid((unsigned)(((N + BN - 1) / BN) * ((M + BM - 1) / BM)));
-  hipLaunchKernelGGL((mm_kernel<T, NC, AMC, BMC, BT, TM, TN, KT, SPOL, APOL, false>), grid, dim3(MM_THREADS), 0, s,
-                     (const T *)A, (const T *)B, (const T *)bias, (T *)C, M, N, K);
-  return hipGetLastError();
+  const unsigned gx = (unsigned)(((g.N + BN - 1) / BN) * ((g.M + BM - 1) / BM));
+  for (int64_t b0 = 0; b0 < batches; b0 += MM_MAX_GRID_Y) {
+    g.bb0 = b0;
+    const int64_t nb = (batches - b0) < MM_MAX_GRID_Y ? (batches - b0) : MM_MAX_GRID_Y;
+    if (g.mode == 2)  // the AddMM epilogue is a separate instantiation: it needs more registers
+      hipLaunchKernelGGL((mm_kernel<T, NC, AMC, BMC, BT, TM, TN, KT, SPOL, APOL, false, true>),
+                         dim3(gx, (unsigned)nb), dim3(MM_THREADS), 0, s, (const T *)A, (const T *)B, (T *)C, g);
+    else
+      hipLaunchKernelGGL((mm_kernel<T, NC, AMC, BMC, BT, TM, TN, KT, SPOL, APOL, false, false>),
+                         dim3(gx, (unsigned)nb), dim3(MM_THREADS), 0, s, (const T *)A, (const T *)B, (T *)C, g);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 // Launch shape and Simple-Renorm policies (measured on the product workloads):
@@ -578,51 +625,99 @@ static hipError_t mm_launch_tile(int64_t M, int64_t N, int64_t K, const void *A,
 //             below the subnormal grid), almost always as a trailing run, so both steps
 //             use the kept-terms form (SR_SUFFIX), which skips the final carry.
 template <typename T, int NC, bool AMC, bool BMC, bool BT>
-static hipError_t mm_launch(int64_t M, int64_t N, int64_t K, const void *A, const void *B, const void *bias,
-                            void *C, hipStream_t s) {
+static hipError_t mm_launch(const MmArgs<T> &g, int64_t batches, const void *A, const void *B, void *C,
+                            hipStream_t s) {
   if constexpr (sizeof(T) == 4) {
-    if (M * N >= ((int64_t)1 << 25))
-      return mm_launch_tile<T, NC, AMC, BMC, BT, 1, 2, SR_FULL, SR_FULL>(M, N, K, A, B, bias, C, s);
-    return mm_launch_tile<T, NC, AMC, BMC, BT, 1, 1, SR_FULL, SR_FULL>(M, N, K, A, B, bias, C, s);
+    if (g.M * g.N >= ((int64_t)1 << 25))
+      return mm_launch_tile<T, NC, AMC, BMC, BT, 1, 2, SR_FULL, SR_FULL>(g, batches, A, B, C, s);
+    return mm_launch_tile<T, NC, AMC, BMC, BT, 1, 1, SR_FULL, SR_FULL>(g, batches, A, B, C, s);
   } else {
     if constexpr (BT)  // MC-Linear: two rows of x per lane share each weight value
-      return mm_launch_tile<T, NC, AMC, BMC, BT, 2, 1, SR_SUFFIX, SR_SUFFIX>(M, N, K, A, B, bias, C, s);
+      return mm_launch_tile<T, NC, AMC, BMC, BT, 2, 1, SR_SUFFIX, SR_SUFFIX>(g, batches, A, B, C, s);
     // nc = 2: 32-step LDS tiles halve the per-tile staging and barriers, which weigh
     // more against its short steps (8% faster on 1024^3; flat or slower at nc >= 3)
     constexpr int KT = NC == 2 ? 32 : 16;
-    return mm_launch_tile<T, NC, AMC, BMC, BT, 1, 1, SR_SUFFIX, SR_SUFFIX, KT>(M, N, K, A, B, bias, C, s);
+    return mm_launch_tile<T, NC, AMC, BMC, BT, 1, 1, SR_SUFFIX, SR_SUFFIX, KT>(g, batches, A, B, C, s);
   }
 }
 
 template <typename T, int NC>
-static hipError_t mm_kinds(int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B, int b_mc,
-                           int b_trans, const void *bias, void *C, hipStream_t s) {
+static hipError_t mm_kinds(const MmArgs<T> &g, int64_t batches, const void *A, int a_mc, const void *B, int b_mc,
+                           int b_trans, void *C, hipStream_t s) {
   if (b_trans) {
     // linear layer: plain input times MC weight stored [out][in]
-    if (!a_mc && b_mc) return mm_launch<T, NC, false, true, true>(M, N, K, A, B, bias, C, s);
+    if (!a_mc && b_mc) return mm_launch<T, NC, false, true, true>(g, batches, A, B, C, s);
     return hipErrorInvalidValue;
   }
-  if (a_mc && b_mc) return mm_launch<T, NC, true, true, false>(M, N, K, A, B, bias, C, s);
-  if (a_mc) return mm_launch<T, NC, true, false, false>(M, N, K, A, B, bias, C, s);
-  return mm_launch<T, NC, false, true, false>(M, N, K, A, B, bias, C, s);
+  if (a_mc && b_mc) return mm_launch<T, NC, true, true, false>(g, batches, A, B, C, s);
+  if (a_mc) return mm_launch<T, NC, true, false, false>(g, batches, A, B, C, s);
+  return mm_launch<T, NC, false, true, false>(g, batches, A, B, C, s);
 }
 
 template <typename T>
-static hipError_t mm_dispatch(int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B,
-                              int b_mc, int b_trans, const void *bias, void *C, hipStream_t s) {
+static hipError_t mm_dispatch(int nc, const MmArgs<T> &g, int64_t batches, const void *A, int a_mc, const void *B,
+                              int b_mc, int b_trans, void *C, hipStream_t s) {
   switch (nc) {
-    case 1: return mm_kinds<T, 1>(M, N, K, A, a_mc, B, b_mc, b_trans, bias, C, s);
-    case 2: return mm_kinds<T, 2>(M, N, K, A, a_mc, B, b_mc, b_trans, bias, C, s);
-    case 3: return mm_kinds<T, 3>(M, N, K, A, a_mc, B, b_mc, b_trans, bias, C, s);
-    case 4: return mm_kinds<T, 4>(M, N, K, A, a_mc, B, b_mc, b_trans, bias, C, s);
+    case 1: return mm_kinds<T, 1>(g, batches, A, a_mc, B, b_mc, b_trans, C, s);
+    case 2: return mm_kinds<T, 2>(g, batches, A, a_mc, B, b_mc, b_trans, C, s);
+    case 3: return mm_kinds<T, 3>(g, batches, A, a_mc, B, b_mc, b_trans, C, s);
+    case 4: return mm_kinds<T, 4>(g, batches, A, a_mc, B, b_mc, b_trans, C, s);
   }
   return hipErrorInvalidValue;
 }
 
+template <typename T>
+static hipError_t mm_typed(const MmLaunch &L, hipStream_t s) {
+  MmArgs<T> g;
+  g.M = L.M;
+  g.N = L.N;
+  g.K = L.K;
+  g.a_plane = L.a_plane;
+  g.b_plane = L.b_plane;
+  g.c_plane = L.B1 * L.B2 * L.M * L.N;
+  g.B2 = L.B2;
+  g.bb0 = 0;
+  g.a_s1 = L.a_s1;
+  g.a_s2 = L.a_s2;
+  g.b_s1 = L.b_s1;
+  g.b_s2 = L.b_s2;
+  g.mode = L.mode;
+  g.y = (const T *)L.y;
+  g.y_plane = L.y_plane;
+  g.y_ld = L.y_ld;
+  g.alpha = (T)L.alpha;
+  g.beta = (T)L.beta;
+  return mm_dispatch<T>(L.nc, g, L.B1 * L.B2, L.A, L.a_mc, L.B, L.b_mc, L.b_trans, L.C, s);
+}
+
+hipError_t launch_matmul_general(const MmLaunch &L, hipStream_t stream) {
+  if (L.dtype == 0) return mm_typed<_Float16>(L, stream);
+  return mm_typed<float>(L, stream);
+}
+
 hipError_t launch_matmul(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc,
                          const void *B, int b_mc, int b_trans, const void *bias, void *C, hipStream_t stream) {
-  if (dtype == 0) return mm_dispatch<_Float16>(nc, M, N, K, A, a_mc, B, b_mc, b_trans, bias, C, stream);
-  return mm_dispatch<float>(nc, M, N, K, A, a_mc, B, b_mc, b_trans, bias, C, stream);
+  MmLaunch L;
+  L.dtype = dtype;
+  L.nc = nc;
+  L.M = M;
+  L.N = N;
+  L.K = K;
+  L.A = A;
+  L.a_mc = a_mc;
+  L.a_plane = M * K;
+  L.B = B;
+  L.b_mc = b_mc;
+  L.b_trans = b_trans;
+  L.b_plane = K * N;
+  L.C = C;
+  if (bias != nullptr) {
+    L.mode = 1;
+    L.y = bias;
+    L.y_plane = N;
+    L.y_ld = 0;
+  }
+  return launch_matmul_general(L, stream);
 }
 
 }  // namespace mcf

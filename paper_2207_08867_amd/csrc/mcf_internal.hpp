@@ -22,6 +22,25 @@ hipError_t launch_exp_f16(int nc, int64_t n, const void *x, void *out, hipStream
 // Exp-MCN over binary32 components (correctly rounded component exponential).
 hipError_t launch_exp_f32(int nc, int64_t n, const void *x, void *out, hipStream_t stream);
 
+// A product launch in full generality (validated by the ABI layer): batches
+// B1 x B2 with per-operand batch strides (0 broadcasts) and plane strides; C dense
+// [nc][B1][B2][M][N]; b_trans: B stored [planes][N][K]; epilogue mode 0 none, 1
+// Add-MCN with y, 2 AddMM (Add-MCN(ScalingN(C, alpha), ScalingN(y, beta))); alpha and
+// beta are exactly representable in the component format.
+struct MmLaunch {
+  int dtype = 1, nc = 1;
+  int64_t M = 0, N = 0, K = 0, B1 = 1, B2 = 1;
+  const void *A = nullptr, *B = nullptr;
+  void *C = nullptr;
+  int a_mc = 1, b_mc = 1, b_trans = 0;
+  int64_t a_plane = 0, b_plane = 0, a_s1 = 0, a_s2 = 0, b_s1 = 0, b_s2 = 0;
+  int mode = 0;
+  const void *y = nullptr;
+  int64_t y_plane = 0, y_ld = 0;
+  double alpha = 1.0, beta = 1.0;
+};
+hipError_t launch_matmul_general(const MmLaunch &L, hipStream_t stream);
+
 // C[nc][M][N] = A x B.  b_trans: B is stored as [planes][N][K] (a linear layer's
 // weight) instead of [planes][K][N].  bias: [nc][N] MC bias added with Add-MCN, or
 // NULL.
