@@ -13,7 +13,8 @@ Also reported on the same line (not part of `value`):
   * the maximum error against the exact product on sampled outputs;
   * the other workloads (64^3 binary32 nc=2; 1024^3 binary16 nc=2 and 3; the
     4096x1024x1024 binary16 nc=3 MC-Linear over 100 layers; the 2^26-element binary16
-    nc=3 elementwise operations with their HBM bandwidth);
+    nc=3 elementwise operations with their HBM bandwidth; the K-split Dot and MV; the
+    paper's BMM-MCN and AddMM-MCN sizes);
   * cpu_baseline: the CPU oracle timed on a sample of the headline workload.
 
 Usage: python bench.py [--gpus 1] [--steps 3] [--warmup 1] [--no-extra]
@@ -245,6 +246,45 @@ def bench_splitk(torch, mcf, inputs, steps=20):
     return res
 
 
+# The paper's CPU times (Ryzen 7 5800X, PyTorch 1.11; Appendix A.3, matrix operator
+# table) for 1-, 2-, 3-component MC x plain products: context, not a target.
+PAPER_CPU_S = {"bmm": (4.84, 8.03, 11.2), "addmm": (0.750, 1.12, 1.44)}
+
+
+def bench_batched(torch, mcf, inputs, steps=20):
+    """The paper's BMM-MCN (16 x 500 x 200) x (16 x 200 x 50) and AddMM-MCN
+    100 + (500 x 200) x (200 x 100) workloads, MC x plain, binary32, nc = 1, 2, 3."""
+    res = {}
+    g = np.random.default_rng(0)
+    for nc in (1, 2, 3):
+        A = inputs.split(g.normal(0.0, 1 / np.sqrt(200), (16, 500, 200)), nc, np.float32)
+        B = inputs.split(g.normal(0.0, 1 / np.sqrt(200), (16, 200, 50)), 1, np.float32)
+        tA, tB = torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda()
+        out = torch.empty((nc, 16, 500, 50), dtype=torch.float32, device="cuda")
+        cases = [("bmm", lambda: mcf.mc_bmm(tA, tB, nc=nc, b_mc=False, out=out), 16 * 500 * 200 * 50)]
+        A2 = inputs.split(g.normal(0.0, 1 / np.sqrt(200), (500, 200)), nc, np.float32)
+        B2 = inputs.split(g.normal(0.0, 1 / np.sqrt(200), (200, 100)), 1, np.float32)
+        Y2 = inputs.split(g.normal(0.0, 1.0, (100,)), nc, np.float32)
+        tA2, tB2, tY2 = (torch.from_numpy(v).cuda() for v in (A2, B2, Y2))
+        out2 = torch.empty((nc, 500, 100), dtype=torch.float32, device="cuda")
+        cases.append(("addmm", lambda: mcf.mc_addmm(tA2, tB2, tY2, nc=nc, alpha=1.0, beta=1.0, out=out2),
+                      500 * 200 * 100))
+        for name, fn, macs in cases:
+            for _ in range(3):
+                fn()
+            tm = Timer(torch)
+            for _ in range(steps):
+                tm.run(fn)
+            ms = float(np.median(tm.ms()))
+            res[f"{name}_f32_nc{nc}"] = {
+                "us": round(ms * 1e3, 1), "MC-GFLOP/s": round(2 * macs / (ms * 1e-3) / 1e9, 1),
+                "valu_frac": round(algo_ops_per_mac(nc, False) * macs / (ms * 1e-3) / VALU_PEAK, 3),
+                "paper_cpu_s": PAPER_CPU_S[name][nc - 1]}
+            log(f"  {name} nc={nc}: {ms * 1e3:.1f} us")
+    return {"workload": "BMM-MCN (16x500x200)x(16x200x50), AddMM-MCN 100+(500x200)x(200x100); MC x plain, "
+                        "binary32", "ops": res}
+
+
 def bench_linear(torch, mcf, inputs, layers=100):
     T, I, O, nc = 4096, 1024, 1024, 3
     gen = inputs.linear_inputs(T, I, O, nc, np.float16, layers=layers, seed=0)
@@ -361,6 +401,8 @@ def main():
         extra["elementwise"] = bench_elementwise(torch, mcf, inputs)
         log("K-split products")
         extra["splitk"] = bench_splitk(torch, mcf, inputs)
+        log("batched products and AddMM")
+        extra["batched"] = bench_batched(torch, mcf, inputs)
         line["extra"] = extra
     if not args.no_cpu:
         log("cpu baseline (oracle)")
