@@ -68,12 +68,15 @@ def ew_fp_ops(op: str, nc: int) -> int:
       ScalingN(nc):  2 nc + 7 (nc - 1);   Add-MCN(nc): 6 + 13 (nc - 1);
       Div-MCN:       (nc + 1) divisions + nc (ScalingN + Add-MCN);
       Renormalize:   (nc - 1) + nc Two-Sums;
-      Mult-MCN:      2 Div-MCN + 2 Renormalize."""
+      Mult-MCN:      2 Div-MCN + 2 Renormalize;
+      Mult-MCN-Slow: 1 + nc (Div-MCN + Add-MCN + 1)."""
     scal = 2 * nc + 7 * (nc - 1)
     add = 6 + 13 * (nc - 1)
     div = (nc + 1) + nc * (scal + add)
     if op == "div":
         return div
+    if op == "mult_slow":  # first digit, then nc times DivN + Add-MCN + next digit
+        return 1 + nc * (div + add + 1)
     return 2 * div + 2 * 6 * (2 * nc - 1)
 
 
@@ -189,6 +192,8 @@ def bench_elementwise(torch, mcf, inputs, steps=10):
         "div_mcn": (lambda: mcf.mc_div(dev["a"], dev["d"], nc=nc, out=out), 18),
         "exp_mcn": (lambda: mcf.mc_exp(dev["e"], nc=nc, out=out), 12),
         "renormalize": (lambda: mcf.mc_renorm(dev["a"], mode=0, out=out), 12),
+        "square_mcn": (lambda: mcf.mc_square(dev["a"], nc=nc, out=out), 12),
+        "mult_mcn_slow": (lambda: mcf.mc_mul_slow(dev["a"], dev["d"], nc=nc, out=out), 18),
     }
     # binary32 Exp-MCN (correctly rounded component exponential), same input recipe
     e32 = torch.from_numpy(inputs.split(np.random.default_rng(0).uniform(-4.0, 4.0, n), nc, np.float32)).cuda()
@@ -205,8 +210,8 @@ def bench_elementwise(torch, mcf, inputs, steps=10):
         gbs = bpe * n / (ms * 1e-3) / 1e9
         res[name] = {"us": round(ms * 1e3, 1), "GB/s": round(gbs, 1), "hbm_frac": round(gbs * 1e9 / HBM_PEAK, 3),
                      "Gelem/s": round(n / (ms * 1e-3) / 1e9, 2)}
-        if name in ("mult_mcn", "div_mcn"):  # VALU-bound: their binding roofline
-            ops = ew_fp_ops("div" if name == "div_mcn" else "mult", nc)
+        if name in ("mult_mcn", "div_mcn", "mult_mcn_slow"):  # VALU-bound: their binding roofline
+            ops = ew_fp_ops({"div_mcn": "div", "mult_mcn": "mult", "mult_mcn_slow": "mult_slow"}[name], nc)
             res[name]["fp_ops_per_elem"] = ops
             res[name]["valu_frac"] = round(ops * n / (ms * 1e-3) / VALU_PEAK, 3)
         log(f"  elementwise {name}: {ms * 1e3:.1f} us, {gbs:.0f} GB/s")

@@ -88,6 +88,19 @@ int mc_mul(int dtype, int nc, int64_t n, const void *x, int x_mc, const void *y,
 int mc_div(int dtype, int nc, int64_t n, const void *x, int x_mc, const void *y, int y_mc, void *out,
            void *stream);
 
+/* Multiplication, Mult-MCN-Slow (Appendix A.2.1), for two MC operands: p = fl(x_0 y_0)
+ * is the first product digit; nc times the remainder x = Add-MCN(x, -DivN(p, y)) is
+ * formed and its next digit p = fl(x_0 y_0) taken; the nc+1 digits pass through
+ * Simple-Renorm.  x, y, out: [nc][n]; out may be x or y exactly. */
+int mc_mul_slow(int dtype, int nc, int64_t n, const void *x, const void *y, void *out, void *stream);
+
+/* Square, Square-MCN (Appendix A.2.1).  The printed first step fl(2^{x_0}) is read as
+ * fl(x_0 x_0), the square's leading term: h = (fl(x_0 x_0), 0, ..., 0), then
+ * h = Grow-ExpN(h, fl(2 x_0 x_1)) (the addend is zero when nc = 1).  As printed, the
+ * result is accurate to about one unit of x_0^2 (the rounding of x_0^2 and the terms
+ * x_1^2, x_0 x_2, ... are not carried).  x, out: [nc][n]; out == x allowed. */
+int mc_square(int dtype, int nc, int64_t n, const void *x, void *out, void *stream);
+
 /* Exponential, Exp-MCN (Appendix A.2.1): h = exp(x_0) (one component), then for
  * i = 1 .. nc-1, h = ScalingN(h, exp(x_i), expand) growing h by one component per
  * step.  The component exponential is correctly rounded in both formats (binary16

@@ -25,7 +25,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 _SRC = os.path.join(_HERE, "mcf_oracle.c")
 
-OP_ADD, OP_MUL, OP_DIV, OP_EXP, OP_RENORM, OP_SIMPLE_RENORM, OP_SCALING_EXPAND = range(7)
+OP_ADD, OP_MUL, OP_DIV, OP_EXP, OP_RENORM, OP_SIMPLE_RENORM, OP_SCALING_EXPAND, OP_MUL_SLOW, OP_SQUARE = range(9)
 
 _lib = None
 
@@ -236,6 +236,16 @@ def exp(x, *, nc):
 def renorm(x, *, nc, nc_out=None, mode=0):
     """mode 0: Renormalize; mode 1: Simple-Renorm."""
     return elementwise(OP_RENORM if mode == 0 else OP_SIMPLE_RENORM, x, nc=nc, nc_out=nc_out or nc)
+
+
+def mul_slow(x, y, *, nc):
+    """Mult-MCN-Slow (MC,MC)."""
+    return elementwise(OP_MUL_SLOW, x, y, nc=nc)
+
+
+def square(x, *, nc):
+    """Square-MCN (first step read as fl(x_0 x_0))."""
+    return elementwise(OP_SQUARE, x, nc=nc)
 
 
 def scaling_expand(x, v, *, nc):

@@ -299,6 +299,38 @@ static void mult_mcn(int f, const double *x, const double *y, int n, double *out
   renormalize(f, q, n, n, out);
 }
 
+/* Mult-MCN-Slow (Appendix A.2.1): product digits by repeated division.  p = fl(x_0
+ * y_0) is the first digit; then n times the remainder x = Add-MCN(x, -DivN(p, y)) is
+ * formed and its next digit p = fl(x_0 y_0) taken; the n+1 digits pass through
+ * Simple-Renorm. */
+static void mult_mcn_slow(int f, const double *x_in, const double *y, int n, double *out) {
+  double h[MAXC + 1], x[MAXC] = {0.0}, d[MAXC], neg[MAXC], r[MAXC];
+  for (int i = 0; i < n; ++i) x[i] = x_in[i];
+  double p = fl_mul(f, x[0], y[0]);
+  h[0] = p;
+  for (int i = 1; i <= n; ++i) {
+    div_n(f, p, y, n, d);
+    for (int c = 0; c < n; ++c) neg[c] = -d[c]; /* negation is exact */
+    add_mcn(f, x, neg, n, r);
+    for (int c = 0; c < n; ++c) x[c] = r[c];
+    p = fl_mul(f, x[0], y[0]);
+    h[i] = p;
+  }
+  simple_renorm(h, n + 1, n, out);
+}
+
+/* Square-MCN (Appendix A.2.1).  Reading: the printed first step fl(2^{x_0}) is taken
+ * as fl(x_0 x_0) (the algorithm squares x).  h = (fl(x_0 x_0), 0, ..., 0), then
+ * h = Grow-ExpN(h, fl(2 x_0 x_1)) (2 x_0 is exact, so this is one rounding of the
+ * product); with n = 1 there is no x_1 and the addend is zero. */
+static void square_mcn(int f, const double *x, int n, double *out) {
+  double h[MAXC];
+  h[0] = fl_mul(f, x[0], x[0]);
+  for (int i = 1; i < n; ++i) h[i] = 0.0;
+  double v = n > 1 ? fl_mul(f, fl_mul(f, 2.0, x[0]), x[1]) : 0.0;
+  grow_expn(f, h, n, v, out);
+}
+
 /* Exp-MCN (Appendix A.2.1).  Reading: the factor of step i is exp(x_i) (the printed
  * exp(h_i) is taken as a typo); h starts with one component and ScalingN with expand
  * grows it by one per step, to n components. */
@@ -426,7 +458,7 @@ static void scatter(int f, void *base, int nc, int64_t n, int64_t i, const doubl
 
 /* Operation codes for mcf_oracle_elementwise. */
 enum { OP_ADD = 0, OP_MUL = 1, OP_DIV = 2, OP_EXP = 3, OP_RENORM = 4, OP_SIMPLE_RENORM = 5,
-       OP_SCALING_EXPAND = 6 };
+       OP_SCALING_EXPAND = 6, OP_MUL_SLOW = 7, OP_SQUARE = 8 };
 
 /* out = op(x, y) elementwise over n elements.  x_mc / y_mc say whether an operand is
  * an MC value (nc planes) or a plain tensor (one plane).
@@ -436,12 +468,16 @@ enum { OP_ADD = 0, OP_MUL = 1, OP_DIV = 2, OP_EXP = 3, OP_RENORM = 4, OP_SIMPLE_
  *   EXP : Exp-MCN of x (MC).
  *   RENORM / SIMPLE_RENORM : x (MC) has nc components, out has nc_out.
  *   SCALING_EXPAND : (MC,T) ScalingN with expand, out has nc+1 components.
+ *   MUL_SLOW : (MC,MC) Mult-MCN-Slow.
+ *   SQUARE : Square-MCN of x (MC).
  * Returns 0, or -1 on bad arguments. */
 int mcf_oracle_elementwise(int f, int op, int nc, int nc_out, int64_t n, const void *x, int x_mc,
                            const void *y, int y_mc, void *out) {
   if (nc < 1 || nc > MAXC || (f != FMT_F16 && f != FMT_F32)) return -1;
-  int binary = (op == OP_ADD || op == OP_MUL || op == OP_DIV || op == OP_SCALING_EXPAND);
+  int binary = (op == OP_ADD || op == OP_MUL || op == OP_DIV || op == OP_SCALING_EXPAND || op == OP_MUL_SLOW);
   if (binary && !x_mc && !y_mc) return -1;
+  if (op == OP_MUL_SLOW && !(x_mc && y_mc)) return -1;
+  if (op < OP_ADD || op > OP_SQUARE) return -1;
   if ((op == OP_RENORM || op == OP_SIMPLE_RENORM) && (nc_out < 1 || nc_out > nc)) return -1;
   int xn = x_mc ? nc : 1, yn = y_mc ? nc : 1;
 #pragma omp parallel for schedule(static)
@@ -490,6 +526,12 @@ int mcf_oracle_elementwise(int f, int op, int nc, int nc_out, int64_t n, const v
       case OP_SCALING_EXPAND:
         scaling_n(f, a, nc, b[0], 1, r);
         rn = nc + 1;
+        break;
+      case OP_MUL_SLOW:
+        mult_mcn_slow(f, a, b, nc, r);
+        break;
+      case OP_SQUARE:
+        square_mcn(f, a, nc, r);
         break;
     }
     scatter(f, out, rn, n, i, r);

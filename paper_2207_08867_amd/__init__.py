@@ -20,7 +20,7 @@ import os
 __all__ = [
     "mc_add", "mc_mul", "mc_div", "mc_exp", "mc_renorm", "mc_matmul", "mc_matmul_splitk",
     "mc_matmul_splitk_slices", "mc_matmul_splitk_workspace", "mc_linear_fwd", "mc_status_str",
-    "mc_matmul_batched", "mc_bmm", "mc_addmm", "matmul_mcn",
+    "mc_matmul_batched", "mc_bmm", "mc_addmm", "matmul_mcn", "mc_mul_slow", "mc_square",
     "lib", "LIB_PATH", "MCFError",
 ]
 
@@ -47,6 +47,10 @@ def lib() -> ctypes.CDLL:
             f = getattr(L, name)
             f.restype = ci
             f.argtypes = [ci, ci, i64, vp, ci, vp, ci, vp, vp]
+        L.mc_mul_slow.restype = ci
+        L.mc_mul_slow.argtypes = [ci, ci, i64, vp, vp, vp, vp]
+        L.mc_square.restype = ci
+        L.mc_square.argtypes = [ci, ci, i64, vp, vp, vp]
         L.mc_exp.restype = ci
         L.mc_exp.argtypes = [ci, ci, i64, vp, vp, vp]
         L.mc_renorm.restype = ci
@@ -160,6 +164,34 @@ def mc_mul(x, y, *, nc: int, x_mc: bool = True, y_mc: bool = True, out=None):
 def mc_div(x, y, *, nc: int, x_mc: bool = True, y_mc: bool = True, out=None):
     """Div-MCN for (MC, MC); DivN for (T, MC); zero-padded divisor for (MC, T)."""
     return _binary("mc_div", x, y, nc, x_mc, y_mc, out)
+
+
+def mc_mul_slow(x, y, *, nc: int, out=None):
+    """Mult-MCN-Slow of two MC operands of the same shape (nc, ...)."""
+    torch = _torch()
+    if x.dtype != y.dtype or x.device != y.device or x.shape != y.shape or x.shape[0] != nc:
+        raise ValueError("x and y must be MC operands (nc, ...) of one shape, dtype and device")
+    n = x.numel() // nc
+    if out is None:
+        out = torch.empty_like(x)
+    elif out.shape != x.shape or out.dtype != x.dtype:
+        raise ValueError("out has the wrong shape or dtype")
+    st = lib().mc_mul_slow(_dtype_code(x), nc, n, _dev(x, "x"), _dev(y, "y"), _dev(out, "out"), _stream(x))
+    _check(st, "mc_mul_slow")
+    return out
+
+
+def mc_square(x, *, nc: int, out=None):
+    """Square-MCN of an MC operand (nc, ...)."""
+    torch = _torch()
+    _logical_shape(x, nc, True, "x")
+    n = x.numel() // nc
+    if out is None:
+        out = torch.empty_like(x)
+    elif out.shape != x.shape or out.dtype != x.dtype:
+        raise ValueError("out has the wrong shape or dtype")
+    _check(lib().mc_square(_dtype_code(x), nc, n, _dev(x, "x"), _dev(out, "out"), _stream(x)), "mc_square")
+    return out
 
 
 def mc_exp(x, *, nc: int, out=None):

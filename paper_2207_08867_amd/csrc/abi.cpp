@@ -98,6 +98,21 @@ int mc_div(int dtype, int nc, int64_t n, const void *x, int x_mc, const void *y,
   return binary_op(mcf::EW_DIV, dtype, nc, n, x, x_mc, y, y_mc, out, stream);
 }
 
+int mc_mul_slow(int dtype, int nc, int64_t n, const void *x, const void *y, void *out, void *stream) {
+  return binary_op(mcf::EW_MUL_SLOW, dtype, nc, n, x, 1, y, 1, out, stream);
+}
+
+int mc_square(int dtype, int nc, int64_t n, const void *x, void *out, void *stream) {
+  int st = check_common(dtype, nc, n);
+  if (st != MCF_OK) return st;
+  if (n == 0) return MCF_OK;
+  if (!x || !out) return MCF_E_NULL;
+  const int64_t b = nc * n * elem_size(dtype);
+  if (bad_alias(out, b, x, b)) return MCF_E_ALIAS;
+  return hip_status(mcf::launch_elementwise(dtype, mcf::EW_SQUARE, nc, nc, n, x, 1, nullptr, 0, out,
+                                            (hipStream_t)stream));
+}
+
 int mc_exp(int dtype, int nc, int64_t n, const void *x, void *out, void *stream) {
   int st = check_common(dtype, nc, n);
   if (st != MCF_OK) return st;

@@ -78,4 +78,30 @@ __device__ __forceinline__ void mult_mcn_fast(const T (&x)[N], const T (&y)[N], 
   renormalize<T, N, N>(q, out);
 }
 
+// Mult-MCN-Slow (mcf_arith.hpp: mult_mcn_slow) with its DivN steps taken by
+// div_mcn_fast: the same bits.
+template <typename T, int N>
+__device__ __forceinline__ void mult_mcn_slow_fast(const T (&x_in)[N], const T (&y)[N], T (&out)[N]) {
+  T x[N];
+#pragma unroll
+  for (int c = 0; c < N; ++c) x[c] = x_in[c];
+  T h[N + 1];
+  T p = x[0] * y[0];
+  h[0] = p;
+#pragma unroll
+  for (int i = 1; i <= N; ++i) {
+    T pv[N], d[N], neg[N];
+    pv[0] = p;
+#pragma unroll
+    for (int c = 1; c < N; ++c) pv[c] = T(0);
+    div_mcn_fast<T, N>(pv, y, d);
+#pragma unroll
+    for (int c = 0; c < N; ++c) neg[c] = -d[c];
+    add_mcn<T, N>(x, neg, x);
+    p = x[0] * y[0];
+    h[i] = p;
+  }
+  simple_renorm<T, N + 1, N>(h, out);
+}
+
 }  // namespace mcf

@@ -98,6 +98,10 @@ __device__ __forceinline__ void elem(const T (&a)[NC], const T (&b)[NC], T (&r)[
     for (int c = 0; c < NC; ++c) ex[c] = exp32_cr(a[c]);
     const T h0[1] = {ex[0]};
     exp_chain<T, NC, 1>(h0, ex, r);
+  } else if constexpr (OP == EW_MUL_SLOW) {
+    mult_mcn_slow_fast<T, NC>(a, b, r);
+  } else if constexpr (OP == EW_SQUARE) {
+    square_mcn<T, NC>(a, r);
   } else if constexpr (OP == EW_RENORM) {
     renormalize<T, NC, NCOUT>(a, r);
   } else {
@@ -112,7 +116,8 @@ __device__ __forceinline__ void elem(const T (&a)[NC], const T (&b)[NC], T (&r)[
 template <typename T, int NC, int OP, bool XMC, bool YMC, int NCOUT, int W, int U>
 __device__ __forceinline__ void ew_chunks(const T *x, const T *y, T *out, int64_t n, const int64_t (&e0)[U]) {
   constexpr int XN = XMC ? NC : 1;
-  constexpr int YN = (OP == EW_RENORM || OP == EW_SIMPLE_RENORM || OP == EW_EXP) ? 0 : (YMC ? NC : 1);
+  constexpr int YN = (OP == EW_RENORM || OP == EW_SIMPLE_RENORM || OP == EW_EXP || OP == EW_SQUARE) ? 0
+                                                                                               : (YMC ? NC : 1);
   Pack<T, W> xa[U][XN];
   Pack<T, W> ya[U][YN > 0 ? YN : 1];
 #pragma unroll
@@ -235,6 +240,8 @@ static hipError_t ew_dispatch_nc(int op, int nc_out, int64_t n, const void *x, i
     case EW_ADD: return ew_kinds<T, NC, EW_ADD>(n, x, x_mc, y, y_mc, out, s);
     case EW_MUL: return ew_kinds<T, NC, EW_MUL>(n, x, x_mc, y, y_mc, out, s);
     case EW_DIV: return ew_kinds<T, NC, EW_DIV>(n, x, x_mc, y, y_mc, out, s);
+    case EW_MUL_SLOW: return ew_launch<T, NC, EW_MUL_SLOW, true, true, NC>(n, x, y, out, s);
+    case EW_SQUARE: return ew_launch<T, NC, EW_SQUARE, true, false, NC>(n, x, nullptr, out, s);
     case EW_RENORM: return renorm_dispatch<T, NC, EW_RENORM>(nc_out, n, x, out, s);
     case EW_SIMPLE_RENORM: return renorm_dispatch<T, NC, EW_SIMPLE_RENORM>(nc_out, n, x, out, s);
   }

@@ -197,4 +197,46 @@ __device__ __forceinline__ void mult_mcn(const T (&x)[N], const T (&y)[N], T (&o
   renormalize<T, N, N>(q, out);
 }
 
+// Mult-MCN-Slow: product digits by repeated division.  p = fl(x_0 y_0) is the first
+// digit; N times the remainder x = Add-MCN(x, -DivN(p, y)) is formed and its next
+// digit p = fl(x_0 y_0) taken; the N+1 digits pass through Simple-Renorm.
+template <typename T, int N>
+__device__ __forceinline__ void mult_mcn_slow(const T (&x_in)[N], const T (&y)[N], T (&out)[N]) {
+  T x[N];
+#pragma unroll
+  for (int c = 0; c < N; ++c) x[c] = x_in[c];
+  T h[N + 1];
+  T p = x[0] * y[0];
+  h[0] = p;
+#pragma unroll
+  for (int i = 1; i <= N; ++i) {
+    T pv[N], d[N], neg[N];
+    pv[0] = p;
+#pragma unroll
+    for (int c = 1; c < N; ++c) pv[c] = T(0);
+    div_mcn<T, N>(pv, y, d);  // DivN(p, y): the plain dividend padded with zeros
+#pragma unroll
+    for (int c = 0; c < N; ++c) neg[c] = -d[c];
+    add_mcn<T, N>(x, neg, x);
+    p = x[0] * y[0];
+    h[i] = p;
+  }
+  simple_renorm<T, N + 1, N>(h, out);
+}
+
+// Square-MCN.  The printed first step fl(2^(x_0)) is read as fl(x_0 x_0), the
+// square's leading term: h = (fl(x_0 x_0), 0, ..., 0), then h = Grow-ExpN(h,
+// fl(2 x_0 x_1)) (2 x_0 is exact, so the addend is one rounding of the product).
+// With N = 1 there is no x_1 and the addend is zero.
+template <typename T, int N>
+__device__ __forceinline__ void square_mcn(const T (&x)[N], T (&out)[N]) {
+  T h[N];
+  h[0] = x[0] * x[0];
+#pragma unroll
+  for (int c = 1; c < N; ++c) h[c] = T(0);
+  T v = T(0);
+  if constexpr (N > 1) v = (T(2) * x[0]) * x[1];
+  grow_expn<T, N>(h, v, out);
+}
+
 }  // namespace mcf

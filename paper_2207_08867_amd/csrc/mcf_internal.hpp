@@ -8,10 +8,12 @@
 
 namespace mcf {
 
-enum EwOp { EW_ADD = 0, EW_MUL = 1, EW_DIV = 2, EW_RENORM = 3, EW_SIMPLE_RENORM = 4, EW_EXP = 5 };
+enum EwOp { EW_ADD = 0, EW_MUL = 1, EW_DIV = 2, EW_RENORM = 3, EW_SIMPLE_RENORM = 4, EW_EXP = 5, EW_MUL_SLOW = 6,
+            EW_SQUARE = 7 };
 
-// Elementwise binary (add/mul/div) and renormalization launchers.  dtype 0 = binary16,
-// 1 = binary32.  For renormalization y is unused, nc is nc_in.
+// Elementwise binary (add/mul/div/Mult-MCN-Slow), Square-MCN and renormalization
+// launchers.  dtype 0 = binary16, 1 = binary32.  For the unary ones y is unused; for
+// renormalization nc is nc_in.
 hipError_t launch_elementwise(int dtype, int op, int nc, int nc_out, int64_t n, const void *x, int x_mc,
                               const void *y, int y_mc, void *out, hipStream_t stream);
 
