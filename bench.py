@@ -11,6 +11,7 @@ Also reported on the same line (not part of `value`):
   * roofline of the product kernel: algorithmic VALU operations per launch over the
     launch duration measured with HIP events, against the VALU issue peak;
   * the maximum error against the exact product on sampled outputs;
+  * the pruned MC x MC product (mc_matmul_pruned) on the headline operands;
   * the other workloads (64^3 binary32 nc=2; 1024^3 binary16 nc=2 and 3; the
     4096x1024x1024 binary16 nc=3 MC-Linear over 100 layers; the 2^26-element binary16
     nc=3 elementwise operations with their HBM bandwidth; the K-split Dot and MV; the
@@ -58,6 +59,13 @@ def algo_ops_per_mac(nc: int, mc_x_mc: bool) -> int:
     else:
         per = (2 + 9 * (nc - 2) + 2) + (6 + 13 * (nc - 2) + 2)
     return per * (nc if mc_x_mc else 1)
+
+
+def pruned_ops_per_mac(nc: int) -> int:
+    """Essential operations per multiply-add of the pruned MC x MC product: component p
+    of B drives an (nc - p)-component ScalingN + Add-MCN step (counted as in
+    algo_ops_per_mac): 34 + 12 + 2 = 48 at nc = 3."""
+    return sum(algo_ops_per_mac(nc - p, False) for p in range(nc))
 
 
 def ew_fp_ops(op: str, nc: int) -> int:
@@ -386,6 +394,24 @@ def main():
     }
     if not args.no_extra:
         extra = {}
+        log("pruned MC x MC product on the headline operands")
+        tA, tB = torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda()
+        Cp = torch.empty((nc, M, N), dtype=torch.float32, device="cuda")
+        mcf.mc_matmul_pruned(tA, tB, nc=nc, out=Cp)
+        torch.cuda.synchronize()
+        tm = Timer(torch)
+        for _ in range(args.steps):
+            tm.run(lambda: mcf.mc_matmul_pruned(tA, tB, nc=nc, out=Cp))
+        pms = float(np.mean(tm.ms()))
+        Cph = Cp.cpu().numpy()
+        del tA, tB, Cp
+        extra["matmul_pruned_8192_f32_nc3"] = {
+            "ms": round(pms, 3), "MC-GFLOP/s": round(2.0 * M * N * K / (pms * 1e-3) / 1e9, 2),
+            "ops_per_mac": pruned_ops_per_mac(nc),
+            "valu_frac": round(pruned_ops_per_mac(nc) * M * N * K / (pms * 1e-3) / VALU_PEAK, 4),
+            "error": exact_error(oracle, A, B, Cph, nc, K, np.float32)}
+        log(f"  pruned: {pms:.1f} ms")
+        del Cph
         A1, B1 = inputs.matmul_uniform(64, 64, 64, 2, np.float32, seed=0)
         C1, ms1, k1 = bench_matmul(torch, mcf, A1, B1, 2, 20, 3)
         extra["matmul_64_f32_nc2"] = {"us": round(k1 * 1e3, 1),

@@ -130,6 +130,20 @@ int mc_renorm(int dtype, int nc_in, int nc_out, int64_t n, const void *x, void *
 int mc_matmul(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B,
               int b_mc, void *C, void *stream);
 
+/* Pruned product of two MC matrices, a faster contraction with the accuracy class of
+ * mc_matmul (Section 2.2 leaves faster MC products open).  The component products
+ * A^(a) B^(b) with a + b >= nc are of the order of u^nc relative to A B -- the size of
+ * MM-MCN's own error -- and are left out: component b of B multiplies the first
+ * nc - b components of A, in MM-MCN order with nc - b components,
+ *   C = MM_nc(A, B^(0)) (+) MM_{nc-1}(A[:nc-1], B^(1)) (+) ... (+) MM_1(A[:1], B^(nc-1)),
+ * each part zero-padded to nc components, (+) = Add-MCN left to right.  A fixed
+ * function of the inputs (reproducible on any launch geometry) but not mc_matmul's
+ * bits: the error bound |C - C*| <= 4 K u^nc (|A||B|) is what it shares.  At nc = 3 it
+ * needs 48 essential operations per multiply-add against mc_matmul's 102.
+ * A: [nc][M][K], B: [nc][K][N], C: [nc][M][N], C not overlapping A or B. */
+int mc_matmul_pruned(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, const void *B, void *C,
+                     void *stream);
+
 /* Batched and broadcast matrix products, BMM-MCN and 4DMM-MCN (Appendix A.2.2): for
  * every batch index (i1, i2) in [0, B1) x [0, B2), the matrices of A and B at that
  * index are multiplied exactly as mc_matmul multiplies its operands (MM-MCN order;

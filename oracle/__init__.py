@@ -71,6 +71,8 @@ def lib() -> ctypes.CDLL:
         L.mcf_oracle_elementwise.argtypes = [ci, ci, ci, ci, i64, vp, ci, vp, ci, vp]
         L.mcf_oracle_matmul.restype = ci
         L.mcf_oracle_matmul.argtypes = [ci, ci, i64, i64, i64, vp, ci, vp, ci, vp, vp, i64, vp]
+        L.mcf_oracle_matmul_pruned.restype = ci
+        L.mcf_oracle_matmul_pruned.argtypes = [ci, ci, i64, i64, i64, vp, vp, vp, vp, i64, vp]
         L.mcf_oracle_matmul_splitk.restype = ci
         L.mcf_oracle_matmul_splitk.argtypes = [ci, ci, i64, i64, i64, vp, ci, vp, ci, i64, vp, vp, i64, vp]
         L.mcf_oracle_linear.restype = ci
@@ -291,6 +293,27 @@ def matmul(A, B, *, nc, a_mc=True, b_mc=True, rows=None, cols=None):
     out = np.empty((nc, count), dtype=dtype)
     rc = lib().mcf_oracle_matmul(fmt, nc, M, N, K, _ptr(A), int(a_mc), _ptr(B), int(b_mc), _ptr(r), _ptr(c),
                                  count, _ptr(out))
+    if rc != 0:
+        raise ValueError("oracle: bad arguments")
+    return out.reshape(nc, M, N) if rows is None else out
+
+
+def matmul_pruned(A, B, *, nc, rows=None, cols=None):
+    """Pruned MC x MC product: C = MM_nc(A, B^(0)) (+) MM_{nc-1}(A[:nc-1], B^(1)) (+) ...
+    (+) MM_1(A[:1], B^(nc-1)), each part in MM-MCN order with the stated number of
+    components, zero-padded to nc, combined left to right by Add-MCN.
+    A: (nc, M, K), B: (nc, K, N).  Returns (nc, M, N), or (nc, count) at positions."""
+    dtype = np.dtype(A.dtype)
+    fmt = fmt_of(dtype)
+    A = _planar(A, dtype)
+    B = _planar(B, dtype)
+    M, K = A.shape[1:]
+    K2, N = B.shape[1:]
+    if K2 != K or A.shape[0] != nc or B.shape[0] != nc:
+        raise ValueError("matmul_pruned: shape mismatch")
+    r, c, count = _positions(M, N, rows, cols)
+    out = np.empty((nc, count), dtype=dtype)
+    rc = lib().mcf_oracle_matmul_pruned(fmt, nc, M, N, K, _ptr(A), _ptr(B), _ptr(r), _ptr(c), count, _ptr(out))
     if rc != 0:
         raise ValueError("oracle: bad arguments")
     return out.reshape(nc, M, N) if rows is None else out

@@ -609,6 +609,41 @@ static void mm_entry(const mm_args *g, int nc, int64_t i, int64_t j, double *out
   }
 }
 
+/* Pruned MC x MC product, one output (a reading of the faster contraction the paper
+ * leaves open, Section 2.2: the component products A^(a) B^(b) with a + b >= nc are
+ * of the order of u^nc relative, the size of MM-MCN's own error, and are left out).
+ * Component b of B multiplies the first nc - b components of A in MM-MCN order with
+ * nc - b components; the parts, padded with zeros to nc components, are combined
+ * left to right with Add-MCN:
+ *   C = MM_nc(A, B^(0)) (+) MM_{nc-1}(A[:nc-1], B^(1)) (+) ... (+) MM_1(A[:1], B^(nc-1)). */
+static void mm_entry_pruned(const mm_args *g, int nc, int64_t i, int64_t j, double *out) {
+  double part[MAXC], t[MAXC];
+  mm_entry_plain(g, nc, i, j, 0, 0, 1, out);
+  for (int b = 1; b < nc; ++b) {
+    for (int c = 0; c < MAXC; ++c) part[c] = 0.0;
+    mm_entry_plain(g, nc - b, i, j, b, 0, 1, part);
+    add_mcn(g->f, out, part, nc, t);
+    for (int c = 0; c < nc; ++c) out[c] = t[c];
+  }
+}
+
+/* The pruned product of two MC matrices at the `count` positions (as
+ * mcf_oracle_matmul with both operands MC). */
+int mcf_oracle_matmul_pruned(int f, int nc, int64_t M, int64_t N, int64_t K, const void *A, const void *B,
+                             const int64_t *rows, const int64_t *cols, int64_t count, void *out) {
+  if (nc < 1 || nc > MAXC) return -1;
+  mm_args g = {f, A, 1, B, 1, K, K, 1, N, 1, M * K, K * N};
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t t = 0; t < count; ++t) {
+    int64_t i = rows ? rows[t] : t / N;
+    int64_t j = rows ? cols[t] : t % N;
+    double r[MAXC];
+    mm_entry_pruned(&g, nc, i, j, r);
+    scatter(f, out, nc, count, t, r);
+  }
+  return 0;
+}
+
 /* C = A x B with A [M][K] and B [K][N] row-major planes (nc planes when MC, one when
  * plain; at least one MC), evaluated only at the `count` positions (rows[t], cols[t]);
  * out is [nc][count].  rows == NULL means every position in row-major order (count

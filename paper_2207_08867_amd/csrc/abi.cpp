@@ -154,6 +154,33 @@ int mc_matmul(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A,
   return hip_status(mcf::launch_matmul(dtype, nc, M, N, K, A, a_mc, B, b_mc, 0, nullptr, C, (hipStream_t)stream));
 }
 
+int mc_matmul_pruned(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, const void *B, void *C,
+                     void *stream) {
+  if (dtype != MCF_F16 && dtype != MCF_F32) return MCF_E_DTYPE;
+  if (nc < 1 || nc > MAX_NC) return MCF_E_NC;
+  if (M < 0 || N < 0 || K < 0) return MCF_E_SHAPE;
+  if (M > ((int64_t)1 << 20) || N > ((int64_t)1 << 30) || K > ((int64_t)1 << 40)) return MCF_E_SHAPE;
+  if (!grid_fits(M, N)) return MCF_E_SHAPE;
+  if (M == 0 || N == 0) return MCF_OK;
+  if (!C || (K > 0 && (!A || !B))) return MCF_E_NULL;
+  const int64_t es = elem_size(dtype);
+  const int64_t cb = nc * M * N * es;
+  if (overlap(C, cb, A, nc * M * K * es) || overlap(C, cb, B, nc * K * N * es)) return MCF_E_ALIAS;
+  mcf::MmLaunch L;
+  L.dtype = dtype;
+  L.nc = nc;
+  L.M = M;
+  L.N = N;
+  L.K = K;
+  L.A = A;
+  L.a_plane = M * K;
+  L.B = B;
+  L.b_plane = K * N;
+  L.C = C;
+  L.prune = 1;
+  return hip_status(mcf::launch_matmul_general(L, (hipStream_t)stream));
+}
+
 int mc_matmul_batched(int dtype, int nc, int64_t B1, int64_t B2, int64_t M, int64_t N, int64_t K, const void *A,
                       int a_mc, int64_t a_plane, int64_t a_s1, int64_t a_s2, const void *B, int b_mc,
                       int64_t b_plane, int64_t b_s1, int64_t b_s2, void *C, void *stream) {

@@ -50,7 +50,7 @@ struct Operands {
 // arithmetic; GROUP = true: the arithmetic of all terms of a step shares one
 // straight-line block and one (rarely taken) compaction branch.
 template <typename T, int NC, bool AMC, bool BMC, int TM, int TN, int KT, int BM, int BN, int SPOL, int APOL,
-          bool GROUP>
+          bool GROUP, bool PRUNE>
 struct Lane {
   static constexpr int NA = AMC ? NC : 1;
   static constexpr int NB = BMC ? NC : 1;
@@ -138,39 +138,63 @@ struct Lane {
   // general step.  HEAD / TAIL: the products' errors are known to be zero (see mm_kernel).
   template <bool HEAD, bool TAIL>
   __device__ __forceinline__ void scale_kept(const T (&x)[NC], T v, T (&t)[NC]) {
-    T last;
-    scaling_kept<T, NC, HEAD, TAIL>(x, v, t, last);
-    if (__builtin_expect(kept_invalid<T, NC, TAIL>(t, last), 0)) {
-      T h[NC + 1];
-      scaling_terms<T, NC>(x, v, h);
-      compact_nz<T, NC + 1, NC>(h, t);
-    }
+    kept_scale<T, NC, HEAD, TAIL>(x, v, t);
   }
 
   // a = Add-MCN(a, t) in kept-terms form (TINY: the add_tiny form)
   template <bool TINY>
   __device__ __forceinline__ void add_kept_into(T (&a)[NC], const T (&t)[NC]) {
-    T s[NC], last;
-    bool bad;
-    if constexpr (TINY) {
-      bad = add_tiny<T, NC>(a, t, s);
-    } else {
-      add_kept<T, NC>(a, t, s, last);
-      bad = kept_invalid<T, NC, false>(s, last);
-    }
-    if (__builtin_expect(bad, 0)) {
-      T h[NC + 1];
-      add_terms<T, NC>(a, t, h);
-      compact_nz<T, NC + 1, NC>(h, s);
-    }
+    kept_add<T, NC, TINY>(a, t);
+  }
+
+  // Pruned MC x MC product: component P of B multiplies the first NC - P components
+  // of A in MM-MCN order with NC - P components; the accumulator of P keeps zeros in
+  // its other components, so the epilogue's Add-MCN combination pads it with zeros.
+  // FIRST: the step initialises the accumulators (every P, whatever PMASK says).
+  template <int P, int PMASK, bool TPS, bool FIRST>
+  __device__ __forceinline__ void prune_step(const Ops &o) {
+    if constexpr (P < NP) {
+      if constexpr (FIRST || ((PMASK >> P) & 1)) {
+        constexpr int NCP = NC - P;
 #pragma unroll
-    for (int c = 0; c < NC; ++c) a[c] = s[c];
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j) {
+            const T(&a)[NCP] = *reinterpret_cast<const T(*)[NCP]>(&o.a[i][0]);
+            T(&ac)[NCP] = *reinterpret_cast<T(*)[NCP]>(&acc[P][i][j][0]);
+            const T v = o.b[j][P];
+            T t[NCP];
+            if constexpr (SPOL == SR_SUFFIX) {
+              kept_scale<T, NCP, TPS && (P > 0), TPS>(a, v, t);
+            } else {
+              T h[NCP + 1];
+              scaling_terms<T, NCP>(a, v, h);
+              if (__builtin_expect(sr_try<T, NCP, SPOL>(h, t, v == T(0)), 0)) compact_nz<T, NCP + 1, NCP>(h, t);
+            }
+            if constexpr (FIRST) {
+#pragma unroll
+              for (int c = 0; c < NCP; ++c) ac[c] = t[c];
+#pragma unroll
+              for (int c = NCP; c < NC; ++c) acc[P][i][j][c] = T(0);
+            } else if constexpr (SPOL == SR_SUFFIX) {
+              kept_add<T, NCP, TPS && (P > 0)>(ac, t);
+            } else {
+              T h[NCP + 1];
+              add_terms<T, NCP>(ac, t, h);
+              if (__builtin_expect(sr_try<T, NCP, APOL>(h, ac), 0)) compact_nz<T, NCP + 1, NCP>(h, ac);
+            }
+          }
+      }
+      prune_step<P + 1, PMASK, TPS, FIRST>(o);
+    }
   }
 
   // term k = 0 initialises the accumulators
   template <bool TPS>
   __device__ __forceinline__ void first(const Ops &o) {
-    if constexpr (SPOL == SR_SUFFIX) {
+    if constexpr (PRUNE) {
+      prune_step<0, (1 << NP) - 1, TPS, true>(o);
+    } else if constexpr (SPOL == SR_SUFFIX) {
 #pragma unroll
       for (int p = 0; p < NP; ++p)
 #pragma unroll
@@ -279,6 +303,15 @@ struct Lane {
                                       int ty) {
     // two steps per loop iteration, so the accumulators keep their registers across
     // the back edge instead of being copied
+    if constexpr (PRUNE) {
+#pragma unroll 2
+      for (int kk = kk0; kk < kt; ++kk) {
+        Ops o;
+        o.load(As, Bs, kk, tx, ty);
+        prune_step<0, PMASK, TPS, false>(o);
+      }
+      return;
+    }
     if constexpr (SPOL == SR_SUFFIX && NC == 2) {
       // nc = 2: the tests of two steps share one branch.  (For nc >= 3 grouping keeps
       // more temporaries live, lowers the wavefronts per SIMD and was measured
@@ -388,7 +421,7 @@ struct MmArgs {
 // sit just under that bound (the 8192^3 one spills one 8-byte value outside its loop)
 // and one register more would drop them to 4.  nc = 4 needs more registers.
 template <typename T, int NC, bool AMC, bool BMC, bool BT, int TM, int TN, int KT, int SPOL, int APOL,
-          bool GROUP, bool ADDMM>
+          bool GROUP, bool ADDMM, bool PRUNE>
 __global__ __attribute__((amdgpu_flat_work_group_size(1, MM_THREADS), amdgpu_waves_per_eu(NC <= 3 ? 5 : 1))) void
 mm_kernel(const T *__restrict__ A, const T *__restrict__ B,
                                                         T *__restrict__ C, const MmArgs<T> g) {
@@ -416,7 +449,7 @@ mm_kernel(const T *__restrict__ A, const T *__restrict__ B,
   m0 *= BM;
   n0 *= BN;
 
-  Lane<T, NC, AMC, BMC, TM, TN, KT, BM, BN, SPOL, APOL, GROUP> lane;
+  Lane<T, NC, AMC, BMC, TM, TN, KT, BM, BN, SPOL, APOL, GROUP, PRUNE> lane;
   auto &acc = lane.acc;
 
   // Each thread stages A_PER elements of the A tile and B_PER of the B tile per
@@ -597,7 +630,8 @@ mm_kernel(const T *__restrict__ A, const T *__restrict__ B,
 // Batches go to grid y, at most MM_MAX_GRID_Y per launch.
 constexpr int64_t MM_MAX_GRID_Y = 65535;
 
-template <typename T, int NC, bool AMC, bool BMC, bool BT, int TM, int TN, int SPOL, int APOL, int KT = 16>
+template <typename T, int NC, bool AMC, bool BMC, bool BT, int TM, int TN, int SPOL, int APOL, int KT = 16,
+          bool PRUNE = false>
 static hipError_t mm_launch_tile(MmArgs<T> g, int64_t batches, const void *A, const void *B, void *C,
                                  hipStream_t s) {
   constexpr int BM = 16 * TM, BN = 16 * TN;
@@ -606,10 +640,10 @@ static hipError_t mm_launch_tile(MmArgs<T> g, int64_t batches, const void *A, co
     g.bb0 = b0;
     const int64_t nb = (batches - b0) < MM_MAX_GRID_Y ? (batches - b0) : MM_MAX_GRID_Y;
     if (g.mode == 2)  // the AddMM epilogue is a separate instantiation: it needs more registers
-      hipLaunchKernelGGL((mm_kernel<T, NC, AMC, BMC, BT, TM, TN, KT, SPOL, APOL, false, true>),
+      hipLaunchKernelGGL((mm_kernel<T, NC, AMC, BMC, BT, TM, TN, KT, SPOL, APOL, false, true, PRUNE>),
                          dim3(gx, (unsigned)nb), dim3(MM_THREADS), 0, s, (const T *)A, (const T *)B, (T *)C, g);
     else
-      hipLaunchKernelGGL((mm_kernel<T, NC, AMC, BMC, BT, TM, TN, KT, SPOL, APOL, false, false>),
+      hipLaunchKernelGGL((mm_kernel<T, NC, AMC, BMC, BT, TM, TN, KT, SPOL, APOL, false, false, PRUNE>),
                          dim3(gx, (unsigned)nb), dim3(MM_THREADS), 0, s, (const T *)A, (const T *)B, (T *)C, g);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -624,26 +658,30 @@ static hipError_t mm_launch_tile(MmArgs<T> g, int64_t batches, const void *A, co
 //             on its 4096 x 1024 x 1024 layer); the low terms of a step are often zero (they fall
 //             below the subnormal grid), almost always as a trailing run, so both steps
 //             use the kept-terms form (SR_SUFFIX), which skips the final carry.
-template <typename T, int NC, bool AMC, bool BMC, bool BT>
+template <typename T, int NC, bool AMC, bool BMC, bool BT, bool PRUNE = false>
 static hipError_t mm_launch(const MmArgs<T> &g, int64_t batches, const void *A, const void *B, void *C,
                             hipStream_t s) {
   if constexpr (sizeof(T) == 4) {
     if (g.M * g.N >= ((int64_t)1 << 25))
-      return mm_launch_tile<T, NC, AMC, BMC, BT, 1, 2, SR_FULL, SR_FULL>(g, batches, A, B, C, s);
-    return mm_launch_tile<T, NC, AMC, BMC, BT, 1, 1, SR_FULL, SR_FULL>(g, batches, A, B, C, s);
+      return mm_launch_tile<T, NC, AMC, BMC, BT, 1, 2, SR_FULL, SR_FULL, 16, PRUNE>(g, batches, A, B, C, s);
+    return mm_launch_tile<T, NC, AMC, BMC, BT, 1, 1, SR_FULL, SR_FULL, 16, PRUNE>(g, batches, A, B, C, s);
   } else {
     if constexpr (BT)  // MC-Linear: two rows of x per lane share each weight value
       return mm_launch_tile<T, NC, AMC, BMC, BT, 2, 1, SR_SUFFIX, SR_SUFFIX>(g, batches, A, B, C, s);
     // nc = 2: 32-step LDS tiles halve the per-tile staging and barriers, which weigh
     // more against its short steps (8% faster on 1024^3; flat or slower at nc >= 3)
     constexpr int KT = NC == 2 ? 32 : 16;
-    return mm_launch_tile<T, NC, AMC, BMC, BT, 1, 1, SR_SUFFIX, SR_SUFFIX, KT>(g, batches, A, B, C, s);
+    return mm_launch_tile<T, NC, AMC, BMC, BT, 1, 1, SR_SUFFIX, SR_SUFFIX, KT, PRUNE>(g, batches, A, B, C, s);
   }
 }
 
 template <typename T, int NC>
 static hipError_t mm_kinds(const MmArgs<T> &g, int64_t batches, const void *A, int a_mc, const void *B, int b_mc,
-                           int b_trans, void *C, hipStream_t s) {
+                           int b_trans, int prune, void *C, hipStream_t s) {
+  if (prune) {  // pruned MC x MC product
+    if (a_mc && b_mc && !b_trans) return mm_launch<T, NC, true, true, false, true>(g, batches, A, B, C, s);
+    return hipErrorInvalidValue;
+  }
   if (b_trans) {
     // linear layer: plain input times MC weight stored [out][in]
     if (!a_mc && b_mc) return mm_launch<T, NC, false, true, true>(g, batches, A, B, C, s);
@@ -656,12 +694,12 @@ static hipError_t mm_kinds(const MmArgs<T> &g, int64_t batches, const void *A, i
 
 template <typename T>
 static hipError_t mm_dispatch(int nc, const MmArgs<T> &g, int64_t batches, const void *A, int a_mc, const void *B,
-                              int b_mc, int b_trans, void *C, hipStream_t s) {
+                              int b_mc, int b_trans, int prune, void *C, hipStream_t s) {
   switch (nc) {
-    case 1: return mm_kinds<T, 1>(g, batches, A, a_mc, B, b_mc, b_trans, C, s);
-    case 2: return mm_kinds<T, 2>(g, batches, A, a_mc, B, b_mc, b_trans, C, s);
-    case 3: return mm_kinds<T, 3>(g, batches, A, a_mc, B, b_mc, b_trans, C, s);
-    case 4: return mm_kinds<T, 4>(g, batches, A, a_mc, B, b_mc, b_trans, C, s);
+    case 1: return mm_kinds<T, 1>(g, batches, A, a_mc, B, b_mc, b_trans, prune, C, s);
+    case 2: return mm_kinds<T, 2>(g, batches, A, a_mc, B, b_mc, b_trans, prune, C, s);
+    case 3: return mm_kinds<T, 3>(g, batches, A, a_mc, B, b_mc, b_trans, prune, C, s);
+    case 4: return mm_kinds<T, 4>(g, batches, A, a_mc, B, b_mc, b_trans, prune, C, s);
   }
   return hipErrorInvalidValue;
 }
@@ -687,7 +725,7 @@ static hipError_t mm_typed(const MmLaunch &L, hipStream_t s) {
   g.y_ld = L.y_ld;
   g.alpha = (T)L.alpha;
   g.beta = (T)L.beta;
-  return mm_dispatch<T>(L.nc, g, L.B1 * L.B2, L.A, L.a_mc, L.B, L.b_mc, L.b_trans, L.C, s);
+  return mm_dispatch<T>(L.nc, g, L.B1 * L.B2, L.A, L.a_mc, L.B, L.b_mc, L.b_trans, L.prune, L.C, s);
 }
 
 hipError_t launch_matmul_general(const MmLaunch &L, hipStream_t stream) {

@@ -40,6 +40,7 @@ struct MmLaunch {
   const void *y = nullptr;
   int64_t y_plane = 0, y_ld = 0;
   double alpha = 1.0, beta = 1.0;
+  int prune = 0;  // 1: the pruned MC x MC product (both operands MC, no epilogue)
 };
 hipError_t launch_matmul_general(const MmLaunch &L, hipStream_t stream);
 

@@ -79,7 +79,11 @@ enum SrPolicy { SR_FULL = 0, SR_SELECT = 1, SR_HEAD = 2, SR_NET = 3, SR_SUFFIX =
 
 template <typename T, int N, int POL>
 __device__ __forceinline__ bool sr_try(const T (&h)[N + 1], T (&out)[N], bool ok = false) {
-  if constexpr (N == 1) {
+  if constexpr (N == 1 && POL == SR_FULL) {
+    // keep h_0 when it is non-zero; the dropped h_1 is then never needed
+    out[0] = h[0];
+    return !(ok || h[0] != T(0));
+  } else if constexpr (N == 1) {
     out[0] = (h[0] != T(0)) ? h[0] : h[1];
     return false;
   } else if constexpr (POL == SR_NET) {
@@ -267,6 +271,39 @@ __device__ __forceinline__ bool kept_invalid(const T (&h)[N], T last) {
     if constexpr (LAST_EXACT) return bad;
     return bad | (z[N - 1] & !abs_below(last, (T)exact_limit<T>()));
   }
+}
+
+// ScalingN of (x, v) in kept-terms form into t; lanes failing the test run the
+// general step.  HEAD / TAIL: the products' errors are known to be zero.
+template <typename T, int N, bool HEAD, bool TAIL>
+__device__ __forceinline__ void kept_scale(const T (&x)[N], T v, T (&t)[N]) {
+  T last;
+  scaling_kept<T, N, HEAD, TAIL>(x, v, t, last);
+  if (__builtin_expect(kept_invalid<T, N, TAIL>(t, last), 0)) {
+    T h[N + 1];
+    scaling_terms<T, N>(x, v, h);
+    compact_nz<T, N + 1, N>(h, t);
+  }
+}
+
+// a = Add-MCN(a, t) in kept-terms form (TINY: the add_tiny form).
+template <typename T, int N, bool TINY>
+__device__ __forceinline__ void kept_add(T (&a)[N], const T (&t)[N]) {
+  T s[N], last;
+  bool bad;
+  if constexpr (TINY) {
+    bad = add_tiny<T, N>(a, t, s);
+  } else {
+    add_kept<T, N>(a, t, s, last);
+    bad = kept_invalid<T, N, false>(s, last);
+  }
+  if (__builtin_expect(bad, 0)) {
+    T h[N + 1];
+    add_terms<T, N>(a, t, h);
+    compact_nz<T, N + 1, N>(h, s);
+  }
+#pragma unroll
+  for (int c = 0; c < N; ++c) a[c] = s[c];
 }
 
 // out = Add-MCN(x, y) for one value (the epilogue's combinations).

@@ -174,3 +174,54 @@ def test_degenerate_sizes(orc):
     B = np.zeros((nc, 0, 4), dtype=dt)
     C = orc.matmul(A, B, nc=nc)
     assert C.shape == (nc, 3, 4) and (C == 0).all() and not np.signbit(C).any()
+
+
+# ---------------------------------------------------------------------------------
+# pruned MC x MC product
+# ---------------------------------------------------------------------------------
+
+def _seq_gemm(A, B, dt):
+    acc = (A[:, 0][:, None] * B[0][None, :]).astype(dt)
+    for k in range(1, A.shape[1]):
+        acc = (acc + (A[:, k][:, None] * B[k][None, :]).astype(dt)).astype(dt)
+    return acc
+
+
+@pytest.mark.parametrize("dt", [np.float16, np.float32])
+def test_pruned_nc1_and_nc2_structure(orc, dt):
+    """nc = 1: nothing is pruned (the product is MM-MCN).  nc = 2: the pruned product
+    is Add-MCN(MM-MCN(A, B^(0)), (G, 0)) with G the sequential float GEMM of A^(0) and
+    B^(1), evaluated by numpy."""
+    A, B = inputs.matmul_normal(9, 7, 11, 1, dt, seed=31)
+    assert np.array_equal(orc.matmul_pruned(A, B, nc=1), orc.matmul(A, B, nc=1))
+    A, B = inputs.matmul_normal(9, 7, 11, 2, dt, seed=32)
+    P0 = orc.matmul(A, B[:1], nc=2, a_mc=True, b_mc=False)
+    G = _seq_gemm(A[0], B[1], dt)
+    want = orc.add(P0, np.stack([G, np.zeros_like(G)]), nc=2)
+    assert np.array_equal(orc.matmul_pruned(A, B, nc=2), want)
+
+
+@pytest.mark.parametrize("dt", [np.float16, np.float32])
+@pytest.mark.parametrize("nc", [2, 3, 4])
+def test_pruned_zero_low_components_of_b(orc, dt, nc):
+    """When B's low components are zero, nothing is left out: the pruned product is
+    MM-MCN bit for bit."""
+    A, B = inputs.matmul_normal(12, 10, 9, nc, dt, seed=33)
+    B[1:] = 0
+    assert np.array_equal(orc.matmul_pruned(A, B, nc=nc), orc.matmul(A, B, nc=nc))
+
+
+@pytest.mark.parametrize("dt", [np.float16, np.float32])
+@pytest.mark.parametrize("nc", [2, 3, 4])
+def test_pruned_exact_bound(orc, dt, nc):
+    """Within 4 K u^min(nc,3) (|A||B|) (+ the binary16 floor) of the exact product."""
+    for M, N, K, gen in ((16, 12, 300, "normal"), (8, 8, 64, "uniform")):
+        if gen == "normal":
+            A, B = inputs.matmul_normal(M, N, K, nc, dt, seed=34)
+        else:
+            A, B = inputs.matmul_uniform(M, N, K, nc, dt, seed=34)
+        C = orc.matmul_pruned(A, B, nc=nc)
+        err, absab, _ = orc.matmul_exact_err(A, B, C)
+        u = U[dt]
+        floor = nc * nc * K * 2.0 ** -25 if dt == np.float16 else 0.0
+        assert (np.abs(err) <= 4 * K * u ** min(nc, 3) * absab + floor).all()
