@@ -11,7 +11,8 @@
  * Memory.  All tensor pointers are DEVICE pointers owned by the caller; the library
  *   allocates nothing per call and keeps no state besides a per-device binary16
  *   exponential table (128 KiB, built on the first mc_exp call on a device).  Calls
- *   that need scratch memory (mc_matmul_splitk) take a caller-owned workspace.
+ *   that need scratch memory (mc_matmul_splitk, mc_matmul_exact) take a
+ *   caller-owned workspace.
  * Layout.  Dense, component-major ("planar"): component c of element i of an MC
  *   array of n elements is at element offset c*n + i.  A plain tensor is one plane.
  *   Matrices are row-major inside each plane.  The paper's interleaved layout
@@ -204,6 +205,37 @@ int64_t mc_matmul_splitk_slices(int64_t M, int64_t N, int64_t K);
  * negative mcf_status for arguments mc_matmul_splitk would reject. */
 int64_t mc_matmul_splitk_workspace(int dtype, int nc, int64_t M, int64_t N, int64_t K, int a_mc, int b_mc,
                                    int64_t slices);
+
+/* Exact MC product for binary16 components, rounded into nc components.  An MC
+ * number is the unevaluated sum of its components (Section 2.1), so every output has
+ * one exact value P_ij = sum_k (sum_c A^(c)_ik)(sum_c B^(c)_kj), the quantity that
+ * MM-MCN (Section 2.2) approximates within about 4 K u^nc sum_k |A_ik||B_kj|
+ * (Section 2.4).  This call returns P_ij split by successive round-to-nearest-even
+ * into binary16: c_0 = RN(P), c_1 = RN(P - c_0), ..., so the components never
+ * overlap and their sum is within half an ulp of c_{nc-1} (at most 2^-25 absolute
+ * in the subnormal range) of P.  Not mc_matmul's bits: a different, more accurate
+ * result.  The contraction runs on the int8 matrix cores: each entry is an exact
+ * integer multiple of 2^-24, cut into 7-bit digits whose products are summed
+ * exactly.
+ * dtype: MCF_F16 only (else MCF_E_DTYPE).
+ * Special values (input values ARE inspected here): an output whose row of A or
+ *   column of B holds an infinite or NaN component is NaN in every component; if
+ *   |P| rounds above 65504 the result is (+-inf, +0, ..., +0); an exact zero gives +0
+ *   in every component, a non-zero P that rounds to zero keeps its sign.
+ * A: [nc or 1][M][K]; B: [nc or 1][K][N], or [nc or 1][N][K] when b_trans = 1 (a
+ *   linear layer's weight); C: [nc][M][N], not overlapping A or B.
+ * workspace: device memory of at least mc_matmul_exact_workspace(...) bytes, owned by
+ *   the caller, not overlapping A, B or C (else MCF_E_ALIAS); contents on entry do
+ *   not matter; calls sharing a workspace must not overlap in time.  Too small:
+ *   MCF_E_ARG; NULL: MCF_E_NULL.
+ * Sizes: M, N, K <= 2^31 and (M + N) K <= 2^40 (else MCF_E_SHAPE). */
+int mc_matmul_exact(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B,
+                    int b_mc, int b_trans, void *workspace, int64_t workspace_bytes, void *C, void *stream);
+
+/* Workspace bytes mc_matmul_exact needs (about 7 (M + N) K bytes of digit planes,
+ * plus 16 M N bytes of partial sums when K > 65536), or a negative mcf_status for
+ * sizes it would reject. */
+int64_t mc_matmul_exact_workspace(int dtype, int nc, int64_t M, int64_t N, int64_t K);
 
 /* MC-Linear forward (Section 2.3): y = x W^T (+ b).  The weight and bias are MC,
  * the input is a plain tensor; each output accumulates ScalingN(W[o][i], x[t][i])

@@ -21,7 +21,7 @@ __all__ = [
     "mc_add", "mc_mul", "mc_div", "mc_exp", "mc_renorm", "mc_matmul", "mc_matmul_splitk",
     "mc_matmul_splitk_slices", "mc_matmul_splitk_workspace", "mc_linear_fwd", "mc_status_str",
     "mc_matmul_batched", "mc_bmm", "mc_addmm", "matmul_mcn", "mc_mul_slow", "mc_square", "mc_matmul_pruned",
-    "lib", "LIB_PATH", "MCFError",
+    "mc_matmul_exact", "mc_matmul_exact_workspace", "lib", "LIB_PATH", "MCFError",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmcf.so")
@@ -71,6 +71,10 @@ def lib() -> ctypes.CDLL:
         L.mc_addmm.restype = ci
         L.mc_addmm.argtypes = [ci, ci, i64, i64, i64, vp, ci, vp, ci, vp, i64, ctypes.c_double, ctypes.c_double,
                                vp, vp]
+        L.mc_matmul_exact.restype = ci
+        L.mc_matmul_exact.argtypes = [ci, ci, i64, i64, i64, vp, ci, vp, ci, ci, vp, i64, vp, vp]
+        L.mc_matmul_exact_workspace.restype = i64
+        L.mc_matmul_exact_workspace.argtypes = [ci, ci, i64, i64, i64]
         L.mc_linear_fwd.restype = ci
         L.mc_linear_fwd.argtypes = [ci, ci, i64, i64, i64, vp, vp, vp, vp, vp]
         L.mc_status_str.restype = ctypes.c_char_p
@@ -297,6 +301,37 @@ def mc_matmul_splitk(A, B, *, nc: int, a_mc: bool = True, b_mc: bool = True, sli
     st = lib().mc_matmul_splitk(code, nc, M, N, K, _dev(A3, "A"), int(bool(a_mc)), _dev(B3, "B"), int(bool(b_mc)),
                                 int(slices), wp, wn, _dev(out, "out"), _stream(A))
     _check(st, "mc_matmul_splitk")
+    return out
+
+
+def mc_matmul_exact_workspace(nc: int, M: int, N: int, K: int) -> int:
+    """Workspace bytes the exact binary16 product needs."""
+    w = lib().mc_matmul_exact_workspace(MCF_F16, nc, M, N, K)
+    _check(int(w) if w < 0 else 0, "mc_matmul_exact_workspace")
+    return int(w)
+
+
+def mc_matmul_exact(A, B, *, nc: int, a_mc: bool = True, b_mc: bool = True, b_trans: bool = False, out=None,
+                    workspace=None):
+    """The exact product of binary16 MC matrices split into nc components by
+    successive rounding (int8 matrix cores).  A: (nc|1, M, K); B: (nc|1, K, N), or
+    (nc|1, N, K) with b_trans -> (nc, M, N).  `workspace`: an optional device byte
+    tensor; one is allocated here when not given."""
+    torch = _torch()
+    if b_trans:
+        Bv = B if B.dim() == 3 else B.reshape((1,) + tuple(B.shape))
+        A3, _, M, N, K, out = _mm_operands(A, Bv.transpose(1, 2), nc, a_mc, b_mc, out)
+        B3 = Bv
+    else:
+        A3, B3, M, N, K, out = _mm_operands(A, B, nc, a_mc, b_mc, out)
+    wb = mc_matmul_exact_workspace(nc, M, N, K)
+    if workspace is None:
+        workspace = torch.empty(max(wb, 1), dtype=torch.uint8, device=A.device)
+    wn = workspace.numel() * workspace.element_size()
+    st = lib().mc_matmul_exact(_dtype_code(A), nc, M, N, K, _dev(A3, "A"), int(bool(a_mc)), _dev(B3, "B"),
+                               int(bool(b_mc)), int(bool(b_trans)), _dev(workspace, "workspace"), wn,
+                               _dev(out, "out"), _stream(A))
+    _check(st, "mc_matmul_exact")
     return out
 
 

@@ -79,6 +79,19 @@ int64_t splitk_workspace_bytes(int dtype, int nc, int64_t M, int64_t N, int64_t 
   return (int64_t)G * np * nc * M * N * elem_size(dtype);
 }
 
+int exact_check(int dtype, int nc, int64_t M, int64_t N, int64_t K, int a_mc, int b_mc, int b_trans) {
+  if (dtype != MCF_F16) return MCF_E_DTYPE;
+  if (nc < 1 || nc > MAX_NC) return MCF_E_NC;
+  if ((a_mc != 0 && a_mc != 1) || (b_mc != 0 && b_mc != 1) || (b_trans != 0 && b_trans != 1)) return MCF_E_ARG;
+  if (M < 0 || N < 0 || K < 0) return MCF_E_SHAPE;
+  // digit planes of 7 (M + N) K bytes, grids of (M / 32) (N / 32) workgroups, K chunks
+  // of 65536 in the second grid dimension
+  if (M > ((int64_t)1 << 31) || N > ((int64_t)1 << 31) || K > ((int64_t)1 << 31)) return MCF_E_SHAPE;
+  if ((M + N) > 0 && K > ((int64_t)1 << 40) / (M + N + 128)) return MCF_E_SHAPE;
+  if (((M + 63) / 32) * ((N + 63) / 32) >= ((int64_t)1 << 31)) return MCF_E_SHAPE;
+  return MCF_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -303,6 +316,29 @@ int mc_matmul_splitk(int dtype, int nc, int64_t M, int64_t N, int64_t K, const v
   }
   return hip_status(
       mcf::launch_matmul_splitk(dtype, nc, M, N, K, A, a_mc, B, b_mc, S, workspace, C, (hipStream_t)stream));
+}
+
+int64_t mc_matmul_exact_workspace(int dtype, int nc, int64_t M, int64_t N, int64_t K) {
+  int st = exact_check(dtype, nc, M, N, K, 1, 1, 0);
+  if (st != MCF_OK) return st;
+  if (M == 0 || N == 0) return 0;
+  return mcf::exact_workspace_bytes(M, N, K);
+}
+
+int mc_matmul_exact(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B,
+                    int b_mc, int b_trans, void *workspace, int64_t workspace_bytes, void *C, void *stream) {
+  int st = exact_check(dtype, nc, M, N, K, a_mc, b_mc, b_trans);
+  if (st != MCF_OK) return st;
+  if (M == 0 || N == 0) return MCF_OK;
+  if (!C || !workspace || (K > 0 && (!A || !B))) return MCF_E_NULL;
+  const int64_t wb = mcf::exact_workspace_bytes(M, N, K);
+  if (workspace_bytes < wb) return MCF_E_ARG;
+  const int64_t cb = nc * M * N * 2, ab = (a_mc ? nc : 1) * M * K * 2, bb = (b_mc ? nc : 1) * K * N * 2;
+  if (overlap(C, cb, A, ab) || overlap(C, cb, B, bb)) return MCF_E_ALIAS;
+  if (overlap(workspace, wb, A, ab) || overlap(workspace, wb, B, bb) || overlap(workspace, wb, C, cb))
+    return MCF_E_ALIAS;
+  return hip_status(
+      mcf::launch_matmul_exact(nc, M, N, K, A, a_mc, B, b_mc, b_trans, workspace, C, (hipStream_t)stream));
 }
 
 int mc_linear_fwd(int dtype, int nc, int64_t batch, int64_t in, int64_t out, const void *x, const void *W,
