@@ -215,7 +215,7 @@ int64_t mc_matmul_splitk_workspace(int dtype, int nc, int64_t M, int64_t N, int6
  * overlap and their sum is within half an ulp of c_{nc-1} (at most 2^-25 absolute
  * in the subnormal range) of P.  Not mc_matmul's bits: a different, more accurate
  * result.  The contraction runs on the int8 matrix cores: each entry is an exact
- * integer multiple of 2^-24, cut into 7-bit digits whose products are summed
+ * integer multiple of 2^-24, cut into 8-bit digits whose products are summed
  * exactly.
  * dtype: MCF_F16 only (else MCF_E_DTYPE).
  * Special values (input values ARE inspected here): an output whose row of A or
@@ -228,12 +228,14 @@ int64_t mc_matmul_splitk_workspace(int dtype, int nc, int64_t M, int64_t N, int6
  *   the caller, not overlapping A, B or C (else MCF_E_ALIAS); contents on entry do
  *   not matter; calls sharing a workspace must not overlap in time.  Too small:
  *   MCF_E_ARG; NULL: MCF_E_NULL.
- * Sizes: M, N, K <= 2^31 and (M + N) K <= 2^40 (else MCF_E_SHAPE). */
+ * Sizes: M, N <= 2^31, K <= 2^29, (M + N) K <= 2^40 and M N <= 2^38 (else
+ *   MCF_E_SHAPE). */
 int mc_matmul_exact(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B,
                     int b_mc, int b_trans, void *workspace, int64_t workspace_bytes, void *C, void *stream);
 
-/* Workspace bytes mc_matmul_exact needs (about 7 (M + N) K bytes of digit planes,
- * plus 16 M N bytes of partial sums when K > 65536), or a negative mcf_status for
+/* Workspace bytes mc_matmul_exact needs (about 6 (M + N) K bytes of digit planes,
+ * plus 16 M N ceil(K / 16384) bytes of partial sums when K > 16384), or a negative
+ * mcf_status for
  * sizes it would reject. */
 int64_t mc_matmul_exact_workspace(int dtype, int nc, int64_t M, int64_t N, int64_t K);
 

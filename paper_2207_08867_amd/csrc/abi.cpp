@@ -84,11 +84,12 @@ int exact_check(int dtype, int nc, int64_t M, int64_t N, int64_t K, int a_mc, in
   if (nc < 1 || nc > MAX_NC) return MCF_E_NC;
   if ((a_mc != 0 && a_mc != 1) || (b_mc != 0 && b_mc != 1) || (b_trans != 0 && b_trans != 1)) return MCF_E_ARG;
   if (M < 0 || N < 0 || K < 0) return MCF_E_SHAPE;
-  // digit planes of 7 (M + N) K bytes, grids of (M / 32) (N / 32) workgroups, K chunks
-  // of 65536 in the second grid dimension
-  if (M > ((int64_t)1 << 31) || N > ((int64_t)1 << 31) || K > ((int64_t)1 << 31)) return MCF_E_SHAPE;
-  if ((M + N) > 0 && K > ((int64_t)1 << 40) / (M + N + 128)) return MCF_E_SHAPE;
-  if (((M + 63) / 32) * ((N + 63) / 32) >= ((int64_t)1 << 31)) return MCF_E_SHAPE;
+  // digit planes of 6 (M + N) K bytes, grids of (M / 32) (N / 32) workgroups (rows
+  // padded to 128) and up to K / 16384 chunks in the second grid dimension
+  if (M > ((int64_t)1 << 31) || N > ((int64_t)1 << 31) || K > ((int64_t)1 << 29)) return MCF_E_SHAPE;
+  if ((M + N) > 0 && K > ((int64_t)1 << 40) / (M + N + 256)) return MCF_E_SHAPE;
+  if (((M + 127) / 32) * ((N + 127) / 32) >= ((int64_t)1 << 31)) return MCF_E_SHAPE;
+  if (M > 0 && N > ((int64_t)1 << 38) / M) return MCF_E_SHAPE;
   return MCF_OK;
 }
 

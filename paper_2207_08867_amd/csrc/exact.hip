@@ -12,22 +12,32 @@
 //
 // How.  Every binary16 value is an integer multiple of 2^-24, so an MC entry with at
 // most four components is an exact integer X = sum_c x_c 2^24 with |X| < 2^42.  X is
-// cut into XD = 7 balanced base-128 digits d_s in [-64, 63] (X = sum_s d_s 128^s),
-// stored as int8 planes D[s][row][k].  Then
-//     P_ij 2^48 = sum_{s,t} 128^(s+t) sum_k DA[s]_ik DB[t]_kj,
+// cut into XD = 6 balanced base-256 digits d_s in [-128, 127] (X = sum_s d_s 256^s),
+// stored as int8 planes.  Then
+//     P_ij 2^48 = sum_{s,t} 256^(s+t) sum_k DA[s]_ik DB[t]_kj,
 // and every inner sum is an int8 x int8 contraction with int32 accumulation: exact
-// as long as it cannot overflow.  At most 7 digit pairs share a shift class s + t and
-// each product is at most 4096 in magnitude, so 65536 reduction steps stay below
-// 7 * 4096 * 65536 < 2^31.  The classes are combined exactly in 128-bit integers
-// (|P 2^48| < K 2^84 < 2^127 for K <= 2^40) and rounded in integer arithmetic.
+// as long as it cannot overflow.  Each product is at most 2^14 in magnitude and at
+// most DM digit pairs share a shift class s + t, where DM is the number of digit
+// levels a code path handles, so a chunk of 2^31 / (DM 2^14) reduction steps
+// cannot overflow: 32768 for DM = 3, 16384 for DM = 4 and 6.  The classes are combined
+// exactly in 128-bit integers (|P 2^48| < K 2^84 < 2^127 for K <= 2^40) and rounded in
+// integer arithmetic.
+//
+// Digit layout ("fragment order").  Planes are cut into blocks of 16 rows x 64 k
+// (1 KiB); inside a block, byte (r, k) sits at ((k / 16) * 16 + r) * 16 + k % 16, so
+// that the 64 lanes of a wavefront read a block as one contiguous KiB with lane l
+// holding row l % 16, k = 16 (l / 16) .. 16 (l / 16) + 15 -- the operand layout of
+// v_mfma_i32_16x16x64_i8.  Block (s, kb, rb) of an operand with RB row blocks and KB
+// k blocks starts at ((s * KB + kb) * RB + rb) KiB.
 //
 // Kernels: xs_init clears the level statistics and the non-finite flags; xs_slice
-// writes the digit planes of both operands and records, per operand, the lowest and
-// highest digit level in use; xm_kernel<DM> runs the contraction over the levels in
-// use (two instantiations, DM = 4 for operands whose digits span at most four levels
-// and DM = 7 otherwise, both launched: each reads the statistics on the device and
-// the one that does not apply returns at once, so the host never waits); xm_finish
-// adds K-chunk partial sums when K exceeds one chunk.
+// writes the digit planes of both operands (one 16-byte chunk of every level per lane,
+// so that stores are contiguous) and records, per operand, the lowest and highest
+// digit level in use; xm_kernel runs the contraction over the levels in use, with one
+// code path each for operands whose digits span at most three levels (DM = 3), at most
+// four (DM = 4) and up to six (DM = 6), chosen on the device from the statistics so
+// that the host never waits; xm_finish adds K-chunk partial sums when K exceeds one
+// chunk.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -41,15 +51,21 @@ typedef int v4i __attribute__((ext_vector_type(4)));
 typedef __int128 i128;
 typedef unsigned __int128 u128;
 
-constexpr int XD = 7;                    // digits per entry
-constexpr int XPAD = 64;                 // row padding of the digit planes (a workgroup tile)
-constexpr int XKSTEP = 64;               // k per matrix-core instruction
-constexpr int64_t XKCHUNK = 65536;       // k per int32 accumulation (see the overflow bound above)
+constexpr int XD = 6;                    // digits per entry
+constexpr int XPAD = 128;                // row padding of the digit planes
+constexpr int XKSTEP = 64;               // k per matrix-core instruction (one k block)
 constexpr int XS_THREADS = 256;
 
-// statistics words: [0] A's highest level + 1, [1] B's, [2] XD - A's lowest level,
-// [3] XD - B's lowest level (all max-reduced from zero)
-constexpr int XSTAT_WORDS = 4;
+// k per int32 accumulation chunk of a code path handling DM levels
+__host__ __device__ constexpr int64_t x_chunk(int dm) { return dm <= 3 ? 32768 : 16384; }
+
+// Statistics, four kinds: [0] A's highest level + 1, [1] B's, [2] XD - A's lowest
+// level, [3] XD - B's lowest level, each max-reduced from zero.  Each kind is spread
+// over XSLOTS words 256 bytes apart (workgroup b updates slot b % XSLOTS), so that
+// concurrent updates do not all meet on one address; readers take the maximum over
+// the slots.  Word (kind, slot) is at index (kind * XSLOTS + slot) * 64.
+constexpr int XSLOTS = 64;
+constexpr int XSTAT_WORDS = 4 * XSLOTS * 64;
 
 // binary16 bits -> the exact integer value * 2^24 (finite inputs)
 __device__ __forceinline__ int64_t f16_units(uint32_t b) {
@@ -64,86 +80,138 @@ struct SliceOp {
   const uint16_t *src;   // planes of binary16
   int planes;            // nc for an MC operand, 1 for a plain one
   int kcontig;           // 1: k is the fast index of src; 0: rows are
+  int vec;               // 1: rows of src may be read 16 bytes at a time (kcontig, K % 8 == 0, aligned)
   int64_t plane, rs, ks; // element (row, k) of plane c at c*plane + row*rs + k*ks
   int64_t R, Rp;         // rows, rows padded to XPAD
-  int8_t *D;             // XD planes of Rp x Kp digits
+  int8_t *D;             // XD planes of Rp x Kp digits in fragment order
   uint8_t *bad;          // per-row non-finite flags
-  uint32_t *hi, *loinv;  // statistics words of this operand
-  int64_t threads;       // Rp * Kp / 16
+  uint32_t *stats;       // the statistics block
+  int64_t chunks;        // 16-byte chunks per level: Rp * Kp / 16
 };
+
+// Level statistics of a workgroup: wavefront maxima, then the workgroup maximum, then
+// an atomic only if it raises the stored word (a plain read first: every workgroup
+// would otherwise update the same two words, and same-address atomics serialise).
+// Every lane of the workgroup must call this.
+__device__ __forceinline__ void x_stats(uint32_t *stats, int kind_hi, int kind_lo, uint32_t top, uint32_t low) {
+  __shared__ uint32_t red[2][XS_THREADS / 64];
+  const uint32_t wtop = __ockl_wfred_max_u32(top);
+  const uint32_t wlow = __ockl_wfred_max_u32(XD - low);
+  const int wave = threadIdx.x / 64;
+  if (threadIdx.x % 64 == 0) {
+    red[0][wave] = wtop;
+    red[1][wave] = wlow;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t bt = 0, bl = 0;
+    for (int w = 0; w < XS_THREADS / 64; ++w) {
+      bt = max(bt, red[0][w]);
+      bl = max(bl, red[1][w]);
+    }
+    const int slot = (int)(blockIdx.x % XSLOTS) * 64;
+    uint32_t *hi = stats + (kind_hi * XSLOTS) * 64 + slot, *lo = stats + (kind_lo * XSLOTS) * 64 + slot;
+    if (bt > __atomic_load_n(hi, __ATOMIC_RELAXED)) atomicMax(hi, bt);
+    if (bl > __atomic_load_n(lo, __ATOMIC_RELAXED)) atomicMax(lo, bl);
+  }
+}
 
 __global__ void xs_init(uint32_t *stats, uint8_t *bad_a, int64_t na, uint8_t *bad_b, int64_t nb) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  if (t < XSTAT_WORDS) stats[t] = 0;
+  for (int64_t i = t; i < 4 * XSLOTS; i += stride) stats[i * 64] = 0;
   for (int64_t i = t; i < na; i += stride) bad_a[i] = 0;
   for (int64_t i = t; i < nb; i += stride) bad_b[i] = 0;
 }
 
-// One lane per (row, run of 16 consecutive k): forms the 16 exact integers, cuts them
-// into digits and stores 16 bytes per digit plane.  Entries beyond R or K are zero.
+// Balanced digits without per-digit arithmetic: with Y = X + 128 (1 + 256 + ... +
+// 256^5), which is non-negative for |X| < 2^47, byte s of Y is d_s + 128, so the int8
+// digit d_s is byte s of Y with its top bit flipped.
+constexpr uint64_t XBIAS = 0x808080808080ull;
+
+// Lane t writes 16-byte chunk t of every level plane.  In fragment order chunk t is
+// row block rb = (t / 64) % RB, k block kb = t / (64 RB), and inside the block lane
+// l = t % 64 holds row 16 rb + l % 16, k = 64 kb + 16 (l / 16) .. + 15.  Entries
+// beyond R or K are zero.
 __global__ __launch_bounds__(XS_THREADS) void xs_slice(SliceOp a, SliceOp b, int64_t K, int64_t Kp,
                                                        int64_t a_blocks) {
   const bool is_a = blockIdx.x < a_blocks;
   const SliceOp &o = is_a ? a : b;
   const int64_t t = (int64_t)(is_a ? blockIdx.x : blockIdx.x - a_blocks) * XS_THREADS + threadIdx.x;
-  const int64_t runs = Kp / 16;
-  uint32_t top = 0, low = XD;  // highest level + 1 and lowest non-zero level of this lane
-  if (t < o.threads) {
-    int64_t row, run;
-    if (o.kcontig) {
-      row = t / runs;
-      run = t - row * runs;
-    } else {
-      run = t / o.Rp;
-      row = t - run * o.Rp;
-    }
-    const int64_t k0 = run * 16;
-    uint32_t dig[XD][4];
+  uint32_t top = 0, low = XD;
+  if (t < o.chunks) {
+    const int64_t RB = o.Rp / 16;
+    const int64_t blk = t / 64;
+    const int l = (int)(t % 64);
+    const int64_t kb = blk / RB, rb = blk - kb * RB;
+    const int64_t row = rb * 16 + l % 16;
+    const int64_t k0 = kb * 64 + 16 * (l / 16);
+    int64_t X[16];
 #pragma unroll
-    for (int s = 0; s < XD; ++s)
-#pragma unroll
-      for (int w = 0; w < 4; ++w) dig[s][w] = 0;
+    for (int j = 0; j < 16; ++j) X[j] = 0;
     bool bad = false;
     if (row < o.R) {
-      const uint16_t *p = o.src + row * o.rs;
+      const uint16_t *p = o.src + row * o.rs + k0 * o.ks;
+      if (o.vec && k0 + 16 <= K) {
+        for (int c = 0; c < o.planes; ++c) {
+          const uint4 v0 = *(const uint4 *)(p + c * o.plane);
+          const uint4 v1 = *(const uint4 *)(p + c * o.plane + 8);
+          const uint32_t w[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const int64_t k = k0 + j;
-        int64_t X = 0;
-        if (k < K) {
-          for (int c = 0; c < o.planes; ++c) {
-            const uint32_t bits = p[c * o.plane + k * o.ks];
+          for (int j = 0; j < 16; ++j) {
+            const uint32_t bits = (w[j / 2] >> (16 * (j % 2))) & 0xFFFFu;
             if (f16_nonfinite(bits)) bad = true;
-            else X += f16_units(bits);
+            else X[j] += f16_units(bits);
           }
         }
+      } else {
+        for (int c = 0; c < o.planes; ++c) {
 #pragma unroll
-        for (int s = 0; s < XD; ++s) {
-          const int64_t d = ((X + 64) & 127) - 64;  // balanced digit in [-64, 63]
-          X = (X - d) >> 7;                          // exact: X - d is a multiple of 128
-          dig[s][j >> 2] |= ((uint32_t)d & 0xFFu) << (8 * (j & 3));
-          if (d != 0) {
-            top = max(top, (uint32_t)s + 1);
-            low = min(low, (uint32_t)s);
+          for (int j = 0; j < 16; ++j) {
+            if (k0 + j < K) {
+              const uint32_t bits = p[c * o.plane + j * o.ks];
+              if (f16_nonfinite(bits)) bad = true;
+              else X[j] += f16_units(bits);
+            }
           }
         }
       }
       if (bad) o.bad[row] = 1;
     }
-    const int64_t plane = o.Rp * Kp;
-    int8_t *dst = o.D + row * Kp + k0;
+    uint32_t lo[16], hi[16];
+    uint64_t any = 0;
 #pragma unroll
-    for (int s = 0; s < XD; ++s)
-      *(uint4 *)(dst + s * plane) = make_uint4(dig[s][0], dig[s][1], dig[s][2], dig[s][3]);
+    for (int j = 0; j < 16; ++j) {
+      const uint64_t Y = (uint64_t)X[j] + XBIAS;
+      const uint64_t D = Y ^ XBIAS;  // the digits as bytes; zero digits are zero bytes
+      any |= D;
+      lo[j] = (uint32_t)D;
+      hi[j] = (uint32_t)(D >> 32);
+      const int bl = D ? 64 - __builtin_clzll(D) : 0;
+      top = max(top, (uint32_t)((bl + 7) / 8));
+    }
+    if (any) low = (uint32_t)(__builtin_ctzll(any) / 8);
+    const int64_t level = o.chunks * 16;
+    int8_t *dst = o.D + t * 16;
+#pragma unroll
+    for (int s = 0; s < XD; ++s) {
+      uint32_t w[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        uint32_t v = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int j = 4 * q + i;
+          const uint32_t byte = s < 4 ? (lo[j] >> (8 * s)) & 0xFFu : (hi[j] >> (8 * (s - 4))) & 0xFFu;
+          v |= byte << (8 * i);
+        }
+        w[q] = v;
+      }
+      *(uint4 *)(dst + s * level) = make_uint4(w[0], w[1], w[2], w[3]);
+    }
   }
-  // every lane of the wavefront takes part in the reductions
-  const uint32_t wtop = __ockl_wfred_max_u32(top);
-  const uint32_t wlow = __ockl_wfred_max_u32(XD - low);
-  if (threadIdx.x % warpSize == 0) {
-    if (wtop) atomicMax(o.hi, wtop);
-    if (wlow) atomicMax(o.loinv, wlow);
-  }
+  // every lane of the workgroup takes part in the reductions
+  x_stats(o.stats, is_a ? 0 : 1, is_a ? 2 : 3, top, low);
 }
 
 // ---------------------------------------------------------------------------------
@@ -157,16 +225,20 @@ __device__ __forceinline__ int bitlen(u128 a) {
 
 // Rounds rem * 2^-48 to the nearest binary16 (ties to even, gradual underflow),
 // subtracts the rounded value from rem and returns its bits; on overflow returns the
-// infinity of rem's sign and sets *ovf.
-__device__ __forceinline__ uint32_t take_f16(i128 &rem, bool &ovf) {
+// infinity of rem's sign and sets ovf.  W is the integer type of rem (int64_t when
+// |rem| < 2^62, which cannot overflow binary16, else i128).
+template <typename W, typename UW>
+__device__ __forceinline__ uint32_t take_f16(W &rem, bool &ovf) {
   if (rem == 0) return 0;
   const bool neg = rem < 0;
-  const u128 a = neg ? (u128)0 - (u128)rem : (u128)rem;
-  const int e = bitlen(a) - 1;
+  const UW a = neg ? (UW)0 - (UW)rem : (UW)rem;
+  int e;
+  if constexpr (sizeof(W) == 8) e = 63 - __builtin_clzll((uint64_t)a);
+  else e = bitlen(a) - 1;
   const int qe = e - 10 > 24 ? e - 10 : 24;  // quantum 2^(qe-48): 11 significant bits, 2^-24 floor
-  u128 n = a >> qe;
-  const u128 r = a - (n << qe);
-  const u128 half = (u128)1 << (qe - 1);
+  UW n = a >> qe;
+  const UW r = a - (n << qe);
+  const UW half = (UW)1 << (qe - 1);
   if (r > half || (r == half && (n & 1))) n += 1;
   // binary16 bits rise by 1024 per binade and by 1 per quantum, continuously through
   // the subnormals: bits = (qe - 24) * 1024 + n
@@ -176,21 +248,28 @@ __device__ __forceinline__ uint32_t take_f16(i128 &rem, bool &ovf) {
     ovf = true;
     return sign | 0x7C00u;
   }
-  const i128 v = (i128)(n << qe);
+  const W v = (W)(n << qe);
   rem = neg ? rem + v : rem - v;
   return sign | (uint32_t)enc;
 }
 
+// Splits V * 2^-48 into nc binary16 components by successive rounding and stores them
+// (NaN in every component when nan is set).
 __device__ __forceinline__ void store_split(i128 V, int nc, bool nan, uint16_t *C, int64_t plane, int64_t idx) {
+  uint32_t bits[4] = {0, 0, 0, 0};
   if (nan) {
-    for (int c = 0; c < nc; ++c) C[c * plane + idx] = 0x7E00;
-    return;
+    for (int c = 0; c < 4; ++c) bits[c] = 0x7E00;
+  } else {
+    const u128 a = V < 0 ? (u128)0 - (u128)V : (u128)V;
+    bool ovf = false;
+    if ((a >> 62) == 0) {  // the common case: 64-bit arithmetic
+      int64_t v = (int64_t)V;
+      for (int c = 0; c < nc; ++c) bits[c] = take_f16<int64_t, uint64_t>(v, ovf);
+    } else {
+      for (int c = 0; c < nc; ++c) bits[c] = ovf ? 0u : take_f16<i128, u128>(V, ovf);
+    }
   }
-  bool ovf = false;
-  for (int c = 0; c < nc; ++c) {
-    const uint32_t bits = ovf ? 0u : take_f16(V, ovf);
-    C[c * plane + idx] = (uint16_t)bits;
-  }
+  for (int c = 0; c < nc; ++c) C[c * plane + idx] = (uint16_t)bits[c];
 }
 
 // ---------------------------------------------------------------------------------
@@ -204,104 +283,189 @@ struct XmArgs {
   int64_t M, N, Kp, Mp, Np;
   int nc;
   uint16_t *C;       // [nc][M][N]
-  i128 *partial;     // [S][M][N] when S > 1
-  int64_t S;         // K chunks (gridDim.y)
+  i128 *partial;     // [S][M][N] when the code path that runs needs S > 1 chunks
   int64_t tiles_n;   // workgroup tiles along N
 };
 
-// Workgroup of 4 wavefronts in a 2 x 2 arrangement; each wavefront computes WT x WT
-// tiles of 16 x 16 outputs with v_mfma_i32_16x16x64_i8.  Operand layout of that
-// instruction (64 lanes): lane l supplies row (l % 16) of its 16 x 64 operand slice,
-// bytes k = 16 (l / 16) .. 16 (l / 16) + 15; the result element i of lane l is row
-// 4 (l / 16) + i, column l % 16 of the 16 x 16 tile.
-template <int DM, int WT>
-__global__ __launch_bounds__(256) void xm_kernel(XmArgs g) {
+struct XLevels {
+  int loA, loB, nA, nB;
+  bool small;  // both operands within three levels: the DM = 3 code path runs
+};
+
+// The first wavefront reads slot l of each kind in lane l and reduces; the result
+// reaches the other wavefronts through LDS.  Every lane of the workgroup must call
+// this (it holds a barrier).
+__device__ __forceinline__ XLevels x_levels(const uint32_t *stats) {
+  __shared__ uint32_t sw[4];
+  XLevels v;
+  if (threadIdx.x < 64) {
+    const int l = threadIdx.x;
+#pragma unroll
+    for (int kind = 0; kind < 4; ++kind) {
+      const uint32_t m = __ockl_wfred_max_u32(stats[(kind * XSLOTS + l) * 64]);
+      if (l == 0) sw[kind] = m;
+    }
+  }
+  __syncthreads();
+  uint32_t w[4];
+#pragma unroll
+  for (int kind = 0; kind < 4; ++kind) w[kind] = sw[kind];
+  const int hiA = (int)w[0], hiB = (int)w[1];
+  v.loA = XD - (int)w[2];
+  v.loB = XD - (int)w[3];
+  v.nA = hiA > v.loA ? hiA - v.loA : 0;
+  v.nB = hiB > v.loB ? hiB - v.loB : 0;
+  v.small = v.nA <= 3 && v.nB <= 3;
+  return v;
+}
+
+// Branch-free rounding for |rem| < 2^62 (which cannot overflow binary16): as
+// take_f16 with the sign folded in by two's-complement identities.
+__device__ __forceinline__ uint32_t take_f16_fast(int64_t &rem) {
+  const uint64_t sgn = (uint64_t)(rem >> 63);      // 0 or all ones
+  const uint64_t a = ((uint64_t)rem ^ sgn) - sgn;  // |rem|
+  const int e = 63 - __builtin_clzll(a | 1);
+  const int qe = e - 10 > 24 ? e - 10 : 24;
+  const uint64_t n0 = a >> qe;
+  const uint64_t r = a - (n0 << qe);
+  const uint64_t half = 1ull << (qe - 1);
+  const uint64_t n = n0 + (uint64_t)((r > half) | ((r == half) & (bool)(n0 & 1)));
+  const uint64_t v = n << qe;
+  rem -= (int64_t)((v ^ sgn) - sgn);  // rem - sign(rem) v
+  return ((uint32_t)sgn & 0x8000u) | (uint32_t)((qe - 24) * 1024 + (int)n);
+}
+
+// One wavefront's WTR x WTC tiles of 16 x 16 outputs with v_mfma_i32_16x16x64_i8
+// (result element i of lane l is row 4 (l / 16) + i, column l % 16 of its tile), one
+// int32 accumulator per tile and shift class, over k blocks [kb0, kb1).  The operand
+// fragments of the next k block are loaded while the current one is multiplied.
+template <int DM, int WTR, int WTC>
+__device__ __forceinline__ void xm_tile(const XmArgs &g, const XLevels &lv, int64_t row0, int64_t col0,
+                                        int64_t chunk, int64_t kb0, int64_t kb1, int64_t S) {
   constexpr int NCLS = 2 * DM - 1;
-  const uint32_t hiA = g.stats[0], hiB = g.stats[1];
-  const int loA = XD - (int)g.stats[2], loB = XD - (int)g.stats[3];
-  const int nA = (int)hiA > loA ? (int)hiA - loA : 0;
-  const int nB = (int)hiB > loB ? (int)hiB - loB : 0;
-  const bool small = nA <= 4 && nB <= 4;
-  if ((DM == 4) != small) return;  // the other instantiation handles these operands
+  const int lane = threadIdx.x % 64;
+  const int64_t KB = g.Kp / 64;
 
-  const int lane = threadIdx.x % 64, wave = threadIdx.x / 64;
-  const int64_t tile = blockIdx.x;
-  const int64_t tm = tile / g.tiles_n, tn = tile - tm * g.tiles_n;
-  const int64_t row0 = tm * (32 * WT) + (wave / 2) * (16 * WT);
-  const int64_t col0 = tn * (32 * WT) + (wave % 2) * (16 * WT);
-  const int64_t chunk = blockIdx.y;
-  const int64_t kbeg = chunk * XKCHUNK;
-  const int64_t kend = min(g.Kp, kbeg + XKCHUNK);
-
-  v4i acc[NCLS][WT][WT];
+  v4i acc[NCLS][WTR][WTC];
 #pragma unroll
   for (int q = 0; q < NCLS; ++q)
 #pragma unroll
-    for (int r = 0; r < WT; ++r)
+    for (int r = 0; r < WTR; ++r)
 #pragma unroll
-      for (int c = 0; c < WT; ++c) acc[q][r][c] = v4i{0, 0, 0, 0};
+      for (int c = 0; c < WTC; ++c) acc[q][r][c] = v4i{0, 0, 0, 0};
 
-  const int64_t pa = g.Mp * g.Kp, pb = g.Np * g.Kp;
-  const int8_t *baseA = g.DA + (int64_t)loA * pa + (row0 + lane % 16) * g.Kp + 16 * (lane / 16);
-  const int8_t *baseB = g.DB + (int64_t)loB * pb + (col0 + lane % 16) * g.Kp + 16 * (lane / 16);
+  // fragment (level s, k block kb, row block rb) at ((s KB + kb) RB + rb) KiB
+  const int64_t RBa = g.Mp / 16, RBb = g.Np / 16;
+  const int8_t *pa = g.DA + (((int64_t)lv.loA * KB) * RBa + row0 / 16) * 1024 + lane * 16;
+  const int8_t *pb = g.DB + (((int64_t)lv.loB * KB) * RBb + col0 / 16) * 1024 + lane * 16;
+  const int64_t la = KB * RBa * 1024, lb = KB * RBb * 1024;  // level strides
+  const int64_t ka = RBa * 1024, kbs = RBb * 1024;           // k-block strides
 
-  for (int64_t k0 = kbeg; k0 < kend; k0 += XKSTEP) {
-    v4i fa[DM][WT], fb[DM][WT];
+  v4i fa[DM][WTR], fb[DM][WTC];
+  auto load = [&](int64_t kb, v4i (&xa)[DM][WTR], v4i (&xb)[DM][WTC]) {
 #pragma unroll
     for (int s = 0; s < DM; ++s) {
-      if (s < nA) {
+      if (s < lv.nA) {
 #pragma unroll
-        for (int r = 0; r < WT; ++r) fa[s][r] = *(const v4i *)(baseA + s * pa + (int64_t)(16 * r) * g.Kp + k0);
+        for (int r = 0; r < WTR; ++r) xa[s][r] = *(const v4i *)(pa + s * la + kb * ka + r * 1024);
       }
-      if (s < nB) {
+      if (s < lv.nB) {
 #pragma unroll
-        for (int c = 0; c < WT; ++c) fb[s][c] = *(const v4i *)(baseB + s * pb + (int64_t)(16 * c) * g.Kp + k0);
+        for (int c = 0; c < WTC; ++c) xb[s][c] = *(const v4i *)(pb + s * lb + kb * kbs + c * 1024);
       }
     }
+  };
+  if (kb0 < kb1) load(kb0, fa, fb);
+  for (int64_t kb = kb0; kb < kb1; ++kb) {
+    v4i na[DM][WTR], nb[DM][WTC];
+    if (kb + 1 < kb1) load(kb + 1, na, nb);
 #pragma unroll
     for (int s = 0; s < DM; ++s) {
-      if (s < nA) {
+      if (s < lv.nA) {
 #pragma unroll
         for (int t = 0; t < DM; ++t) {
-          if (t < nB) {
+          if (t < lv.nB) {
 #pragma unroll
-            for (int r = 0; r < WT; ++r)
+            for (int r = 0; r < WTR; ++r)
 #pragma unroll
-              for (int c = 0; c < WT; ++c)
+              for (int c = 0; c < WTC; ++c)
                 acc[s + t][r][c] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[s][r], fb[t][c], acc[s + t][r][c], 0, 0, 0);
           }
         }
       }
     }
+#pragma unroll
+    for (int s = 0; s < DM; ++s) {
+#pragma unroll
+      for (int r = 0; r < WTR; ++r) fa[s][r] = na[s][r];
+#pragma unroll
+      for (int c = 0; c < WTC; ++c) fb[s][c] = nb[s][c];
+    }
   }
 
-  // combine the shift classes exactly: V = sum_q acc[q] 128^(q + loA + loB)
-  const int shift0 = 7 * (loA + loB);
+  // V = sum_q acc[q] 256^q 2^shift0 exactly.  First a conservative test that every
+  // value of the wavefront stays below 2^62 in magnitude: each term is below
+  // 2^(bitlen|acc[q]| + 8 q + shift0) and there are at most 11 terms.  Then, when it
+  // holds, V is summed in wrapping 64-bit arithmetic, which is exact because the true
+  // sum fits; otherwise in 128-bit integers.
+  const int shift0 = 8 * (lv.loA + lv.loB);
+  bool fits = true;
 #pragma unroll
-  for (int r = 0; r < WT; ++r) {
+  for (int r = 0; r < WTR; ++r)
 #pragma unroll
-    for (int c = 0; c < WT; ++c) {
+    for (int c = 0; c < WTC; ++c)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        int hb = 0;
+#pragma unroll
+        for (int q = 0; q < NCLS; ++q) {
+          const int32_t x = acc[q][r][c][i];
+          const uint32_t ax = (uint32_t)(x < 0 ? -(int64_t)x : (int64_t)x);
+          const int bl = ax ? 32 - __builtin_clz(ax) : 0;
+          hb = max(hb, bl ? bl + 8 * q : 0);
+        }
+        fits = fits && (hb == 0 || hb + 4 + shift0 <= 62);
+      }
+  const bool fast = __all(fits);  // uniform across the wavefront
+  const int64_t MN = g.M * g.N;
+#pragma unroll
+  for (int r = 0; r < WTR; ++r) {
+#pragma unroll
+    for (int c = 0; c < WTC; ++c) {
       const int64_t col = col0 + 16 * c + lane % 16;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int64_t row = row0 + 16 * r + 4 * (lane / 16) + i;
-        // five consecutive classes fit one int64 (|acc| < 2^31, relative shifts up to
-        // 28 bits); the groups are then combined 35 bits apart in 128 bits
-        constexpr int NG = (NCLS + 4) / 5;
-        int64_t part[NG];
-#pragma unroll
-        for (int q = 0; q < NG; ++q) part[q] = 0;
-#pragma unroll
-        for (int q = 0; q < NCLS; ++q) part[q / 5] += (int64_t)acc[q][r][c][i] * ((int64_t)1 << (7 * (q % 5)));
-        u128 Vu = 0;
-#pragma unroll
-        for (int q = 0; q < NG; ++q) Vu += (u128)(i128)part[q] << (35 * q);
-        const i128 V = (i128)(Vu << shift0);
         if (row < g.M && col < g.N) {
-          if (g.S == 1) {
-            store_split(V, g.nc, g.bad_a[row] | g.bad_b[col], g.C, g.M * g.N, row * g.N + col);
+          const int64_t idx = row * g.N + col;
+          if (fast && S == 1) {
+            uint64_t vu = 0;
+#pragma unroll
+            for (int q = 0; q < NCLS; ++q) {
+              const int sh = 8 * q + shift0;
+              vu += sh < 64 ? (uint64_t)(int64_t)acc[q][r][c][i] << sh : 0;
+            }
+            int64_t v = (int64_t)vu;
+            if (g.bad_a[row] | g.bad_b[col]) {
+              for (int k = 0; k < g.nc; ++k) g.C[k * MN + idx] = 0x7E00;
+            } else {
+              for (int k = 0; k < g.nc; ++k) g.C[k * MN + idx] = (uint16_t)take_f16_fast(v);
+            }
           } else {
-            g.partial[(chunk * g.M + row) * g.N + col] = V;
+            // four consecutive classes fit one int64 (|acc| < 2^31, relative shifts up
+            // to 24 bits); the groups are combined 32 bits apart in 128 bits
+            constexpr int NG = (NCLS + 3) / 4;
+            int64_t part[NG];
+#pragma unroll
+            for (int q = 0; q < NG; ++q) part[q] = 0;
+#pragma unroll
+            for (int q = 0; q < NCLS; ++q) part[q / 4] += (int64_t)acc[q][r][c][i] * ((int64_t)1 << (8 * (q % 4)));
+            u128 Vu = 0;
+#pragma unroll
+            for (int q = 0; q < NG; ++q) Vu += (u128)(i128)part[q] << (32 * q);
+            const i128 V = (i128)(Vu << shift0);
+            if (S > 1) g.partial[chunk * MN + idx] = V;
+            else store_split(V, g.nc, g.bad_a[row] | g.bad_b[col], g.C, MN, idx);
           }
         }
       }
@@ -309,12 +473,48 @@ __global__ __launch_bounds__(256) void xm_kernel(XmArgs g) {
   }
 }
 
+// One workgroup of 4 wavefronts per 64 x 64 tile of C; blockIdx.y is the K chunk.
+// Operands within three digit levels: each wavefront takes a 32 x 32 quarter (2 x 2
+// tiles, five shift classes).  Within four: two passes over 64 x 32 halves, each
+// wavefront taking 32 x 16 (2 x 1 tiles, seven classes).  Otherwise: four passes over
+// the 32 x 32 quarters, each wavefront taking one 16 x 16 tile (eleven classes).
+__global__ __attribute__((amdgpu_flat_work_group_size(1, 256), amdgpu_waves_per_eu(2))) void xm_kernel(XmArgs g) {
+  const XLevels lv = x_levels(g.stats);
+  const int wave = threadIdx.x / 64;
+  const int64_t tile = blockIdx.x;
+  const int64_t tm = tile / g.tiles_n, tn = tile - tm * g.tiles_n;
+  const int64_t KB = g.Kp / 64;
+  const int64_t chunk = blockIdx.y;
+  const int dm = lv.small ? 3 : (lv.nA <= 4 && lv.nB <= 4 ? 4 : 6);
+  const int64_t CKB = x_chunk(dm) / 64;
+  const int64_t kb0 = chunk * CKB;
+  if (kb0 >= KB && KB > 0) return;  // the grid holds the chunks of the smallest chunk size
+  const int64_t kb1 = min(KB, kb0 + CKB);
+  const int64_t S = KB == 0 ? 1 : (KB + CKB - 1) / CKB;
+  if (dm == 3) {
+    xm_tile<3, 2, 2>(g, lv, tm * 64 + (wave / 2) * 32, tn * 64 + (wave % 2) * 32, chunk, kb0, kb1, S);
+  } else if (dm == 4) {
+    for (int sub = 0; sub < 2; ++sub)
+      xm_tile<4, 2, 1>(g, lv, tm * 64 + (wave / 2) * 32, tn * 64 + sub * 32 + (wave % 2) * 16, chunk, kb0, kb1, S);
+  } else {
+    for (int sub = 0; sub < 4; ++sub)
+      xm_tile<6, 1, 1>(g, lv, tm * 64 + (sub / 2) * 32 + (wave / 2) * 16, tn * 64 + (sub % 2) * 32 + (wave % 2) * 16,
+                       chunk, kb0, kb1, S);
+  }
+}
+
 __global__ void xm_finish(XmArgs g) {
+  const XLevels lv = x_levels(g.stats);  // every lane, before any returns
+  const int dm = lv.small ? 3 : (lv.nA <= 4 && lv.nB <= 4 ? 4 : 6);
+  const int64_t chunk_kb = x_chunk(dm) / 64;
+  const int64_t KB = g.Kp / 64;
+  const int64_t S = (KB + chunk_kb - 1) / chunk_kb;
+  if (S <= 1) return;  // the product kernel wrote C itself
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t MN = g.M * g.N;
   if (t >= MN) return;
   i128 V = 0;
-  for (int64_t s = 0; s < g.S; ++s) V += g.partial[s * MN + t];
+  for (int64_t s = 0; s < S; ++s) V += g.partial[s * MN + t];
   const int64_t row = t / g.N, col = t - row * g.N;
   store_split(V, g.nc, g.bad_a[row] | g.bad_b[col], g.C, MN, t);
 }
@@ -322,7 +522,7 @@ __global__ void xm_finish(XmArgs g) {
 int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
 struct XLayout {
-  int64_t Mp, Np, Kp, S;
+  int64_t Mp, Np, Kp, Smax;
   int64_t off_stats, off_bad_a, off_bad_b, off_da, off_db, off_part, total;
 };
 
@@ -331,10 +531,10 @@ XLayout x_layout(int64_t M, int64_t N, int64_t K) {
   L.Mp = round_up(M, XPAD);
   L.Np = round_up(N, XPAD);
   L.Kp = round_up(K, XKSTEP);
-  L.S = L.Kp == 0 ? 1 : (L.Kp + XKCHUNK - 1) / XKCHUNK;
+  L.Smax = L.Kp == 0 ? 1 : (L.Kp + x_chunk(6) - 1) / x_chunk(6);
   int64_t o = 0;
   L.off_stats = o;
-  o += 256;
+  o += XSTAT_WORDS * 4;
   L.off_bad_a = o;
   o += round_up(M, 256);
   L.off_bad_b = o;
@@ -344,7 +544,7 @@ XLayout x_layout(int64_t M, int64_t N, int64_t K) {
   L.off_db = o;
   o += round_up(XD * L.Np * L.Kp, 256);
   L.off_part = o;
-  if (L.S > 1) o += L.S * M * N * (int64_t)sizeof(i128);
+  if (L.Smax > 1) o += L.Smax * M * N * (int64_t)sizeof(i128);
   L.total = o;
   return L;
 }
@@ -363,7 +563,8 @@ hipError_t launch_matmul_exact(int nc, int64_t M, int64_t N, int64_t K, const vo
 
   {
     const int64_t n = M > N ? M : N;
-    const int blocks = (int)((n + 255) / 256 < 1024 ? (n + 255) / 256 + 1 : 1024);
+    const int64_t nb = (n > 4 * XSLOTS ? n : 4 * XSLOTS);
+    const int blocks = (int)((nb + 255) / 256 < 1024 ? (nb + 255) / 256 : 1024);
     hipLaunchKernelGGL(xs_init, dim3(blocks), dim3(256), 0, stream, stats, bad_a, M, bad_b, N);
   }
   if (L.Kp > 0) {
@@ -371,6 +572,7 @@ hipError_t launch_matmul_exact(int nc, int64_t M, int64_t N, int64_t K, const vo
     a.src = (const uint16_t *)A;
     a.planes = a_mc ? nc : 1;
     a.kcontig = 1;
+    a.vec = (K % 8 == 0) && ((uintptr_t)A % 16 == 0);
     a.plane = M * K;
     a.rs = K;
     a.ks = 1;
@@ -378,12 +580,12 @@ hipError_t launch_matmul_exact(int nc, int64_t M, int64_t N, int64_t K, const vo
     a.Rp = L.Mp;
     a.D = DA;
     a.bad = bad_a;
-    a.hi = stats + 0;
-    a.loinv = stats + 2;
-    a.threads = L.Mp * L.Kp / 16;
+    a.stats = stats;
+    a.chunks = L.Mp * L.Kp / 16;
     b.src = (const uint16_t *)B;
     b.planes = b_mc ? nc : 1;
     b.kcontig = b_trans ? 1 : 0;
+    b.vec = b_trans && (K % 8 == 0) && ((uintptr_t)B % 16 == 0);
     b.plane = K * N;
     b.rs = b_trans ? K : 1;
     b.ks = b_trans ? 1 : N;
@@ -391,11 +593,10 @@ hipError_t launch_matmul_exact(int nc, int64_t M, int64_t N, int64_t K, const vo
     b.Rp = L.Np;
     b.D = DB;
     b.bad = bad_b;
-    b.hi = stats + 1;
-    b.loinv = stats + 3;
-    b.threads = L.Np * L.Kp / 16;
-    const int64_t ab = (a.threads + XS_THREADS - 1) / XS_THREADS;
-    const int64_t bb = (b.threads + XS_THREADS - 1) / XS_THREADS;
+    b.stats = stats;
+    b.chunks = L.Np * L.Kp / 16;
+    const int64_t ab = (a.chunks + XS_THREADS - 1) / XS_THREADS;
+    const int64_t bb = (b.chunks + XS_THREADS - 1) / XS_THREADS;
     hipLaunchKernelGGL(xs_slice, dim3((unsigned)(ab + bb)), dim3(XS_THREADS), 0, stream, a, b, K, L.Kp, ab);
   }
   XmArgs g;
@@ -412,19 +613,12 @@ hipError_t launch_matmul_exact(int nc, int64_t M, int64_t N, int64_t K, const vo
   g.nc = nc;
   g.C = (uint16_t *)C;
   g.partial = (i128 *)(w + L.off_part);
-  g.S = L.S;
-  // DM = 4: 2 x 2 tiles per wavefront (64 x 64 per workgroup); DM = 7: 1 x 1 (32 x 32)
   {
     g.tiles_n = L.Np / 64;
     const int64_t tiles = (L.Mp / 64) * g.tiles_n;
-    hipLaunchKernelGGL((xm_kernel<4, 2>), dim3((unsigned)tiles, (unsigned)L.S), dim3(256), 0, stream, g);
+    hipLaunchKernelGGL(xm_kernel, dim3((unsigned)tiles, (unsigned)L.Smax), dim3(256), 0, stream, g);
   }
-  {
-    g.tiles_n = L.Np / 32;
-    const int64_t tiles = (L.Mp / 32) * g.tiles_n;
-    hipLaunchKernelGGL((xm_kernel<7, 1>), dim3((unsigned)tiles, (unsigned)L.S), dim3(256), 0, stream, g);
-  }
-  if (L.S > 1) {
+  if (L.Smax > 1) {
     const int64_t n = M * N;
     hipLaunchKernelGGL(xm_finish, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, g);
   }
