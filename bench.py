@@ -13,7 +13,9 @@ Also reported on the same line (not part of `value`):
   * the maximum error against the exact product on sampled outputs;
   * the pruned MC x MC product (mc_matmul_pruned) on the headline operands;
   * the other workloads (64^3 binary32 nc=2; 1024^3 binary16 nc=2 and 3; the
-    4096x1024x1024 binary16 nc=3 MC-Linear over 100 layers; the 2^26-element binary16
+    4096x1024x1024 binary16 nc=3 MC-Linear over 100 layers; the exact binary16
+    product on the int8 matrix cores at 1024^3 and the MC-Linear layer shape; the
+    2^26-element binary16
     nc=3 elementwise operations with their HBM bandwidth; the K-split Dot and MV; the
     paper's BMM-MCN and AddMM-MCN sizes);
   * cpu_baseline: the CPU oracle timed on a sample of the headline workload.
@@ -324,6 +326,60 @@ def bench_linear(torch, mcf, inputs, layers=100):
             "valu_frac": round(algo_ops_per_mac(nc, False) * macs / (kms * 1e-3) / VALU_PEAK, 3)}
 
 
+MFMA_I8_PEAK = 5.0e15  # dense int8 matrix-core operations / s
+
+
+def digit_levels(X16):
+    """Balanced base-256 digit levels in use by binary16 MC entries (planes first):
+    (lowest, highest + 1) over the whole operand.  Measurement support only: the
+    number of int8 digit-pair contractions the exact product performs."""
+    X = np.zeros(X16.shape[1:], dtype=np.int64)
+    for c in range(X16.shape[0]):
+        X += np.round(X16[c].astype(np.float64) * 2.0 ** 24).astype(np.int64)
+    D = (X + 0x808080808080) ^ 0x808080808080  # digit bytes (zero byte = zero digit)
+    used = [bool(((D >> (8 * s)) & 0xFF).any()) for s in range(6)]
+    lv = [s for s in range(6) if used[s]]
+    return (lv[0], lv[-1] + 1) if lv else (0, 0)
+
+
+def bench_exact(torch, mcf, oracle, inputs, steps=20):
+    """The exact binary16 product (int8 matrix cores) on the 1024^3 MC x MC operands of
+    the binary16 MM-MCN lines and on one MC-Linear layer product x W^T."""
+    out = {}
+    cases = []
+    for nc in (2, 3):
+        A, B = inputs.matmul_normal(1024, 1024, 1024, nc, np.float16, seed=0)
+        cases.append((f"matmul_exact_1024_f16_nc{nc}", A, B, nc, True, False))
+    x, W, _ = next(inputs.linear_inputs(4096, 1024, 1024, 3, np.float16, seed=0))
+    cases.append(("linear_exact_4096x1024x1024_f16_nc3", x[None], W, 3, False, True))
+    for name, A, B, nc, a_mc, b_trans in cases:
+        tA, tB = torch.from_numpy(np.ascontiguousarray(A)).cuda(), torch.from_numpy(B).cuda()
+        M, K = A.shape[1:]
+        N = B.shape[1] if b_trans else B.shape[2]
+        ws = torch.empty(mcf.mc_matmul_exact_workspace(nc, M, N, K), dtype=torch.uint8, device="cuda")
+        C = torch.empty((nc, M, N), dtype=torch.float16, device="cuda")
+        run = lambda: mcf.mc_matmul_exact(tA if a_mc else tA[0], tB, nc=nc, a_mc=a_mc, b_trans=b_trans, out=C,
+                                          workspace=ws)
+        for _ in range(3):
+            run()
+        torch.cuda.synchronize()
+        tm = Timer(torch)
+        for _ in range(steps):
+            tm.run(run)
+        us = float(np.median(tm.ms())) * 1e3
+        Bm = np.ascontiguousarray(np.swapaxes(B, 1, 2)) if b_trans else B
+        la, lb = digit_levels(A), digit_levels(Bm)
+        pairs = (la[1] - la[0]) * (lb[1] - lb[0])
+        ops = 2.0 * M * N * K * pairs
+        out[name] = {"us": round(us, 1), "MC-GFLOP/s": round(2.0 * M * N * K / (us * 1e-6) / 1e9, 1),
+                     "digit_pairs": pairs, "int8_ops": ops,
+                     "mfma_int8_frac_whole_call": round(ops / (us * 1e-6) / MFMA_I8_PEAK, 4),
+                     "error": exact_error(oracle, A, Bm, C.cpu().numpy(), nc, K, np.float16)}
+        log(f"  {name}: {us:.1f} us ({pairs} digit pairs)")
+        del tA, tB, ws, C
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -428,6 +484,8 @@ def main():
             log(f"  1024^3 f16 nc={nc3}: {k3:.2f} ms")
         log("MC-Linear")
         extra["linear_4096x1024x1024_f16_nc3"] = bench_linear(torch, mcf, inputs)
+        log("exact binary16 products (int8 matrix cores)")
+        extra["exact"] = bench_exact(torch, mcf, oracle, inputs)
         log("elementwise")
         extra["elementwise"] = bench_elementwise(torch, mcf, inputs)
         log("K-split products")

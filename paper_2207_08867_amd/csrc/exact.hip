@@ -31,8 +31,8 @@
 // k blocks starts at ((s * KB + kb) * RB + rb) KiB.
 //
 // Kernels: xs_init clears the level statistics and the non-finite flags; xs_slice
-// writes the digit planes of both operands (one 16-byte chunk of every level per lane,
-// so that stores are contiguous) and records, per operand, the lowest and highest
+// writes the digit planes of both operands (four bytes of every level per lane, so
+// that stores are contiguous) and records, per operand, the lowest and highest
 // digit level in use; xm_kernel runs the contraction over the levels in use, with one
 // code path each for operands whose digits span at most three levels (DM = 3), at most
 // four (DM = 4) and up to six (DM = 6), chosen on the device from the statistics so
@@ -65,7 +65,9 @@ __host__ __device__ constexpr int64_t x_chunk(int dm) { return dm <= 3 ? 32768 :
 // concurrent updates do not all meet on one address; readers take the maximum over
 // the slots.  Word (kind, slot) is at index (kind * XSLOTS + slot) * 64.
 constexpr int XSLOTS = 64;
-constexpr int XSTAT_WORDS = 4 * XSLOTS * 64;
+// After the slots, one word set to 1 when either operand holds a non-finite component.
+constexpr int XBADW = 4 * XSLOTS * 64;
+constexpr int XSTAT_WORDS = XBADW + 64;
 
 // binary16 bits -> the exact integer value * 2^24 (finite inputs)
 __device__ __forceinline__ int64_t f16_units(uint32_t b) {
@@ -80,7 +82,7 @@ struct SliceOp {
   const uint16_t *src;   // planes of binary16
   int planes;            // nc for an MC operand, 1 for a plain one
   int kcontig;           // 1: k is the fast index of src; 0: rows are
-  int vec;               // 1: rows of src may be read 16 bytes at a time (kcontig, K % 8 == 0, aligned)
+  int vec;               // 1: rows of src may be read 8 bytes at a time (kcontig, K % 4 == 0, aligned)
   int64_t plane, rs, ks; // element (row, k) of plane c at c*plane + row*rs + k*ks
   int64_t R, Rp;         // rows, rows padded to XPAD
   int8_t *D;             // XD planes of Rp x Kp digits in fragment order
@@ -120,6 +122,7 @@ __global__ void xs_init(uint32_t *stats, uint8_t *bad_a, int64_t na, uint8_t *ba
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i = t; i < 4 * XSLOTS; i += stride) stats[i * 64] = 0;
+  if (t == 0) stats[XBADW] = 0;
   for (int64_t i = t; i < na; i += stride) bad_a[i] = 0;
   for (int64_t i = t; i < nb; i += stride) bad_b[i] = 0;
 }
@@ -129,36 +132,35 @@ __global__ void xs_init(uint32_t *stats, uint8_t *bad_a, int64_t na, uint8_t *ba
 // digit d_s is byte s of Y with its top bit flipped.
 constexpr uint64_t XBIAS = 0x808080808080ull;
 
-// Lane t writes 16-byte chunk t of every level plane.  In fragment order chunk t is
-// row block rb = (t / 64) % RB, k block kb = t / (64 RB), and inside the block lane
-// l = t % 64 holds row 16 rb + l % 16, k = 64 kb + 16 (l / 16) .. + 15.  Entries
-// beyond R or K are zero.
+// Lane t writes bytes 4 (t % 4) .. 4 (t % 4) + 3 of 16-byte chunk t / 4 of every level
+// plane.  In fragment order chunk u is row block rb = (u / 64) % RB, k block
+// kb = u / (64 RB), and inside the block lane l = u % 64 holds row 16 rb + l % 16,
+// k = 64 kb + 16 (l / 16) .. + 15.  Entries beyond R or K are zero.
 __global__ __launch_bounds__(XS_THREADS) void xs_slice(SliceOp a, SliceOp b, int64_t K, int64_t Kp,
                                                        int64_t a_blocks) {
   const bool is_a = blockIdx.x < a_blocks;
   const SliceOp &o = is_a ? a : b;
   const int64_t t = (int64_t)(is_a ? blockIdx.x : blockIdx.x - a_blocks) * XS_THREADS + threadIdx.x;
   uint32_t top = 0, low = XD;
-  if (t < o.chunks) {
+  if (t < 4 * o.chunks) {
+    const int64_t u = t / 4;
+    const int part = (int)(t % 4);
     const int64_t RB = o.Rp / 16;
-    const int64_t blk = t / 64;
-    const int l = (int)(t % 64);
+    const int64_t blk = u / 64;
+    const int l = (int)(u % 64);
     const int64_t kb = blk / RB, rb = blk - kb * RB;
     const int64_t row = rb * 16 + l % 16;
-    const int64_t k0 = kb * 64 + 16 * (l / 16);
-    int64_t X[16];
-#pragma unroll
-    for (int j = 0; j < 16; ++j) X[j] = 0;
+    const int64_t k0 = kb * 64 + 16 * (l / 16) + 4 * part;
+    int64_t X[4] = {0, 0, 0, 0};
     bool bad = false;
     if (row < o.R) {
       const uint16_t *p = o.src + row * o.rs + k0 * o.ks;
-      if (o.vec && k0 + 16 <= K) {
+      if (o.vec && k0 + 4 <= K) {
         for (int c = 0; c < o.planes; ++c) {
-          const uint4 v0 = *(const uint4 *)(p + c * o.plane);
-          const uint4 v1 = *(const uint4 *)(p + c * o.plane + 8);
-          const uint32_t w[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+          const uint2 v = *(const uint2 *)(p + c * o.plane);
+          const uint32_t w[2] = {v.x, v.y};
 #pragma unroll
-          for (int j = 0; j < 16; ++j) {
+          for (int j = 0; j < 4; ++j) {
             const uint32_t bits = (w[j / 2] >> (16 * (j % 2))) & 0xFFFFu;
             if (f16_nonfinite(bits)) bad = true;
             else X[j] += f16_units(bits);
@@ -167,7 +169,7 @@ __global__ __launch_bounds__(XS_THREADS) void xs_slice(SliceOp a, SliceOp b, int
       } else {
         for (int c = 0; c < o.planes; ++c) {
 #pragma unroll
-          for (int j = 0; j < 16; ++j) {
+          for (int j = 0; j < 4; ++j) {
             if (k0 + j < K) {
               const uint32_t bits = p[c * o.plane + j * o.ks];
               if (f16_nonfinite(bits)) bad = true;
@@ -176,14 +178,16 @@ __global__ __launch_bounds__(XS_THREADS) void xs_slice(SliceOp a, SliceOp b, int
           }
         }
       }
-      if (bad) o.bad[row] = 1;
+      if (bad) {
+        o.bad[row] = 1;
+        o.stats[XBADW] = 1;
+      }
     }
-    uint32_t lo[16], hi[16];
+    uint32_t lo[4], hi[4];
     uint64_t any = 0;
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      const uint64_t Y = (uint64_t)X[j] + XBIAS;
-      const uint64_t D = Y ^ XBIAS;  // the digits as bytes; zero digits are zero bytes
+    for (int j = 0; j < 4; ++j) {
+      const uint64_t D = ((uint64_t)X[j] + XBIAS) ^ XBIAS;  // the digits as bytes; zero digits are zero bytes
       any |= D;
       lo[j] = (uint32_t)D;
       hi[j] = (uint32_t)(D >> 32);
@@ -192,22 +196,16 @@ __global__ __launch_bounds__(XS_THREADS) void xs_slice(SliceOp a, SliceOp b, int
     }
     if (any) low = (uint32_t)(__builtin_ctzll(any) / 8);
     const int64_t level = o.chunks * 16;
-    int8_t *dst = o.D + t * 16;
+    int8_t *dst = o.D + t * 4;
 #pragma unroll
     for (int s = 0; s < XD; ++s) {
-      uint32_t w[4];
+      uint32_t v = 0;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        uint32_t v = 0;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int j = 4 * q + i;
-          const uint32_t byte = s < 4 ? (lo[j] >> (8 * s)) & 0xFFu : (hi[j] >> (8 * (s - 4))) & 0xFFu;
-          v |= byte << (8 * i);
-        }
-        w[q] = v;
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t byte = s < 4 ? (lo[j] >> (8 * s)) & 0xFFu : (hi[j] >> (8 * (s - 4))) & 0xFFu;
+        v |= byte << (8 * j);
       }
-      *(uint4 *)(dst + s * level) = make_uint4(w[0], w[1], w[2], w[3]);
+      *(uint32_t *)(dst + s * level) = v;
     }
   }
   // every lane of the workgroup takes part in the reductions
@@ -283,20 +281,22 @@ struct XmArgs {
   int64_t M, N, Kp, Mp, Np;
   int nc;
   uint16_t *C;       // [nc][M][N]
+  int cvec;          // rows of C may be written 16 bytes at a time (N % 8 == 0, C aligned)
   i128 *partial;     // [S][M][N] when the code path that runs needs S > 1 chunks
   int64_t tiles_n;   // workgroup tiles along N
 };
 
 struct XLevels {
   int loA, loB, nA, nB;
-  bool small;  // both operands within three levels: the DM = 3 code path runs
+  bool small;   // both operands within three levels: the DM = 3 code path runs
+  bool anybad;  // some input component is infinite or NaN
 };
 
 // The first wavefront reads slot l of each kind in lane l and reduces; the result
 // reaches the other wavefronts through LDS.  Every lane of the workgroup must call
 // this (it holds a barrier).
 __device__ __forceinline__ XLevels x_levels(const uint32_t *stats) {
-  __shared__ uint32_t sw[4];
+  __shared__ uint32_t sw[5];
   XLevels v;
   if (threadIdx.x < 64) {
     const int l = threadIdx.x;
@@ -305,8 +305,10 @@ __device__ __forceinline__ XLevels x_levels(const uint32_t *stats) {
       const uint32_t m = __ockl_wfred_max_u32(stats[(kind * XSLOTS + l) * 64]);
       if (l == 0) sw[kind] = m;
     }
+    if (l == 0) sw[4] = stats[XBADW];
   }
   __syncthreads();
+  v.anybad = sw[4] != 0;
   uint32_t w[4];
 #pragma unroll
   for (int kind = 0; kind < 4; ++kind) w[kind] = sw[kind];
@@ -335,16 +337,145 @@ __device__ __forceinline__ uint32_t take_f16_fast(int64_t &rem) {
   return ((uint32_t)sgn & 0x8000u) | (uint32_t)((qe - 24) * 1024 + (int)n);
 }
 
-// One wavefront's WTR x WTC tiles of 16 x 16 outputs with v_mfma_i32_16x16x64_i8
-// (result element i of lane l is row 4 (l / 16) + i, column l % 16 of its tile), one
-// int32 accumulator per tile and shift class, over k blocks [kb0, kb1).  The operand
-// fragments of the next k block are loaded while the current one is multiplied.
+// Epilogue of one wavefront's WTR x WTC tiles of 16 x 16 outputs (accumulator element
+// i of lane l is row 4 (l / 16) + i, column l % 16 of its tile, one int32 accumulator
+// per tile and shift class).  stage: 16-byte aligned LDS of at least 2560 bytes owned by
+// this wavefront.
 template <int DM, int WTR, int WTC>
+__device__ __forceinline__ void xm_epilogue(const XmArgs &g, const XLevels &lv, v4i (&acc)[2 * DM - 1][WTR][WTC],
+                                            int64_t row0, int64_t col0, int64_t chunk, int64_t S, uint16_t *st) {
+  constexpr int NCLS = 2 * DM - 1;
+  const int lane = threadIdx.x % 64;
+  // V = sum_q acc[q] 256^q 2^shift0 exactly.  First a conservative test that every
+  // value of the wavefront stays below 2^62 in magnitude: each term is below
+  // 2^(bitlen|acc[q]| + 8 q + shift0) and there are at most 11 terms.  Then, when it
+  // holds, V is summed in wrapping 64-bit arithmetic, which is exact because the true
+  // sum fits; otherwise in 128-bit integers.
+  const int shift0 = 8 * (lv.loA + lv.loB);
+  bool fits = true;
+#pragma unroll
+  for (int r = 0; r < WTR; ++r)
+#pragma unroll
+    for (int c = 0; c < WTC; ++c)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        int hb = 0;
+#pragma unroll
+        for (int q = 0; q < NCLS; ++q) {
+          const int32_t x = acc[q][r][c][i];
+          const uint32_t ax = (uint32_t)(x < 0 ? -(int64_t)x : (int64_t)x);
+          const int bl = ax ? 32 - __builtin_clz(ax) : 0;
+          hb = max(hb, bl ? bl + 8 * q : 0);
+        }
+        fits = fits && (hb == 0 || hb + 4 + shift0 <= 62);
+      }
+  const bool fast = __all(fits) && !lv.anybad && S == 1;  // uniform across the wavefront
+  const int64_t MN = g.M * g.N;
+  if (fast) {
+    // V in wrapping 64-bit arithmetic (exact: |V| < 2^62), then one component at a
+    // time: each lane rounds its outputs and writes them to the wavefront's LDS tile,
+    // which goes back to C row by row in 16-byte pieces.
+    int64_t v[WTR][WTC][4];
+#pragma unroll
+    for (int r = 0; r < WTR; ++r)
+#pragma unroll
+      for (int c = 0; c < WTC; ++c)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          uint64_t vu = 0;
+#pragma unroll
+          for (int q = 0; q < NCLS; ++q) {
+            const int sh = 8 * q + shift0;
+            vu += sh < 64 ? (uint64_t)(int64_t)acc[q][r][c][i] << sh : 0;
+          }
+          v[r][c][i] = (int64_t)vu;
+        }
+    constexpr int TR = 16 * WTR, TC = 16 * WTC, LD = TC + 8;
+    static_assert(TR * LD * 2 <= 2560, "stage tile too small");
+    const bool vec = g.cvec && col0 + TC <= g.N;
+    for (int k = 0; k < g.nc; ++k) {
+#pragma unroll
+      for (int r = 0; r < WTR; ++r)
+#pragma unroll
+        for (int c = 0; c < WTC; ++c)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            st[(16 * r + 4 * (lane / 16) + i) * LD + 16 * c + lane % 16] = (uint16_t)take_f16_fast(v[r][c][i]);
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      uint16_t *Ck = g.C + k * MN;
+#pragma unroll
+      for (int q0 = 0; q0 < TR * TC / 8; q0 += 64) {
+        const int q = q0 + lane;
+        const int rr = q / (TC / 8), cc = (q % (TC / 8)) * 8;
+        const int64_t row = row0 + rr;
+        if (q < TR * TC / 8 && row < g.M) {
+          const uint16_t *src = st + rr * LD + cc;
+          if (vec) {
+            *(uint4 *)(Ck + row * g.N + col0 + cc) = *(const uint4 *)src;
+          } else {
+            for (int e = 0; e < 8; ++e)
+              if (col0 + cc + e < g.N) Ck[row * g.N + col0 + cc + e] = src[e];
+          }
+        }
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+    return;
+  }
+#pragma unroll
+  for (int r = 0; r < WTR; ++r) {
+#pragma unroll
+    for (int c = 0; c < WTC; ++c) {
+      const int64_t col = col0 + 16 * c + lane % 16;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int64_t row = row0 + 16 * r + 4 * (lane / 16) + i;
+        if (row < g.M && col < g.N) {
+          const int64_t idx = row * g.N + col;
+          // four consecutive classes fit one int64 (|acc| < 2^31, relative shifts up
+          // to 24 bits); the groups are combined 32 bits apart in 128 bits
+          constexpr int NG = (NCLS + 3) / 4;
+          int64_t part[NG];
+#pragma unroll
+          for (int q = 0; q < NG; ++q) part[q] = 0;
+#pragma unroll
+          for (int q = 0; q < NCLS; ++q) part[q / 4] += (int64_t)acc[q][r][c][i] * ((int64_t)1 << (8 * (q % 4)));
+          u128 Vu = 0;
+#pragma unroll
+          for (int q = 0; q < NG; ++q) Vu += (u128)(i128)part[q] << (32 * q);
+          const i128 V = (i128)(Vu << shift0);
+          if (S > 1) g.partial[chunk * MN + idx] = V;
+          else store_split(V, g.nc, g.bad_a[row] | g.bad_b[col], g.C, MN, idx);
+        }
+      }
+    }
+  }
+}
+
+// One wavefront's WTR x WTC tiles over k blocks [kb0, kb1), operand fragments read
+// straight from the digit planes; the fragments of the next k block are loaded while
+// the current one is multiplied.
+//
+// KS = 2: two wavefronts share each tile, one per half of the k blocks (khalf); the
+// second adds its accumulators into the first's through LDS (red: 16 KiB, exact integer
+// sums) and leaves, and the first runs the epilogue.  Every lane of the workgroup must
+// call it then (it holds barriers).
+template <int DM, int WTR, int WTC, int KS = 1>
 __device__ __forceinline__ void xm_tile(const XmArgs &g, const XLevels &lv, int64_t row0, int64_t col0,
-                                        int64_t chunk, int64_t kb0, int64_t kb1, int64_t S) {
+                                        int64_t chunk, int64_t kb0, int64_t kb1, int64_t S, uint16_t *st,
+                                        int khalf = 0, int *red = nullptr) {
   constexpr int NCLS = 2 * DM - 1;
   const int lane = threadIdx.x % 64;
   const int64_t KB = g.Kp / 64;
+  if constexpr (KS == 2) {
+    const int64_t mid = kb0 + (kb1 - kb0 + 1) / 2;
+    if (khalf) kb0 = mid;
+    else kb1 = mid;
+  }
 
   v4i acc[NCLS][WTR][WTC];
 #pragma unroll
@@ -402,85 +533,52 @@ __device__ __forceinline__ void xm_tile(const XmArgs &g, const XLevels &lv, int6
       for (int c = 0; c < WTC; ++c) fb[s][c] = nb[s][c];
     }
   }
-
-  // V = sum_q acc[q] 256^q 2^shift0 exactly.  First a conservative test that every
-  // value of the wavefront stays below 2^62 in magnitude: each term is below
-  // 2^(bitlen|acc[q]| + 8 q + shift0) and there are at most 11 terms.  Then, when it
-  // holds, V is summed in wrapping 64-bit arithmetic, which is exact because the true
-  // sum fits; otherwise in 128-bit integers.
-  const int shift0 = 8 * (lv.loA + lv.loB);
-  bool fits = true;
+  if constexpr (KS == 2) {
+    static_assert(WTR * WTC * 4 <= 16, "reduction buffer too small");
+    const int qw = (threadIdx.x / 64) % 4;
 #pragma unroll
-  for (int r = 0; r < WTR; ++r)
+    for (int q = 0; q < NCLS; ++q) {
+      if (khalf) {
 #pragma unroll
-    for (int c = 0; c < WTC; ++c)
+        for (int r = 0; r < WTR; ++r)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        int hb = 0;
+          for (int c = 0; c < WTC; ++c)
 #pragma unroll
-        for (int q = 0; q < NCLS; ++q) {
-          const int32_t x = acc[q][r][c][i];
-          const uint32_t ax = (uint32_t)(x < 0 ? -(int64_t)x : (int64_t)x);
-          const int bl = ax ? 32 - __builtin_clz(ax) : 0;
-          hb = max(hb, bl ? bl + 8 * q : 0);
-        }
-        fits = fits && (hb == 0 || hb + 4 + shift0 <= 62);
+            for (int i = 0; i < 4; ++i) red[(qw * 16 + (r * WTC + c) * 4 + i) * 64 + lane] = acc[q][r][c][i];
       }
-  const bool fast = __all(fits);  // uniform across the wavefront
-  const int64_t MN = g.M * g.N;
+      __syncthreads();
+      if (!khalf) {
 #pragma unroll
-  for (int r = 0; r < WTR; ++r) {
+        for (int r = 0; r < WTR; ++r)
 #pragma unroll
-    for (int c = 0; c < WTC; ++c) {
-      const int64_t col = col0 + 16 * c + lane % 16;
+          for (int c = 0; c < WTC; ++c)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int64_t row = row0 + 16 * r + 4 * (lane / 16) + i;
-        if (row < g.M && col < g.N) {
-          const int64_t idx = row * g.N + col;
-          if (fast && S == 1) {
-            uint64_t vu = 0;
-#pragma unroll
-            for (int q = 0; q < NCLS; ++q) {
-              const int sh = 8 * q + shift0;
-              vu += sh < 64 ? (uint64_t)(int64_t)acc[q][r][c][i] << sh : 0;
-            }
-            int64_t v = (int64_t)vu;
-            if (g.bad_a[row] | g.bad_b[col]) {
-              for (int k = 0; k < g.nc; ++k) g.C[k * MN + idx] = 0x7E00;
-            } else {
-              for (int k = 0; k < g.nc; ++k) g.C[k * MN + idx] = (uint16_t)take_f16_fast(v);
-            }
-          } else {
-            // four consecutive classes fit one int64 (|acc| < 2^31, relative shifts up
-            // to 24 bits); the groups are combined 32 bits apart in 128 bits
-            constexpr int NG = (NCLS + 3) / 4;
-            int64_t part[NG];
-#pragma unroll
-            for (int q = 0; q < NG; ++q) part[q] = 0;
-#pragma unroll
-            for (int q = 0; q < NCLS; ++q) part[q / 4] += (int64_t)acc[q][r][c][i] * ((int64_t)1 << (8 * (q % 4)));
-            u128 Vu = 0;
-#pragma unroll
-            for (int q = 0; q < NG; ++q) Vu += (u128)(i128)part[q] << (32 * q);
-            const i128 V = (i128)(Vu << shift0);
-            if (S > 1) g.partial[chunk * MN + idx] = V;
-            else store_split(V, g.nc, g.bad_a[row] | g.bad_b[col], g.C, MN, idx);
-          }
-        }
+            for (int i = 0; i < 4; ++i) acc[q][r][c][i] += red[(qw * 16 + (r * WTC + c) * 4 + i) * 64 + lane];
       }
+      __syncthreads();
     }
+    if (khalf) return;
   }
+  xm_epilogue<DM, WTR, WTC>(g, lv, acc, row0, col0, chunk, S, st);
 }
 
-// One workgroup of 4 wavefronts per 64 x 64 tile of C; blockIdx.y is the K chunk.
+// One workgroup of 4 KS wavefronts per 64 x 64 tile of C; blockIdx.y is the K chunk.
 // Operands within three digit levels: each wavefront takes a 32 x 32 quarter (2 x 2
-// tiles, five shift classes).  Within four: two passes over 64 x 32 halves, each
-// wavefront taking 32 x 16 (2 x 1 tiles, seven classes).  Otherwise: four passes over
-// the 32 x 32 quarters, each wavefront taking one 16 x 16 tile (eleven classes).
-__global__ __attribute__((amdgpu_flat_work_group_size(1, 256), amdgpu_waves_per_eu(2))) void xm_kernel(XmArgs g) {
+// tiles, five shift classes), with KS = 2 two wavefronts per quarter splitting the k
+// blocks (for grids too small to fill the chip).  Within four levels: two passes over
+// 64 x 32 halves, each wavefront taking 32 x 16 (2 x 1 tiles, seven classes).
+// Otherwise: four passes over the 32 x 32 quarters, each wavefront taking one 16 x 16
+// tile (eleven classes).  The second group of wavefronts of a KS = 2 workgroup takes
+// part in the three-level path only.
+template <int KS>
+__global__ __attribute__((amdgpu_flat_work_group_size(1, 256 * KS), amdgpu_waves_per_eu(2))) void xm_kernel(
+    XmArgs g) {
+  // epilogue staging: 2560 bytes per wavefront of the first group; KS = 2 reduction:
+  // 16 KiB, used before the epilogue
+  __shared__ __attribute__((aligned(16))) int8_t smem[KS == 2 ? 16384 : 4 * 2560];
   const XLevels lv = x_levels(g.stats);
-  const int wave = threadIdx.x / 64;
+  const int wave = (threadIdx.x / 64) % 4;
+  const int khalf = threadIdx.x / 256;
   const int64_t tile = blockIdx.x;
   const int64_t tm = tile / g.tiles_n, tn = tile - tm * g.tiles_n;
   const int64_t KB = g.Kp / 64;
@@ -491,15 +589,20 @@ __global__ __attribute__((amdgpu_flat_work_group_size(1, 256), amdgpu_waves_per_
   if (kb0 >= KB && KB > 0) return;  // the grid holds the chunks of the smallest chunk size
   const int64_t kb1 = min(KB, kb0 + CKB);
   const int64_t S = KB == 0 ? 1 : (KB + CKB - 1) / CKB;
+  uint16_t *st = (uint16_t *)(smem + wave * 2560);
   if (dm == 3) {
-    xm_tile<3, 2, 2>(g, lv, tm * 64 + (wave / 2) * 32, tn * 64 + (wave % 2) * 32, chunk, kb0, kb1, S);
-  } else if (dm == 4) {
+    xm_tile<3, 2, 2, KS>(g, lv, tm * 64 + (wave / 2) * 32, tn * 64 + (wave % 2) * 32, chunk, kb0, kb1, S, st, khalf,
+                         (int *)smem);
+    return;
+  }
+  if (khalf) return;
+  if (dm == 4) {
     for (int sub = 0; sub < 2; ++sub)
-      xm_tile<4, 2, 1>(g, lv, tm * 64 + (wave / 2) * 32, tn * 64 + sub * 32 + (wave % 2) * 16, chunk, kb0, kb1, S);
+      xm_tile<4, 2, 1>(g, lv, tm * 64 + (wave / 2) * 32, tn * 64 + sub * 32 + (wave % 2) * 16, chunk, kb0, kb1, S, st);
   } else {
     for (int sub = 0; sub < 4; ++sub)
       xm_tile<6, 1, 1>(g, lv, tm * 64 + (sub / 2) * 32 + (wave / 2) * 16, tn * 64 + (sub % 2) * 32 + (wave % 2) * 16,
-                       chunk, kb0, kb1, S);
+                       chunk, kb0, kb1, S, st);
   }
 }
 
@@ -572,7 +675,7 @@ hipError_t launch_matmul_exact(int nc, int64_t M, int64_t N, int64_t K, const vo
     a.src = (const uint16_t *)A;
     a.planes = a_mc ? nc : 1;
     a.kcontig = 1;
-    a.vec = (K % 8 == 0) && ((uintptr_t)A % 16 == 0);
+    a.vec = (K % 4 == 0) && ((uintptr_t)A % 8 == 0);
     a.plane = M * K;
     a.rs = K;
     a.ks = 1;
@@ -585,7 +688,7 @@ hipError_t launch_matmul_exact(int nc, int64_t M, int64_t N, int64_t K, const vo
     b.src = (const uint16_t *)B;
     b.planes = b_mc ? nc : 1;
     b.kcontig = b_trans ? 1 : 0;
-    b.vec = b_trans && (K % 8 == 0) && ((uintptr_t)B % 16 == 0);
+    b.vec = b_trans && (K % 4 == 0) && ((uintptr_t)B % 8 == 0);
     b.plane = K * N;
     b.rs = b_trans ? K : 1;
     b.ks = b_trans ? 1 : N;
@@ -595,8 +698,8 @@ hipError_t launch_matmul_exact(int nc, int64_t M, int64_t N, int64_t K, const vo
     b.bad = bad_b;
     b.stats = stats;
     b.chunks = L.Np * L.Kp / 16;
-    const int64_t ab = (a.chunks + XS_THREADS - 1) / XS_THREADS;
-    const int64_t bb = (b.chunks + XS_THREADS - 1) / XS_THREADS;
+    const int64_t ab = (4 * a.chunks + XS_THREADS - 1) / XS_THREADS;
+    const int64_t bb = (4 * b.chunks + XS_THREADS - 1) / XS_THREADS;
     hipLaunchKernelGGL(xs_slice, dim3((unsigned)(ab + bb)), dim3(XS_THREADS), 0, stream, a, b, K, L.Kp, ab);
   }
   XmArgs g;
@@ -612,11 +715,17 @@ hipError_t launch_matmul_exact(int nc, int64_t M, int64_t N, int64_t K, const vo
   g.Np = L.Np;
   g.nc = nc;
   g.C = (uint16_t *)C;
+  g.cvec = (N % 8 == 0) && ((uintptr_t)C % 16 == 0);
   g.partial = (i128 *)(w + L.off_part);
   {
     g.tiles_n = L.Np / 64;
     const int64_t tiles = (L.Mp / 64) * g.tiles_n;
-    hipLaunchKernelGGL(xm_kernel, dim3((unsigned)tiles, (unsigned)L.Smax), dim3(256), 0, stream, g);
+    // fewer workgroups than two per compute unit: split each tile's k blocks over two
+    // wavefronts per quarter
+    if (tiles * L.Smax < 512)
+      hipLaunchKernelGGL(xm_kernel<2>, dim3((unsigned)tiles, (unsigned)L.Smax), dim3(512), 0, stream, g);
+    else
+      hipLaunchKernelGGL(xm_kernel<1>, dim3((unsigned)tiles, (unsigned)L.Smax), dim3(256), 0, stream, g);
   }
   if (L.Smax > 1) {
     const int64_t n = M * N;
