@@ -15,6 +15,7 @@ Also reported on the same line (not part of `value`):
   * the other workloads (64^3 binary32 nc=2; 1024^3 binary16 nc=2 and 3; the
     4096x1024x1024 binary16 nc=3 MC-Linear over 100 layers; the exact binary16
     product on the int8 matrix cores at 1024^3 and the MC-Linear layer shape; the
+    paper's linear-regression gradient descent (time per step, final loss); the
     2^26-element binary16
     nc=3 elementwise operations with their HBM bandwidth; the K-split Dot and MV; the
     paper's BMM-MCN and AddMM-MCN sizes);
@@ -380,6 +381,51 @@ def bench_exact(torch, mcf, oracle, inputs, steps=20):
     return out
 
 
+def bench_linreg(torch, mcf, inputs, steps=3000):
+    """The paper's linear-regression precision experiment (Section 2.4): X 10000 x 2
+    ~ N(-0.5, 0.5^2), y = X W*^T, gradient descent with lr = 0.05 on an MC-Linear layer
+    without bias (mc_linreg_gd_step, one call per step).  Reports the time per step and
+    the mean-squared error before the first and after the last step, beside plain
+    float64 gradient descent on the same data (context, like the paper's float64 row)."""
+    n, d, lr = 10000, 2, 0.05
+    out = {}
+    for dt, nc in ((np.float16, 1), (np.float16, 2), (np.float16, 3), (np.float32, 1), (np.float32, 2)):
+        X, y_neg, W0, _ = inputs.linreg_inputs(n, d, nc, dt, seed=0)
+        tX, ty, tW = (torch.from_numpy(np.ascontiguousarray(a)).cuda() for a in (X, y_neg, W0))
+        loss = torch.empty(nc, dtype=tW.dtype, device="cuda")
+        ws = torch.empty(mcf.mc_linreg_workspace(0 if dt == np.float16 else 1, nc, n, d), dtype=torch.uint8,
+                         device="cuda")
+        mcf.mc_linreg_gd_step(tX, ty, tW, lr, loss=loss, workspace=ws)
+        torch.cuda.synchronize()
+        first = float(loss.double().sum())
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        for _ in range(steps - 1):
+            mcf.mc_linreg_gd_step(tX, ty, tW, lr, loss=loss, workspace=ws)
+        e.record()
+        torch.cuda.synchronize()
+        us = s.elapsed_time(e) * 1e3 / (steps - 1)
+        name = f"{'f16' if dt == np.float16 else 'f32'}_nc{nc}"
+        # the same loss in float64 from the final weights (a binary16 MC loss underflows
+        # to 0 below the smallest subnormal, 2^-24)
+        w = tW.double().sum(dim=0).cpu().numpy()
+        r64 = X.astype(np.float64) @ w + y_neg.astype(np.float64)
+        out[name] = {"us_per_step": round(us, 2), "loss_first": first, "loss_last": float(loss.double().sum()),
+                     "loss_last_float64": float(np.mean(r64 * r64))}
+        log(f"  linreg {name}: {us:.1f} us/step, loss {first:.3g} -> {out[name]['loss_last']:.3g} "
+            f"(float64 {out[name]['loss_last_float64']:.3g})")
+    # float64 gradient descent on the binary32 data, for context
+    X, y_neg, W0, _ = inputs.linreg_inputs(n, d, 1, np.float32, seed=0)
+    X64, y64, w = X.astype(np.float64), -y_neg.astype(np.float64), W0[0].astype(np.float64)
+    for _ in range(steps):
+        r = X64 @ w - y64
+        w = w - lr * (2.0 / n) * (X64.T @ r)
+    r = X64 @ w - y64
+    out["float64_reference_loss_last"] = float(np.mean(r * r))
+    out["workload"] = f"n = {n}, d = {d}, lr = {lr}, {steps} steps; one mc_linreg_gd_step call per step"
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -486,6 +532,8 @@ def main():
         extra["linear_4096x1024x1024_f16_nc3"] = bench_linear(torch, mcf, inputs)
         log("exact binary16 products (int8 matrix cores)")
         extra["exact"] = bench_exact(torch, mcf, oracle, inputs)
+        log("linear-regression gradient descent")
+        extra["linreg"] = bench_linreg(torch, mcf, inputs)
         log("elementwise")
         extra["elementwise"] = bench_elementwise(torch, mcf, inputs)
         log("K-split products")

@@ -11,8 +11,8 @@
  * Memory.  All tensor pointers are DEVICE pointers owned by the caller; the library
  *   allocates nothing per call and keeps no state besides a per-device binary16
  *   exponential table (128 KiB, built on the first mc_exp call on a device).  Calls
- *   that need scratch memory (mc_matmul_splitk, mc_matmul_exact) take a
- *   caller-owned workspace.
+ *   that need scratch memory (mc_matmul_splitk, mc_matmul_exact, mc_linreg_gd_step)
+ *   take a caller-owned workspace.
  * Layout.  Dense, component-major ("planar"): component c of element i of an MC
  *   array of n elements is at element offset c*n + i.  A plain tensor is one plane.
  *   Matrices are row-major inside each plane.  The paper's interleaved layout
@@ -246,6 +246,35 @@ int64_t mc_matmul_exact_workspace(int dtype, int nc, int64_t M, int64_t N, int64
  * y: [nc][batch][out]. */
 int mc_linear_fwd(int dtype, int nc, int64_t batch, int64_t in, int64_t out, const void *x, const void *W,
                   const void *b, void *y, void *stream);
+
+/* One gradient-descent step of the paper's linear-regression precision experiment
+ * (Section 2.4): an MC-Linear layer without bias, W (out = 1 row of d weights), fitted
+ * to targets y with the mean-squared error L(W) = (1/n) sum_i (x_i . W - y_i)^2.
+ * The paper leaves the optimizer step unprinted and defines the gradient of an MC value
+ * as the plain gradient of its leading component (Section 2.1).  This call computes, in
+ * stream order:
+ *   yhat = MC-Linear(X, W) (MM-MCN order, as mc_linear_fwd);
+ *   r = Grow-ExpN(yhat, y_neg), the MC residual;
+ *   G = r^T X and RR = r . r, each by the K-split product with its default slice count
+ *     (mc_matmul_splitk_slices);
+ *   per weight j: g = ScalingN(G_j, fl(2/n)); grad_j = the leading component of g;
+ *     W_j = Grow-ExpN(W_j, fl(-lr * grad_j)) (one rounding of the product);
+ *   loss = ScalingN(RR, fl(1/n)), the loss at W before the update.
+ * fl(2/n), fl(1/n): the binary64 quotients rounded once to the component format;
+ * fl(-lr): the binary64 value -lr rounded to the component format.
+ * X: [n][d] plain; y_neg: [n] plain, the NEGATED targets (-y); W: [nc][d] MC, updated
+ *   in place; loss: [nc] MC, or NULL.  W and loss must not overlap each other, X, y_neg
+ *   or the workspace.
+ * workspace: device memory of at least mc_linreg_workspace(...) bytes, owned by the
+ *   caller (contents on entry do not matter; steps sharing it must not overlap in
+ *   time).  Too small: MCF_E_ARG.
+ * Sizes: n >= 1, d >= 1, n <= 2^30, d <= 2^20, n d <= 2^40. */
+int mc_linreg_gd_step(int dtype, int nc, int64_t n, int64_t d, const void *X, const void *y_neg, void *W, double lr,
+                      void *workspace, int64_t workspace_bytes, void *loss, void *stream);
+
+/* Workspace bytes mc_linreg_gd_step needs, or a negative mcf_status for arguments it
+ * would reject. */
+int64_t mc_linreg_workspace(int dtype, int nc, int64_t n, int64_t d);
 
 /* Human-readable name of a status code (static storage). */
 const char *mc_status_str(int status);

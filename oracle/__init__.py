@@ -411,6 +411,44 @@ def linear(X, W, bias=None, *, nc, rows=None, cols=None):
     return out.reshape(nc, T, O) if rows is None else out
 
 
+def linreg_gd_step(X, y_neg, W, lr, *, slices_g, slices_l):
+    """One gradient-descent step of MC-Linear regression with the mean-squared error
+    (the precision experiment of Section 2.4), written as the composition of this
+    module's pinned operations.  The paper does not print the optimizer step; it keeps
+    the gradient of an MC value as the plain gradient of its leading component (Section
+    2.1).  The reading taken here:
+        yhat = MC-Linear(X, W)                      (linear, MM-MCN order)
+        r    = Grow-ExpN(yhat, -y)                  (add, MC + plain)
+        G    = r^T X,  RR = r . r                   (matmul_splitk, slices_g / slices_l)
+        g    = ScalingN(G, fl(2/n)); grad = g_0     (mul, MC x plain; leading component)
+        W'   = Grow-ExpN(W, fl(-lr * grad))         (fl_mul, then add)
+        loss = ScalingN(RR, fl(1/n))                (the loss at W, before the update)
+    fl(2/n), fl(1/n): the binary64 quotient rounded to the component format; fl(-lr):
+    the binary64 value -lr rounded to it.
+
+    X: (n, d) plain; y_neg: (n,) plain (-y); W: (nc, d) MC.  Returns (W', loss (nc,)).
+    """
+    dtype = np.dtype(W.dtype)
+    fmt = fmt_of(dtype)
+    X = _planar(X, dtype)
+    y_neg = _planar(y_neg, dtype)
+    W = _planar(W, dtype)
+    nc, d = W.shape
+    n = X.shape[0]
+    yhat = linear(X, W.reshape(nc, 1, d), nc=nc)                  # (nc, n, 1)
+    r = add(yhat.reshape(nc, n), y_neg.reshape(1, n), nc=nc, y_mc=False)  # (nc, n)
+    G = matmul_splitk(r.reshape(nc, 1, n), X, nc=nc, slices=slices_g, b_mc=False).reshape(nc, d)
+    RR = matmul_splitk(r.reshape(nc, 1, n), r.reshape(nc, n, 1), nc=nc, slices=slices_l).reshape(nc, 1)
+    s2n = fl_round(fmt, np.array([2.0 / n]))[0]
+    s1n = fl_round(fmt, np.array([1.0 / n]))[0]
+    neg_lr = fl_round(fmt, np.array([-float(lr)]))[0]
+    g = mul(G, np.full((1, d), s2n, dtype=dtype), nc=nc, y_mc=False)
+    step = fl_mul(fmt, np.full(d, neg_lr), g[0].astype(np.float64)).astype(dtype).reshape(1, d)
+    W_new = add(W, step, nc=nc, y_mc=False)
+    loss = mul(RR, np.full((1, 1), s1n, dtype=dtype), nc=nc, y_mc=False).reshape(nc)
+    return W_new, loss
+
+
 def matmul_exact_err(A, B, C, *, bias=None, rows=None, cols=None):
     """Exact error of a computed product C (nc, M, N) -- or (nc, count) at positions --
     against the exact product of the MC inputs A (planes, M, K), B (planes, K, N),

@@ -21,7 +21,7 @@ __all__ = [
     "mc_add", "mc_mul", "mc_div", "mc_exp", "mc_renorm", "mc_matmul", "mc_matmul_splitk",
     "mc_matmul_splitk_slices", "mc_matmul_splitk_workspace", "mc_linear_fwd", "mc_status_str",
     "mc_matmul_batched", "mc_bmm", "mc_addmm", "matmul_mcn", "mc_mul_slow", "mc_square", "mc_matmul_pruned",
-    "mc_matmul_exact", "mc_matmul_exact_workspace", "lib", "LIB_PATH", "MCFError",
+    "mc_matmul_exact", "mc_matmul_exact_workspace", "mc_linreg_workspace", "mc_linreg_gd_step", "lib", "LIB_PATH", "MCFError",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmcf.so")
@@ -75,6 +75,10 @@ def lib() -> ctypes.CDLL:
         L.mc_matmul_exact.argtypes = [ci, ci, i64, i64, i64, vp, ci, vp, ci, ci, vp, i64, vp, vp]
         L.mc_matmul_exact_workspace.restype = i64
         L.mc_matmul_exact_workspace.argtypes = [ci, ci, i64, i64, i64]
+        L.mc_linreg_workspace.restype = i64
+        L.mc_linreg_workspace.argtypes = [ci, ci, i64, i64]
+        L.mc_linreg_gd_step.restype = ci
+        L.mc_linreg_gd_step.argtypes = [ci, ci, i64, i64, vp, vp, vp, ctypes.c_double, vp, i64, vp, vp]
         L.mc_linear_fwd.restype = ci
         L.mc_linear_fwd.argtypes = [ci, ci, i64, i64, i64, vp, vp, vp, vp, vp]
         L.mc_status_str.restype = ctypes.c_char_p
@@ -333,6 +337,37 @@ def mc_matmul_exact(A, B, *, nc: int, a_mc: bool = True, b_mc: bool = True, b_tr
                                _dev(out, "out"), _stream(A))
     _check(st, "mc_matmul_exact")
     return out
+
+
+def mc_linreg_workspace(dtype_code: int, nc: int, n: int, d: int) -> int:
+    """Workspace bytes of one linear-regression gradient-descent step."""
+    w = lib().mc_linreg_workspace(dtype_code, nc, n, d)
+    _check(int(w) if w < 0 else 0, "mc_linreg_workspace")
+    return int(w)
+
+
+def mc_linreg_gd_step(X, y_neg, W, lr: float, *, loss=None, workspace=None):
+    """One gradient-descent step of MC-Linear regression with the mean-squared error
+    (see include/mcf.h).  X: (n, d) plain; y_neg: (n,) the negated targets; W: (nc, d)
+    MC, updated in place; loss: optional (nc,) MC output, the loss before the update.
+    `workspace`: an optional device byte tensor; one is allocated here when not given."""
+    torch = _torch()
+    if X.dim() != 2 or W.dim() != 2 or y_neg.dim() != 1:
+        raise ValueError("X must be (n, d), W (nc, d), y_neg (n,)")
+    n, d = X.shape
+    nc = W.shape[0]
+    if W.shape[1] != d or y_neg.shape[0] != n or X.dtype != W.dtype or y_neg.dtype != W.dtype:
+        raise ValueError("shape or dtype mismatch")
+    if loss is not None and (tuple(loss.shape) != (nc,) or loss.dtype != W.dtype):
+        raise ValueError("loss must be (nc,) of W's dtype")
+    code = _dtype_code(W)
+    if workspace is None:
+        workspace = torch.empty(mc_linreg_workspace(code, nc, n, d), dtype=torch.uint8, device=W.device)
+    st = lib().mc_linreg_gd_step(code, nc, n, d, _dev(X, "X"), _dev(y_neg, "y_neg"), _dev(W, "W"), float(lr),
+                                 _dev(workspace, "workspace"), workspace.numel() * workspace.element_size(),
+                                 None if loss is None else _dev(loss, "loss"), _stream(W))
+    _check(st, "mc_linreg_gd_step")
+    return W
 
 
 def mc_linear_fwd(x, W, b=None, *, out=None):

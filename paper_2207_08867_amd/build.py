@@ -18,7 +18,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libmcf.so")
-SOURCES = ["abi.cpp", "elementwise.hip", "matmul.hip", "splitk.hip", "exact.hip"]
+SOURCES = ["abi.cpp", "elementwise.hip", "matmul.hip", "splitk.hip", "exact.hip", "linreg.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 

@@ -93,6 +93,22 @@ int exact_check(int dtype, int nc, int64_t M, int64_t N, int64_t K, int a_mc, in
   return MCF_OK;
 }
 
+int linreg_check(int dtype, int nc, int64_t n, int64_t d) {
+  if (dtype != MCF_F16 && dtype != MCF_F32) return MCF_E_DTYPE;
+  if (nc < 1 || nc > MAX_NC) return MCF_E_NC;
+  if (n < 1 || d < 1) return MCF_E_SHAPE;
+  // X has n d elements; the sequential product's grid covers n rows, the K-split
+  // products' grids d outputs
+  if (n > ((int64_t)1 << 30) || d > ((int64_t)1 << 20) || n > (((int64_t)1 << 40) / d)) return MCF_E_SHAPE;
+  return MCF_OK;
+}
+
+// The component-format rounding of a binary64 value.
+double round_to_format(int dtype, double v) {
+  if (dtype == MCF_F16) return (double)(_Float16)v;
+  return (double)(float)v;
+}
+
 }  // namespace
 
 extern "C" {
@@ -340,6 +356,32 @@ int mc_matmul_exact(int dtype, int nc, int64_t M, int64_t N, int64_t K, const vo
     return MCF_E_ALIAS;
   return hip_status(
       mcf::launch_matmul_exact(nc, M, N, K, A, a_mc, B, b_mc, b_trans, workspace, C, (hipStream_t)stream));
+}
+
+int64_t mc_linreg_workspace(int dtype, int nc, int64_t n, int64_t d) {
+  const int st = linreg_check(dtype, nc, n, d);
+  if (st != MCF_OK) return st;
+  return mcf::linreg_workspace_bytes(dtype, nc, n, d);
+}
+
+int mc_linreg_gd_step(int dtype, int nc, int64_t n, int64_t d, const void *X, const void *y_neg, void *W, double lr,
+                      void *workspace, int64_t workspace_bytes, void *loss, void *stream) {
+  const int st = linreg_check(dtype, nc, n, d);
+  if (st != MCF_OK) return st;
+  if (!X || !y_neg || !W || !workspace) return MCF_E_NULL;
+  const int64_t wb = mcf::linreg_workspace_bytes(dtype, nc, n, d);
+  if (workspace_bytes < wb) return MCF_E_ARG;
+  const int64_t es = elem_size(dtype);
+  const int64_t xb = n * d * es, yb = n * es, Wb = nc * d * es, lb = nc * es;
+  if (overlap(W, Wb, X, xb) || overlap(W, Wb, y_neg, yb) || overlap(W, Wb, workspace, wb)) return MCF_E_ALIAS;
+  if (overlap(workspace, wb, X, xb) || overlap(workspace, wb, y_neg, yb)) return MCF_E_ALIAS;
+  if (loss && (overlap(loss, lb, W, Wb) || overlap(loss, lb, workspace, wb) || overlap(loss, lb, X, xb) ||
+               overlap(loss, lb, y_neg, yb)))
+    return MCF_E_ALIAS;
+  const double s2n = round_to_format(dtype, 2.0 / (double)n), s1n = round_to_format(dtype, 1.0 / (double)n);
+  const double neg_lr = round_to_format(dtype, -lr);
+  return hip_status(mcf::launch_linreg_step(dtype, nc, n, d, X, y_neg, W, s2n, s1n, neg_lr, workspace, loss,
+                                            (hipStream_t)stream));
 }
 
 int mc_linear_fwd(int dtype, int nc, int64_t batch, int64_t in, int64_t out, const void *x, const void *W,

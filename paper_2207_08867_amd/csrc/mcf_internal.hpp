@@ -66,4 +66,11 @@ int64_t exact_workspace_bytes(int64_t M, int64_t N, int64_t K);
 hipError_t launch_matmul_exact(int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B,
                                int b_mc, int b_trans, void *W, void *C, hipStream_t stream);
 
+// One gradient-descent step of MC-Linear regression (linreg.hip).  s2n, s1n and neg_lr
+// are fl(2/n), fl(1/n) and fl(-lr), already values of the component format.  ws holds
+// linreg_workspace_bytes(...) bytes.
+int64_t linreg_workspace_bytes(int dtype, int nc, int64_t n, int64_t d);
+hipError_t launch_linreg_step(int dtype, int nc, int64_t n, int64_t d, const void *X, const void *y_neg, void *W,
+                              double s2n, double s1n, double neg_lr, void *ws, void *loss, hipStream_t stream);
+
 }  // namespace mcf

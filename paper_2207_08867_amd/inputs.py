@@ -89,6 +89,21 @@ def linear_inputs(T, I, O, nc, dtype, layers=1, seed=0):
         yield x, W, b
 
 
+def linreg_inputs(n, d, nc, dtype, seed=0):
+    """The linear-regression precision experiment (Section 2.4): X (n, d) with entries
+    ~ N(-0.5, 0.5^2) rounded once to `dtype`; target weights W* (d,) ~ N(-0.5, 0.5^2) in
+    float64; targets y = X W*^T evaluated in float64 from the rounded X and rounded once;
+    initial weights W0 ~ U(-1/sqrt(d), 1/sqrt(d)) (a linear layer's default
+    initialisation) split into nc components.  Returns (X, y_neg = -y, W0 (nc, d), W*)."""
+    g = rng(seed)
+    X = g.normal(-0.5, 0.5, (n, d)).astype(dtype)
+    w_star = g.normal(-0.5, 0.5, d)
+    y = (X.astype(np.float64) @ w_star).astype(dtype)
+    lim = 1.0 / np.sqrt(d)
+    W0 = split(g.uniform(-lim, lim, d), nc, dtype)
+    return X, (-y).astype(dtype), W0, w_star
+
+
 def elementwise_suite(n: int, nc: int, dtype, seed=0):
     """The elementwise workload's operands drawn once: a ~ U[-1/2, 1/2] (first
     operand of every op and the Renormalize input), b ~ U[-1/2, 1/2] (second addend),
