@@ -20,7 +20,7 @@ import subprocess
 
 import numpy as np
 
-F16, F32 = 0, 1
+F16, F32, F64 = 0, 1, 2
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 _SRC = os.path.join(_HERE, "mcf_oracle.c")
@@ -94,7 +94,9 @@ def fmt_of(dtype) -> int:
         return F16
     if dt == np.float32:
         return F32
-    raise TypeError(f"component dtype must be float16 or float32, got {dt}")
+    if dt == np.float64:
+        return F64
+    raise TypeError(f"component dtype must be float16, float32 or float64, got {dt}")
 
 
 def _ptr(a: np.ndarray | None):

@@ -11,7 +11,8 @@
  * Number model (Section 2.1 and Appendix A.2.1 write every step as fl(.), one
  * rounding in the component format):
  *   - A component value is held in a C double.  Every double handled here is
- *     exactly representable in the component format (binary16 or binary32).
+ *     exactly representable in the component format (binary16, binary32 or
+ *     binary64).
  *   - fl(.) is IEEE-754 round-to-nearest-even into the component format, with
  *     gradual underflow and overflow to infinity.  It is implemented from the IEEE
  *     definition in round_to() below, on top of an exact or correctly-rounded double.
@@ -22,7 +23,11 @@
  *   - /   : correctly-rounded double quotient, then fl(.); innocuous by the same
  *     theorem (53 >= 2p+2 for p = 11 and p = 24).
  *   - fma : exact product, double sum with its exact remainder, then fl(.) with the
- *     remainder's sign used to break a tie (see fl_fma).
+ *     remainder's sign used to break a tie (see fl_fma); binary64: the C library's
+ *     fma, which rounds once.
+ *   - binary64 components: every double operation above is already the correctly
+ *     rounded binary64 result, and fl(.) is the identity on doubles.  No component
+ *     exponential is provided for binary64 (Exp-MCN rejects it).
  *   - exp : the component exponential is taken to be correctly rounded (the paper
  *     calls torch.exp and fixes no accuracy); computed as fl(.) of a double
  *     (binary16) or long double (binary32) exponential.  Exhaustive pinning for
@@ -45,6 +50,7 @@
 
 #define FMT_F16 0
 #define FMT_F32 1
+#define FMT_F64 2
 #define MAXC 8 /* largest component count handled by the fixed-size scratch arrays */
 
 /* ------------------------------------------------------------------------------ */
@@ -57,7 +63,7 @@ typedef struct {
   int emax; /* exponent of the largest finite number */
 } fmt_desc;
 
-static const fmt_desc FMTS[2] = {{11, -14, 15}, {24, -126, 127}};
+static const fmt_desc FMTS[3] = {{11, -14, 15}, {24, -126, 127}, {53, -1022, 1023}};
 
 /* Round the real number x + r to the format, where x is a double and r is an
  * infinitesimal remainder whose sign is dir (-1, 0 or +1).  IEEE round to nearest,
@@ -106,6 +112,7 @@ static double fl_div(int f, double a, double b) { return fl(f, a / b); }
  * only as exact double-precision bookkeeping).  fl(s) is the correctly rounded result
  * unless s sits exactly on a tie of the component format, where t decides. */
 static double fl_fma(int f, double a, double b, double c) {
+  if (f == FMT_F64) return fma(a, b, c); /* the C library's fma rounds once */
   double pr = a * b;
   double s = pr + c;
   double bv = s - pr;
@@ -153,12 +160,15 @@ static uint16_t f16_encode(double v) { /* v must be exactly representable */
 
 static double load_c(int f, const void *base, int64_t idx) {
   if (f == FMT_F16) return f16_decode(((const uint16_t *)base)[idx]);
+  if (f == FMT_F64) return ((const double *)base)[idx];
   return (double)((const float *)base)[idx];
 }
 
 static void store_c(int f, void *base, int64_t idx, double v) {
   if (f == FMT_F16)
     ((uint16_t *)base)[idx] = f16_encode(v);
+  else if (f == FMT_F64)
+    ((double *)base)[idx] = v;
   else
     ((float *)base)[idx] = (float)v;
 }
@@ -473,7 +483,8 @@ enum { OP_ADD = 0, OP_MUL = 1, OP_DIV = 2, OP_EXP = 3, OP_RENORM = 4, OP_SIMPLE_
  * Returns 0, or -1 on bad arguments. */
 int mcf_oracle_elementwise(int f, int op, int nc, int nc_out, int64_t n, const void *x, int x_mc,
                            const void *y, int y_mc, void *out) {
-  if (nc < 1 || nc > MAXC || (f != FMT_F16 && f != FMT_F32)) return -1;
+  if (nc < 1 || nc > MAXC || f < FMT_F16 || f > FMT_F64) return -1;
+  if (op == OP_EXP && f == FMT_F64) return -1; /* no correctly rounded binary64 exp here */
   int binary = (op == OP_ADD || op == OP_MUL || op == OP_DIV || op == OP_SCALING_EXPAND || op == OP_MUL_SLOW);
   if (binary && !x_mc && !y_mc) return -1;
   if (op == OP_MUL_SLOW && !(x_mc && y_mc)) return -1;
@@ -851,8 +862,13 @@ int mcf_oracle_matmul_exact_err(int f, int nc, int64_t M, int64_t N, int64_t K, 
         acc_add(&ea, a, 1);
         for (int cb = 0; cb < b_planes; ++cb) {
           double b = load_c(f, B, cb * K * N + k * N + j);
-          acc_add(&diff, a * b, -1); /* a*b is exact in double */
-          acc_add(&ex, a * b, 1);
+          /* a*b is exact in double for binary16/32 components; for binary64 ones
+           * it is split exactly as p + e, e = fma(a, b, -p) (no underflow assumed) */
+          double p = a * b, e = f == FMT_F64 ? fma(a, b, -p) : 0.0;
+          acc_add(&diff, p, -1);
+          acc_add(&ex, p, 1);
+          acc_add(&diff, e, -1);
+          acc_add(&ex, e, 1);
         }
       }
       for (int cb = 0; cb < b_planes; ++cb) acc_add(&eb, load_c(f, B, cb * K * N + k * N + j), 1);
