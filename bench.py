@@ -15,7 +15,8 @@ Also reported on the same line (not part of `value`):
   * the other workloads (64^3 binary32 nc=2; 1024^3 binary16 nc=2 and 3; the
     4096x1024x1024 binary16 nc=3 MC-Linear over 100 layers; the exact binary16
     product on the int8 matrix cores at 1024^3 and the MC-Linear layer shape; the
-    paper's linear-regression gradient descent (time per step, final loss); the
+    paper's linear-regression gradient descent (time per step, final loss); binary64
+    components (2^26-element Add-MCN, ScalingN, Div-MCN and a 1024^3 product); the
     2^26-element binary16
     nc=3 elementwise operations with their HBM bandwidth; the K-split Dot and MV; the
     paper's BMM-MCN and AddMM-MCN sizes);
@@ -161,7 +162,7 @@ def exact_error(oracle, A, B, C, nc, K, dt, count=64, seed=5):
     Cs = np.ascontiguousarray(C[:, rows, cols])
     err, absab, _ = oracle.matmul_exact_err(A, B, Cs, rows=rows, cols=cols)
     rel = np.abs(err) / absab
-    u = 2.0 ** -24 if dt == np.float32 else 2.0 ** -11
+    u = {np.dtype(np.float16): 2.0 ** -11, np.dtype(np.float32): 2.0 ** -24, np.dtype(np.float64): 2.0 ** -53}[np.dtype(dt)]
     floor = A.shape[0] * B.shape[0] * K * 2.0 ** -25 if dt == np.float16 else 0.0
     lim = 4 * K * u ** min(nc, 3) * absab + floor
     return {"max_rel_err": float(rel.max()), "bound_4Ku^nc": 4 * K * u ** nc,
@@ -381,6 +382,48 @@ def bench_exact(torch, mcf, oracle, inputs, steps=20):
     return out
 
 
+def bench_f64(torch, mcf, oracle, inputs, steps=10):
+    """binary64 components (the paper's MC float64): 2^26-element Add-MCN, ScalingN and
+    Div-MCN at nc = 2 (HBM bandwidth; Div-MCN also against the binary64 VALU rate), and
+    the 1024^3 MC x MC product at nc = 2 (VALU: binary64 adds and FMAs issue at half the
+    binary32 rate)."""
+    g = np.random.default_rng(0)
+    n, nc = 1 << 26, 2
+    a = torch.from_numpy(inputs.expansion(g, n, nc, np.float64)).cuda()
+    b = torch.from_numpy(inputs.expansion(g, n, nc, np.float64)).cuda()
+    d = torch.from_numpy(np.abs(inputs.expansion(g, n, nc, np.float64)) + np.array([[0.5], [0.0]])).cuda()
+    v = b[0].contiguous()
+    out = torch.empty((nc, n), dtype=torch.float64, device="cuda")
+    ops = {"add_mcn": (lambda: mcf.mc_add(a, b, nc=nc, out=out), 48),
+           "scaling_n": (lambda: mcf.mc_mul(a, v, nc=nc, y_mc=False, out=out), 40),
+           "div_mcn": (lambda: mcf.mc_div(a, d, nc=nc, out=out), 48)}
+    res = {}
+    for name, (fn, bpe) in ops.items():
+        for _ in range(2):
+            fn()
+        tm = Timer(torch)
+        for _ in range(steps):
+            tm.run(fn)
+        ms = float(np.median(tm.ms()))
+        gbs = bpe * n / (ms * 1e-3) / 1e9
+        res[name] = {"us": round(ms * 1e3, 1), "GB/s": round(gbs, 1), "hbm_frac": round(gbs * 1e9 / HBM_PEAK, 3)}
+        if name == "div_mcn":
+            fops = ew_fp_ops("div", nc)
+            res[name]["valu_frac_f64"] = round(fops * n / (ms * 1e-3) / (VALU_PEAK / 2), 3)
+        log(f"  f64 {name}: {ms * 1e3:.1f} us, {gbs:.0f} GB/s")
+    del a, b, d, v, out
+    A = inputs.expansion(g, (1024, 1024), nc, np.float64, 1 / 32)
+    B = inputs.expansion(g, (1024, 1024), nc, np.float64, 1 / 32)
+    C, _, kms = bench_matmul(torch, mcf, A, B, nc, 5, 2)
+    macs = 1024 ** 3
+    res["matmul_1024_nc2"] = {
+        "ms": round(kms, 3), "MC-GFLOP/s": round(2 * macs / (kms * 1e-3) / 1e9, 1),
+        "valu_frac_f64": round(algo_ops_per_mac(nc, True) * macs / (kms * 1e-3) / (VALU_PEAK / 2), 3),
+        "error": exact_error(oracle, A, B, C.cpu().numpy(), nc, 1024, np.float64)}
+    log(f"  f64 1024^3 nc=2: {kms:.2f} ms")
+    return {"workload": "binary64 components: 2^26 elements nc = 2; 1024^3 MC x MC nc = 2", "ops": res}
+
+
 def bench_linreg(torch, mcf, inputs, steps=3000):
     """The paper's linear-regression precision experiment (Section 2.4): X 10000 x 2
     ~ N(-0.5, 0.5^2), y = X W*^T, gradient descent with lr = 0.05 on an MC-Linear layer
@@ -534,6 +577,8 @@ def main():
         extra["exact"] = bench_exact(torch, mcf, oracle, inputs)
         log("linear-regression gradient descent")
         extra["linreg"] = bench_linreg(torch, mcf, inputs)
+        log("binary64 components")
+        extra["f64"] = bench_f64(torch, mcf, oracle, inputs)
         log("elementwise")
         extra["elementwise"] = bench_elementwise(torch, mcf, inputs)
         log("K-split products")

@@ -17,11 +17,13 @@
  *   array of n elements is at element offset c*n + i.  A plain tensor is one plane.
  *   Matrices are row-major inside each plane.  The paper's interleaved layout
  *   (components in the last dimension) converts with a transpose on the caller side.
- * Formats.  MCF_F16 = IEEE binary16 components, MCF_F32 = IEEE binary32.  Every step
- *   of every algorithm is one IEEE round-to-nearest-even operation in the component
- *   format with gradual underflow; FMA appears only where the algorithm names it
- *   (Two-Prod); component division is correctly rounded; the binary16 component
- *   exponential is correctly rounded.
+ * Formats.  MCF_F16 = IEEE binary16 components, MCF_F32 = IEEE binary32, MCF_F64 =
+ *   IEEE binary64 (the paper's MC float64).  Every step of every algorithm is one IEEE
+ *   round-to-nearest-even operation in the component format with gradual underflow;
+ *   FMA appears only where the algorithm names it (Two-Prod); component division is
+ *   correctly rounded; the binary16 and binary32 component exponentials are correctly
+ *   rounded.  mc_exp does not take MCF_F64 (MCF_E_DTYPE); mc_matmul_exact takes
+ *   MCF_F16 only.
  * Operand kinds.  Binary operations take an MC value and a plain tensor in either
  *   order, or two MC values (Section 2.1).  The flags x_mc / y_mc / a_mc / b_mc are 1
  *   for an MC operand of nc planes and 0 for a plain tensor of one plane; at least
@@ -48,7 +50,7 @@
 extern "C" {
 #endif
 
-typedef enum { MCF_F16 = 0, MCF_F32 = 1 } mcf_dtype;
+typedef enum { MCF_F16 = 0, MCF_F32 = 1, MCF_F64 = 2 } mcf_dtype;
 
 typedef enum {
   MCF_OK = 0,
@@ -107,7 +109,7 @@ int mc_square(int dtype, int nc, int64_t n, const void *x, void *out, void *stre
  * step.  The component exponential is correctly rounded in both formats (binary16
  * by table lookup; binary32 from a binary64 evaluation, with a double-double one
  * where that lies too close to a rounding boundary).  x, out: [nc][n]; out == x
- * allowed. */
+ * allowed.  MCF_F64: MCF_E_DTYPE. */
 int mc_exp(int dtype, int nc, int64_t n, const void *x, void *out, void *stream);
 
 /* Renormalization (Appendix A.2.1).

@@ -9,7 +9,7 @@ runs in the library's HIP kernels; there is no fallback.
 Tensor conventions (component-major):
   * an MC tensor with nc components and logical shape S is a torch tensor of shape
     (nc, *S); a plain tensor has shape S or (1, *S);
-  * component dtype torch.float16 or torch.float32; all tensors contiguous and on
+  * component dtype torch.float16, torch.float32 or torch.float64; all tensors contiguous and on
     the same GPU.
 """
 from __future__ import annotations
@@ -27,7 +27,7 @@ __all__ = [
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmcf.so")
 _lib = None
 
-MCF_F16, MCF_F32 = 0, 1
+MCF_F16, MCF_F32, MCF_F64 = 0, 1, 2
 
 
 class MCFError(RuntimeError):
@@ -111,7 +111,9 @@ def _dtype_code(t) -> int:
         return MCF_F16
     if t.dtype == torch.float32:
         return MCF_F32
-    raise TypeError(f"component dtype must be float16 or float32, got {t.dtype}")
+    if t.dtype == torch.float64:
+        return MCF_F64
+    raise TypeError(f"component dtype must be float16, float32 or float64, got {t.dtype}")
 
 
 def _dev(t, name):

@@ -10,7 +10,7 @@ namespace {
 
 constexpr int MAX_NC = 4;
 
-int64_t elem_size(int dtype) { return dtype == MCF_F16 ? 2 : 4; }
+int64_t elem_size(int dtype) { return dtype == MCF_F16 ? 2 : (dtype == MCF_F64 ? 8 : 4); }
 
 bool overlap(const void *a, int64_t abytes, const void *b, int64_t bbytes) {
   if (abytes <= 0 || bbytes <= 0) return false;
@@ -32,7 +32,7 @@ bool grid_fits(int64_t M, int64_t N) { return ((M + 15) / 16) * ((N + 15) / 16) 
 int hip_status(hipError_t e) { return e == hipSuccess ? MCF_OK : MCF_E_HIP; }
 
 int check_common(int dtype, int nc, int64_t n) {
-  if (dtype != MCF_F16 && dtype != MCF_F32) return MCF_E_DTYPE;
+  if (dtype != MCF_F16 && dtype != MCF_F32 && dtype != MCF_F64) return MCF_E_DTYPE;
   if (nc < 1 || nc > MAX_NC) return MCF_E_NC;
   if (n < 0) return MCF_E_SHAPE;
   // plane offsets c * n stay far below 2^62 elements
@@ -57,7 +57,7 @@ int binary_op(int op, int dtype, int nc, int64_t n, const void *x, int x_mc, con
 // (the default for slices <= 0, capped at K).
 int splitk_check(int dtype, int nc, int64_t M, int64_t N, int64_t K, int a_mc, int b_mc, int64_t slices,
                  int64_t *S) {
-  if (dtype != MCF_F16 && dtype != MCF_F32) return MCF_E_DTYPE;
+  if (dtype != MCF_F16 && dtype != MCF_F32 && dtype != MCF_F64) return MCF_E_DTYPE;
   if (nc < 1 || nc > MAX_NC) return MCF_E_NC;
   if ((a_mc != 0 && a_mc != 1) || (b_mc != 0 && b_mc != 1) || (!a_mc && !b_mc)) return MCF_E_ARG;
   if (M < 0 || N < 0 || K < 0) return MCF_E_SHAPE;
@@ -94,7 +94,7 @@ int exact_check(int dtype, int nc, int64_t M, int64_t N, int64_t K, int a_mc, in
 }
 
 int linreg_check(int dtype, int nc, int64_t n, int64_t d) {
-  if (dtype != MCF_F16 && dtype != MCF_F32) return MCF_E_DTYPE;
+  if (dtype != MCF_F16 && dtype != MCF_F32 && dtype != MCF_F64) return MCF_E_DTYPE;
   if (nc < 1 || nc > MAX_NC) return MCF_E_NC;
   if (n < 1 || d < 1) return MCF_E_SHAPE;
   // X has n d elements; the sequential product's grid covers n rows, the K-split
@@ -106,6 +106,7 @@ int linreg_check(int dtype, int nc, int64_t n, int64_t d) {
 // The component-format rounding of a binary64 value.
 double round_to_format(int dtype, double v) {
   if (dtype == MCF_F16) return (double)(_Float16)v;
+  if (dtype == MCF_F64) return v;
   return (double)(float)v;
 }
 
@@ -149,6 +150,7 @@ int mc_exp(int dtype, int nc, int64_t n, const void *x, void *out, void *stream)
   if (n == 0) return MCF_OK;
   if (!x || !out) return MCF_E_NULL;
   const int64_t b = nc * n * elem_size(dtype);
+  if (dtype == MCF_F64) return MCF_E_DTYPE;  // no correctly rounded binary64 component exponential
   if (bad_alias(out, b, x, b)) return MCF_E_ALIAS;
   if (dtype == MCF_F16) return hip_status(mcf::launch_exp_f16(nc, n, x, out, (hipStream_t)stream));
   return hip_status(mcf::launch_exp_f32(nc, n, x, out, (hipStream_t)stream));
@@ -169,7 +171,7 @@ int mc_renorm(int dtype, int nc_in, int nc_out, int64_t n, const void *x, void *
 
 int mc_matmul(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B,
               int b_mc, void *C, void *stream) {
-  if (dtype != MCF_F16 && dtype != MCF_F32) return MCF_E_DTYPE;
+  if (dtype != MCF_F16 && dtype != MCF_F32 && dtype != MCF_F64) return MCF_E_DTYPE;
   if (nc < 1 || nc > MAX_NC) return MCF_E_NC;
   if ((a_mc != 0 && a_mc != 1) || (b_mc != 0 && b_mc != 1) || (!a_mc && !b_mc)) return MCF_E_ARG;
   if (M < 0 || N < 0 || K < 0) return MCF_E_SHAPE;
@@ -186,7 +188,7 @@ int mc_matmul(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A,
 
 int mc_matmul_pruned(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, const void *B, void *C,
                      void *stream) {
-  if (dtype != MCF_F16 && dtype != MCF_F32) return MCF_E_DTYPE;
+  if (dtype != MCF_F16 && dtype != MCF_F32 && dtype != MCF_F64) return MCF_E_DTYPE;
   if (nc < 1 || nc > MAX_NC) return MCF_E_NC;
   if (M < 0 || N < 0 || K < 0) return MCF_E_SHAPE;
   if (M > ((int64_t)1 << 20) || N > ((int64_t)1 << 30) || K > ((int64_t)1 << 40)) return MCF_E_SHAPE;
@@ -214,7 +216,7 @@ int mc_matmul_pruned(int dtype, int nc, int64_t M, int64_t N, int64_t K, const v
 int mc_matmul_batched(int dtype, int nc, int64_t B1, int64_t B2, int64_t M, int64_t N, int64_t K, const void *A,
                       int a_mc, int64_t a_plane, int64_t a_s1, int64_t a_s2, const void *B, int b_mc,
                       int64_t b_plane, int64_t b_s1, int64_t b_s2, void *C, void *stream) {
-  if (dtype != MCF_F16 && dtype != MCF_F32) return MCF_E_DTYPE;
+  if (dtype != MCF_F16 && dtype != MCF_F32 && dtype != MCF_F64) return MCF_E_DTYPE;
   if (nc < 1 || nc > MAX_NC) return MCF_E_NC;
   if ((a_mc != 0 && a_mc != 1) || (b_mc != 0 && b_mc != 1) || (!a_mc && !b_mc)) return MCF_E_ARG;
   if (M < 0 || N < 0 || K < 0 || B1 < 0 || B2 < 0) return MCF_E_SHAPE;
@@ -259,7 +261,7 @@ int mc_matmul_batched(int dtype, int nc, int64_t B1, int64_t B2, int64_t M, int6
 
 int mc_addmm(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B, int b_mc,
              const void *Y, int64_t y_rows, double alpha, double beta, void *C, void *stream) {
-  if (dtype != MCF_F16 && dtype != MCF_F32) return MCF_E_DTYPE;
+  if (dtype != MCF_F16 && dtype != MCF_F32 && dtype != MCF_F64) return MCF_E_DTYPE;
   if (nc < 1 || nc > MAX_NC) return MCF_E_NC;
   if ((a_mc != 0 && a_mc != 1) || (b_mc != 0 && b_mc != 1) || (!a_mc && !b_mc)) return MCF_E_ARG;
   if (M < 0 || N < 0 || K < 0) return MCF_E_SHAPE;
@@ -267,8 +269,9 @@ int mc_addmm(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, 
   if (!grid_fits(M, N)) return MCF_E_SHAPE;
   if (y_rows != M && y_rows != 1) return MCF_E_SHAPE;
   // the scalars must be values of the component format
-  const bool exact = dtype == MCF_F32 ? (double)(float)alpha == alpha && (double)(float)beta == beta
-                                      : (double)(_Float16)alpha == alpha && (double)(_Float16)beta == beta;
+  const bool exact = dtype == MCF_F64   ? true
+                     : dtype == MCF_F32 ? (double)(float)alpha == alpha && (double)(float)beta == beta
+                                        : (double)(_Float16)alpha == alpha && (double)(_Float16)beta == beta;
   if (!exact) return MCF_E_ARG;
   if (M == 0 || N == 0) return MCF_OK;
   if (!C || !Y || (K > 0 && (!A || !B))) return MCF_E_NULL;
@@ -386,7 +389,7 @@ int mc_linreg_gd_step(int dtype, int nc, int64_t n, int64_t d, const void *X, co
 
 int mc_linear_fwd(int dtype, int nc, int64_t batch, int64_t in, int64_t out, const void *x, const void *W,
                   const void *b, void *y, void *stream) {
-  if (dtype != MCF_F16 && dtype != MCF_F32) return MCF_E_DTYPE;
+  if (dtype != MCF_F16 && dtype != MCF_F32 && dtype != MCF_F64) return MCF_E_DTYPE;
   if (nc < 1 || nc > MAX_NC) return MCF_E_NC;
   if (batch < 0 || in < 0 || out < 0) return MCF_E_SHAPE;
   if (batch > ((int64_t)1 << 20) || out > ((int64_t)1 << 30) || in > ((int64_t)1 << 40)) return MCF_E_SHAPE;

@@ -263,6 +263,7 @@ static hipError_t ew_dispatch(int op, int nc, int nc_out, int64_t n, const void 
 hipError_t launch_elementwise(int dtype, int op, int nc, int nc_out, int64_t n, const void *x, int x_mc,
                               const void *y, int y_mc, void *out, hipStream_t stream) {
   if (dtype == 0) return ew_dispatch<_Float16>(op, nc, nc_out, n, x, x_mc, y, y_mc, out, stream);
+  if (dtype == 2) return ew_dispatch<double>(op, nc, nc_out, n, x, x_mc, y, y_mc, out, stream);
   return ew_dispatch<float>(op, nc, nc_out, n, x, x_mc, y, y_mc, out, stream);
 }
 

@@ -74,7 +74,7 @@ struct LrLayout {
 };
 
 LrLayout lr_layout(int dtype, int nc, int64_t n, int64_t d) {
-  const int64_t es = dtype == 0 ? 2 : 4;
+  const int64_t es = dtype == 0 ? 2 : (dtype == 2 ? 8 : 4);
   LrLayout L;
   L.r = 0;
   L.g = align256(nc * n * es);
@@ -110,6 +110,7 @@ hipError_t launch_linreg_step(int dtype, int nc, int64_t n, int64_t d, const voi
   if (dtype == 0)
     return lr_update<_Float16>(nc, G, RR, W, d, (_Float16)(float)s2n, (_Float16)(float)s1n, (_Float16)(float)neg_lr,
                                loss, s);
+  if (dtype == 2) return lr_update<double>(nc, G, RR, W, d, s2n, s1n, neg_lr, loss, s);
   return lr_update<float>(nc, G, RR, W, d, (float)s2n, (float)s1n, (float)neg_lr, loss, s);
 }
 

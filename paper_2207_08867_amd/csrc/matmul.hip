@@ -422,7 +422,7 @@ struct MmArgs {
 // and one register more would drop them to 4.  nc = 4 needs more registers.
 template <typename T, int NC, bool AMC, bool BMC, bool BT, int TM, int TN, int KT, int SPOL, int APOL,
           bool GROUP, bool ADDMM, bool PRUNE>
-__global__ __attribute__((amdgpu_flat_work_group_size(1, MM_THREADS), amdgpu_waves_per_eu(NC <= 3 ? 5 : 1))) void
+__global__ __attribute__((amdgpu_flat_work_group_size(1, MM_THREADS), amdgpu_waves_per_eu(NC <= 3 && sizeof(T) <= 4 ? 5 : 1))) void
 mm_kernel(const T *__restrict__ A, const T *__restrict__ B,
                                                         T *__restrict__ C, const MmArgs<T> g) {
   const int64_t M = g.M, N = g.N, K = g.K;
@@ -661,7 +661,9 @@ static hipError_t mm_launch_tile(MmArgs<T> g, int64_t batches, const void *A, co
 template <typename T, int NC, bool AMC, bool BMC, bool BT, bool PRUNE = false>
 static hipError_t mm_launch(const MmArgs<T> &g, int64_t batches, const void *A, const void *B, void *C,
                             hipStream_t s) {
-  if constexpr (sizeof(T) == 4) {
+  if constexpr (sizeof(T) == 8) {  // binary64: as binary32, one output per lane (twice the registers)
+    return mm_launch_tile<T, NC, AMC, BMC, BT, 1, 1, SR_FULL, SR_FULL, 16, PRUNE>(g, batches, A, B, C, s);
+  } else if constexpr (sizeof(T) == 4) {
     if (g.M * g.N >= ((int64_t)1 << 25))
       return mm_launch_tile<T, NC, AMC, BMC, BT, 1, 2, SR_FULL, SR_FULL, 16, PRUNE>(g, batches, A, B, C, s);
     return mm_launch_tile<T, NC, AMC, BMC, BT, 1, 1, SR_FULL, SR_FULL, 16, PRUNE>(g, batches, A, B, C, s);
@@ -730,6 +732,7 @@ static hipError_t mm_typed(const MmLaunch &L, hipStream_t s) {
 
 hipError_t launch_matmul_general(const MmLaunch &L, hipStream_t stream) {
   if (L.dtype == 0) return mm_typed<_Float16>(L, stream);
+  if (L.dtype == 2) return mm_typed<double>(L, stream);
   return mm_typed<float>(L, stream);
 }
 

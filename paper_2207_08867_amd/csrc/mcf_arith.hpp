@@ -2,7 +2,7 @@
 //
 // Every function below follows one algorithm of "MCTensor" (arXiv 2207.08867),
 // Appendix A.2.1, step for step: each printed operation is one IEEE operation in the
-// component type T (binary16 `_Float16` or binary32 `float`), with round to nearest
+// component type T (binary16 `_Float16`, binary32 `float` or binary64 `double`), with round to nearest
 // even and gradual underflow.  The library is compiled with -ffp-contract=off so no
 // multiply-add is fused except the explicit FMA of Two-Prod.
 //
@@ -24,9 +24,13 @@ template <>
 __device__ __forceinline__ _Float16 fma_<_Float16>(_Float16 a, _Float16 b, _Float16 c) {
   return __builtin_fmaf16(a, b, c);
 }
+template <>
+__device__ __forceinline__ double fma_<double>(double a, double b, double c) {
+  return __builtin_fma(a, b, c);
+}
 
-// Correctly rounded component division.  binary32: IEEE division (HIP's default
-// division is correctly rounded).  binary16: the binary32 quotient of the exact
+// Correctly rounded component division.  binary32 and binary64: IEEE division (HIP's
+// default division is correctly rounded).  binary16: the binary32 quotient of the exact
 // binary16 operands, rounded to binary16; the double rounding is innocuous because
 // 24 >= 2*11 + 2.
 template <typename T>
@@ -38,6 +42,10 @@ __device__ __forceinline__ float div_<float>(float a, float b) {
 template <>
 __device__ __forceinline__ _Float16 div_<_Float16>(_Float16 a, _Float16 b) {
   return (_Float16)((float)a / (float)b);
+}
+template <>
+__device__ __forceinline__ double div_<double>(double a, double b) {
+  return a / b;
 }
 
 // Two-Sum: s = fl(a + b) and e = (a + b) - s exactly, the six printed operations.

@@ -51,6 +51,11 @@ __device__ __forceinline__ bool all_nonzero(const T (&v)[K]) {
   static_assert(K >= 1 && K <= 4, "");
   if constexpr (K == 1) {
     return v[0] != T(0);
+  } else if constexpr (sizeof(T) == 8) {  // binary64: a binary32 magnitude could underflow
+    bool nz = true;
+#pragma unroll
+    for (int i = 0; i < K; ++i) nz = nz & (v[i] != T(0));
+    return nz;
   } else if constexpr (K == 2) {
     return __builtin_fminf(__builtin_fabsf((float)v[0]), __builtin_fabsf((float)v[1])) != 0.0f;
   } else {
@@ -163,19 +168,24 @@ __device__ __forceinline__ void add_terms(const T (&x)[N], const T (&y)[N], T (&
 
 // 2^(emin+1): below it the spacing of the format is its smallest subnormal.
 template <typename T>
-__device__ __forceinline__ constexpr float exact_limit();
+__device__ __forceinline__ constexpr double exact_limit();
 template <>
-__device__ __forceinline__ constexpr float exact_limit<_Float16>() {
-  return 0x1p-13f;
+__device__ __forceinline__ constexpr double exact_limit<_Float16>() {
+  return 0x1p-13;
 }
 template <>
-__device__ __forceinline__ constexpr float exact_limit<float>() {
-  return 0x1p-125f;
+__device__ __forceinline__ constexpr double exact_limit<float>() {
+  return 0x1p-125;
+}
+template <>
+__device__ __forceinline__ constexpr double exact_limit<double>() {
+  return 0x1p-1021;
 }
 
 // |x| < lim, compared in the component format (one compare with an abs modifier).
 __device__ __forceinline__ bool abs_below(float x, float lim) { return __builtin_fabsf(x) < lim; }
 __device__ __forceinline__ bool abs_below(_Float16 x, _Float16 lim) { return __builtin_fabsf16(x) < lim; }
+__device__ __forceinline__ bool abs_below(double x, double lim) { return __builtin_fabs(x) < lim; }
 
 // h_0 .. h_{N-1} of ScalingN(x, v) and the last product hp = fl(x_{N-1} v).
 // HEAD_EXACT: the error of x_0 v is known to be zero; TAIL_EXACT: so are the errors

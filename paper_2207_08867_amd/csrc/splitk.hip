@@ -37,6 +37,7 @@ __device__ __forceinline__ float lane_down(float v, int d) { return __shfl_down(
 __device__ __forceinline__ _Float16 lane_down(_Float16 v, int d) {
   return (_Float16)__shfl_down((float)v, (unsigned)d, 64);
 }
+__device__ __forceinline__ double lane_down(double v, int d) { return __shfl_down(v, (unsigned)d, 64); }
 
 // Pairwise Add-MCN tree over groups of W lanes (W a power of two, W <= 256): lane q
 // of a group holds leaf q, and leaves q >= count are absent.  At stride d the entry of
@@ -228,8 +229,8 @@ static hipError_t sk_launch(int64_t M, int64_t N, int64_t K, const void *A, cons
                             hipStream_t s) {
   constexpr int NP = (AMC && BMC) ? NC : 1;
   // Simple-Renorm fast-path policies as in the sequential product (they change speed only)
-  constexpr int SPOL = sizeof(T) == 4 ? SR_FULL : (NC == 2 ? SR_NET : SR_HEAD);
-  constexpr int APOL = sizeof(T) == 4 ? SR_FULL : SR_SELECT;
+  constexpr int SPOL = sizeof(T) >= 4 ? SR_FULL : (NC == 2 ? SR_NET : SR_HEAD);
+  constexpr int APOL = sizeof(T) >= 4 ? SR_FULL : SR_SELECT;
   const int64_t MN = M * N;
   int KS, G;
   splitk_shape(S, &KS, &G);
@@ -268,6 +269,7 @@ static hipError_t sk_dispatch(int nc, int64_t M, int64_t N, int64_t K, const voi
 hipError_t launch_matmul_splitk(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc,
                                 const void *B, int b_mc, int64_t S, void *W, void *C, hipStream_t stream) {
   if (dtype == 0) return sk_dispatch<_Float16>(nc, M, N, K, A, a_mc, B, b_mc, S, W, C, stream);
+  if (dtype == 2) return sk_dispatch<double>(nc, M, N, K, A, a_mc, B, b_mc, S, W, C, stream);
   return sk_dispatch<float>(nc, M, N, K, A, a_mc, B, b_mc, S, W, C, stream);
 }
 

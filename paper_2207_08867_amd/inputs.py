@@ -31,6 +31,22 @@ def split(x: np.ndarray, nc: int, dtype) -> np.ndarray:
     return out
 
 
+def expansion(g: np.random.Generator, shape, nc: int, dtype, scale: float = 1.0) -> np.ndarray:
+    """MC values with every component in use (for formats where splitting a float64
+    draw would leave the low components zero, such as binary64): c_0 ~ N(0, scale^2)
+    rounded to `dtype`, each later component a uniform draw within a quarter ulp of the
+    component before, rounded to `dtype`."""
+    dtype = np.dtype(dtype)
+    p = {np.dtype(np.float16): 11, np.dtype(np.float32): 24, np.dtype(np.float64): 53}[dtype]
+    out = np.zeros((nc,) + tuple(np.atleast_1d(shape)), dtype=dtype)
+    out[0] = g.normal(0.0, scale, out.shape[1:]).astype(dtype)
+    for c in range(1, nc):
+        prev = np.abs(out[c - 1].astype(np.float64))
+        ulp = np.exp2(np.floor(np.log2(np.where(prev > 0, prev, 1.0))) - (p - 1))
+        out[c] = np.where(prev > 0, g.uniform(-0.25, 0.25, out.shape[1:]) * ulp, 0.0).astype(dtype)
+    return out
+
+
 def rng(seed: int = 0) -> np.random.Generator:
     return np.random.default_rng(seed)
 

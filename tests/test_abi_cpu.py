@@ -50,7 +50,7 @@ def test_validation_elementwise(L):
     for f in (L.mc_add, L.mc_mul, L.mc_div):
         assert f(0, 0, 10, x, 1, y, 1, o, None) == MCF_E_NC
         assert f(0, 5, 10, x, 1, y, 1, o, None) == MCF_E_NC
-        assert f(2, 3, 10, x, 1, y, 1, o, None) == MCF_E_DTYPE
+        assert f(3, 3, 10, x, 1, y, 1, o, None) == MCF_E_DTYPE  # 3: no such format
         assert f(0, 3, -1, x, 1, y, 1, o, None) == MCF_E_SHAPE
         assert f(0, 3, 10, x, 0, y, 0, o, None) == MCF_E_ARG
         assert f(0, 3, 10, x, 2, y, 1, o, None) == MCF_E_ARG
@@ -60,7 +60,8 @@ def test_validation_elementwise(L):
         assert f(1, 3, 10, P(0x10000), 1, y, 1, P(0x10004), None) == MCF_E_ALIAS
         # out overlapping a plain y that is shorter than out
         assert f(1, 3, 10, x, 1, P(0x30000), 0, o, None) == MCF_E_ALIAS
-    assert L.mc_exp(2, 3, 10, x, o, None) == MCF_E_DTYPE
+    assert L.mc_exp(3, 3, 10, x, o, None) == MCF_E_DTYPE
+    assert L.mc_exp(2, 3, 10, x, o, None) == MCF_E_DTYPE  # binary64: no component exponential
     assert L.mc_exp(1, 3, 10, x, P(0x10004), None) == MCF_E_ALIAS
     assert L.mc_exp(0, 3, 0, None, None, None) == MCF_OK
     assert L.mc_renorm(0, 3, 4, 10, x, o, 0, None) == MCF_E_NC

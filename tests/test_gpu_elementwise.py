@@ -30,7 +30,7 @@ def assert_bits(got, want, what=""):
     got = np.asarray(got)
     want = np.asarray(want)
     assert got.shape == want.shape, (got.shape, want.shape)
-    u = np.uint16 if got.dtype == np.float16 else np.uint32
+    u = {2: np.uint16, 4: np.uint32, 8: np.uint64}[got.dtype.itemsize]
     gb, wb = got.view(u), want.view(u)
     nan = np.isnan(got.astype(np.float64)) & np.isnan(want.astype(np.float64))
     bad = (gb != wb) & ~nan
