@@ -19,7 +19,10 @@ Readings (the paper defines no such product; these are choices of this variant):
   * overflow: if |P| rounds beyond 65504 the result is (+-inf, 0, ..., 0);
   * non-finite inputs: an output whose row of A or column of B holds an infinite or
     NaN component is NaN in every component;
-  * an exact zero gives +0 in every component.
+  * an exact zero gives +0 in every component;
+  * with a bias row (the MC-Linear forward y = x W^T + b, Section 2.3), the bias is
+    added to the exact sum before the split, and a non-finite bias component makes
+    its column NaN.
 
 Exactness.  Every binary16 value is an integer multiple of 2^-24, so each MC entry
 is an integer X = sum_c x_c 2^24, and every product term is an integer in units of
@@ -117,11 +120,14 @@ def exact_sums(A, B, *, a_mc=True, b_mc=True):
     return P, row_bad, col_bad
 
 
-def matmul_exact(A, B, *, nc, a_mc=True, b_mc=True, rows=None, cols=None) -> np.ndarray:
+def matmul_exact(A, B, *, nc, a_mc=True, b_mc=True, rows=None, cols=None, bias=None) -> np.ndarray:
     """The exact product split into nc binary16 components.
 
-    A: (nc|1, M, K), B: (nc|1, K, N), binary16.  Returns (nc, M, N) binary16, or
-    (nc, count) at the given positions (rows, cols index arrays).
+    A: (nc|1, M, K), B: (nc|1, K, N), binary16; bias: optional (planes, N) binary16 MC
+    row added exactly to every row of the product before the split (the MC-Linear
+    forward y = x W^T + b).  Returns (nc, M, N) binary16, or (nc, count) at the given
+    positions (rows, cols index arrays).  An output whose bias column holds a
+    non-finite component is NaN in every component.
     """
     A = np.asarray(A, dtype=np.float16)
     B = np.asarray(B, dtype=np.float16)
@@ -132,17 +138,25 @@ def matmul_exact(A, B, *, nc, a_mc=True, b_mc=True, rows=None, cols=None) -> np.
     if A.shape[0] != (nc if a_mc else 1) or B.shape[0] != (nc if b_mc else 1) or A.shape[2] != B.shape[1]:
         raise ValueError("matmul_exact: shape mismatch")
     M, N = A.shape[1], B.shape[2]
+    # the bias column sums, in units of 2^-48, and their non-finite flags
+    bsum = [0] * N
+    bbad = [False] * N
+    if bias is not None:
+        bu = f16_units24(np.asarray(bias, dtype=np.float16).reshape(-1, N))
+        for j in range(N):
+            bbad[j] = any(v is None for v in bu[:, j])
+            bsum[j] = 0 if bbad[j] else sum(int(v) for v in bu[:, j]) << 24
     if rows is None:
         P, rb, cb = exact_sums(A, B)
         pos = [(i, j) for i in range(M) for j in range(N)]
-        vals = [(P[i, j], rb[i] or cb[j]) for i, j in pos]
+        vals = [(P[i, j] + bsum[j], rb[i] or cb[j] or bbad[j]) for i, j in pos]
     else:
         rows = np.asarray(rows, dtype=np.int64).ravel()
         cols = np.asarray(cols, dtype=np.int64).ravel()
         vals = []
         for i, j in zip(rows, cols):
             P, rb, cb = exact_sums(A[:, i:i + 1, :], B[:, :, j:j + 1])
-            vals.append((P[0, 0], bool(rb[0] or cb[0])))
+            vals.append((P[0, 0] + bsum[j], bool(rb[0] or cb[0] or bbad[j])))
     out = np.empty((nc, len(vals)), dtype=np.uint16)
     for t, (p, bad) in enumerate(vals):
         out[:, t] = [0x7E00] * nc if bad else split_units48(int(p), nc)

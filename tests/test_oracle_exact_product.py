@@ -197,3 +197,38 @@ def test_plain_operands():
     A1[1:] = 0
     got = xp.matmul_exact(A[:1], B, nc=3, a_mc=False)
     assert np.array_equal(got.view(np.uint16), xp.matmul_exact(A1, B, nc=3).view(np.uint16))
+
+
+@pytest.mark.parametrize("nc", [1, 2, 3])
+def test_bias_alone_returns_canonical_bias(nc):
+    """A = 0: the exact value is the bias itself, split back into its own components."""
+    g = np.random.default_rng(8)
+    b = canonical(g, (9,), nc)
+    A = np.zeros((nc, 4, 6), np.float16)
+    B = canonical(g, (6, 9), nc)
+    got = xp.matmul_exact(A, B, nc=nc, bias=b)
+    assert np.array_equal(got.view(np.uint16), np.broadcast_to(b[:, None, :], got.shape).view(np.uint16))
+
+
+@pytest.mark.parametrize("nc", [2, 3])
+def test_bias_is_an_extra_reduction_term(nc):
+    """x W^T + b equals the bias-free exact product of [A | 1] and [B ; b]."""
+    A, B = inputs.matmul_normal(5, 7, 11, nc, np.float16, seed=9)
+    b = inputs.split(np.random.default_rng(10).normal(0, 0.5, 7), nc, np.float16)
+    b[:, 2] = [np.float16(3000.0)] + [np.float16(0)] * (nc - 1)
+    A1 = np.concatenate([A, np.zeros((nc, 5, 1), np.float16)], axis=2)
+    A1[0, :, -1] = 1
+    B1 = np.concatenate([B, b[:, None, :]], axis=1)
+    got = xp.matmul_exact(A, B, nc=nc, bias=b)
+    assert np.array_equal(got.view(np.uint16), xp.matmul_exact(A1, B1, nc=nc).view(np.uint16))
+    r, c = np.array([0, 4, 2]), np.array([6, 2, 0])
+    assert np.array_equal(xp.matmul_exact(A, B, nc=nc, bias=b, rows=r, cols=c).view(np.uint16),
+                          got[:, r, c].view(np.uint16))
+
+
+def test_nonfinite_bias_column():
+    A, B = inputs.matmul_normal(3, 4, 5, 2, np.float16, seed=11)
+    b = np.zeros((2, 4), np.float16)
+    b[1, 3] = np.inf
+    got = xp.matmul_exact(A, B, nc=2, bias=b)
+    assert np.isnan(got[:, :, 3]).all() and not np.isnan(got[:, :, :3]).any()
