@@ -169,6 +169,20 @@ def exact_error(oracle, A, B, C, nc, K, dt, count=64, seed=5):
             "max_err_over_bound": float(np.max(np.abs(err) / lim)), "sampled_outputs": int(count)}
 
 
+def exact_error_bias(oracle, A, B, bias, C, nc, K, count=64, seed=5):
+    """exact_error for a product plus a bias row (the MC-Linear layer)."""
+    M, N = C.shape[1:]
+    g = np.random.default_rng(seed)
+    rows = g.integers(0, M, count)
+    cols = g.integers(0, N, count)
+    Cs = np.ascontiguousarray(C[:, rows, cols])
+    err, absab, _ = oracle.matmul_exact_err(A, B, Cs, bias=bias, rows=rows, cols=cols)
+    u = 2.0 ** -11
+    lim = 4 * K * u ** min(nc, 3) * absab + A.shape[0] * B.shape[0] * K * 2.0 ** -25
+    return {"max_rel_err": float((np.abs(err) / absab).max()), "bound_4Ku^nc": 4 * K * u ** nc,
+            "max_err_over_bound": float(np.max(np.abs(err) / lim)), "sampled_outputs": int(count)}
+
+
 def cpu_baseline(oracle, A, B, nc, target_s=12.0):
     """The oracle on a bounded sample of output entries of the headline product."""
     M, K = A.shape[1:]
@@ -346,13 +360,14 @@ def digit_levels(X16):
 
 def bench_exact(torch, mcf, oracle, inputs, steps=20):
     """The exact binary16 product (int8 matrix cores) on the 1024^3 MC x MC operands of
-    the binary16 MM-MCN lines and on one MC-Linear layer product x W^T."""
+    the binary16 MM-MCN lines, and the exact MC-Linear forward x W^T + b on one layer of
+    the MC-Linear workload."""
     out = {}
     cases = []
     for nc in (2, 3):
         A, B = inputs.matmul_normal(1024, 1024, 1024, nc, np.float16, seed=0)
         cases.append((f"matmul_exact_1024_f16_nc{nc}", A, B, nc, True, False))
-    x, W, _ = next(inputs.linear_inputs(4096, 1024, 1024, 3, np.float16, seed=0))
+    x, W, b = next(inputs.linear_inputs(4096, 1024, 1024, 3, np.float16, seed=0))
     cases.append(("linear_exact_4096x1024x1024_f16_nc3", x[None], W, 3, False, True))
     for name, A, B, nc, a_mc, b_trans in cases:
         tA, tB = torch.from_numpy(np.ascontiguousarray(A)).cuda(), torch.from_numpy(B).cuda()
@@ -360,8 +375,11 @@ def bench_exact(torch, mcf, oracle, inputs, steps=20):
         N = B.shape[1] if b_trans else B.shape[2]
         ws = torch.empty(mcf.mc_matmul_exact_workspace(nc, M, N, K), dtype=torch.uint8, device="cuda")
         C = torch.empty((nc, M, N), dtype=torch.float16, device="cuda")
-        run = lambda: mcf.mc_matmul_exact(tA if a_mc else tA[0], tB, nc=nc, a_mc=a_mc, b_trans=b_trans, out=C,
-                                          workspace=ws)
+        if b_trans:  # the MC-Linear layer y = x W^T + b (bias added to the exact sum)
+            tb = torch.from_numpy(b).cuda()
+            run = lambda: mcf.mc_linear_fwd_exact(tA[0], tB, tb, out=C, workspace=ws)
+        else:
+            run = lambda: mcf.mc_matmul_exact(tA, tB, nc=nc, out=C, workspace=ws)
         for _ in range(3):
             run()
         torch.cuda.synchronize()
@@ -373,10 +391,12 @@ def bench_exact(torch, mcf, oracle, inputs, steps=20):
         la, lb = digit_levels(A), digit_levels(Bm)
         pairs = (la[1] - la[0]) * (lb[1] - lb[0])
         ops = 2.0 * M * N * K * pairs
+        Ch = C.cpu().numpy()
+        err = (exact_error(oracle, A, Bm, Ch, nc, K, np.float16) if not b_trans else
+               exact_error_bias(oracle, A, Bm, b, Ch, nc, K))
         out[name] = {"us": round(us, 1), "MC-GFLOP/s": round(2.0 * M * N * K / (us * 1e-6) / 1e9, 1),
                      "digit_pairs": pairs, "int8_ops": ops,
-                     "mfma_int8_frac_whole_call": round(ops / (us * 1e-6) / MFMA_I8_PEAK, 4),
-                     "error": exact_error(oracle, A, Bm, C.cpu().numpy(), nc, K, np.float16)}
+                     "mfma_int8_frac_whole_call": round(ops / (us * 1e-6) / MFMA_I8_PEAK, 4), "error": err}
         log(f"  {name}: {us:.1f} us ({pairs} digit pairs)")
         del tA, tB, ws, C
     return out

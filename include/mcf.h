@@ -235,6 +235,19 @@ int64_t mc_matmul_splitk_workspace(int dtype, int nc, int64_t M, int64_t N, int6
 int mc_matmul_exact(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B,
                     int b_mc, int b_trans, void *workspace, int64_t workspace_bytes, void *C, void *stream);
 
+/* Exact MC-Linear forward for binary16 components: y = x W^T + b with the exact value
+ * of every output (x plain, W and b MC; Section 2.3's layer) split into nc components
+ * by successive rounding, as mc_matmul_exact -- the bias is added to the exact sum
+ * before the split.  An output whose column of W or bias holds an infinite or NaN
+ * component, or whose row of x does, is NaN in every component.
+ * x: [batch][in] (plain), W: [nc][out][in], b: [nc][out] or NULL, y: [nc][batch][out]
+ * (not overlapping x, W, b or the workspace).
+ * workspace: as mc_matmul_exact, at least mc_matmul_exact_workspace(dtype, nc, batch,
+ *   out, in) bytes.  dtype: MCF_F16 only.  Sizes as mc_matmul_exact with M = batch,
+ *   N = out, K = in. */
+int mc_linear_fwd_exact(int dtype, int nc, int64_t batch, int64_t in, int64_t out, const void *x, const void *W,
+                        const void *b, void *workspace, int64_t workspace_bytes, void *y, void *stream);
+
 /* Workspace bytes mc_matmul_exact needs (about 6 (M + N) K bytes of digit planes,
  * plus 16 M N ceil(K / 16384) bytes of partial sums when K > 16384), or a negative
  * mcf_status for

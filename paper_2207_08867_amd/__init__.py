@@ -21,7 +21,8 @@ __all__ = [
     "mc_add", "mc_mul", "mc_div", "mc_exp", "mc_renorm", "mc_matmul", "mc_matmul_splitk",
     "mc_matmul_splitk_slices", "mc_matmul_splitk_workspace", "mc_linear_fwd", "mc_status_str",
     "mc_matmul_batched", "mc_bmm", "mc_addmm", "matmul_mcn", "mc_mul_slow", "mc_square", "mc_matmul_pruned",
-    "mc_matmul_exact", "mc_matmul_exact_workspace", "mc_linreg_workspace", "mc_linreg_gd_step", "lib", "LIB_PATH", "MCFError",
+    "mc_matmul_exact", "mc_matmul_exact_workspace", "mc_linreg_workspace", "mc_linreg_gd_step",
+    "mc_linear_fwd_exact", "lib", "LIB_PATH", "MCFError",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmcf.so")
@@ -73,6 +74,8 @@ def lib() -> ctypes.CDLL:
                                vp, vp]
         L.mc_matmul_exact.restype = ci
         L.mc_matmul_exact.argtypes = [ci, ci, i64, i64, i64, vp, ci, vp, ci, ci, vp, i64, vp, vp]
+        L.mc_linear_fwd_exact.restype = ci
+        L.mc_linear_fwd_exact.argtypes = [ci, ci, i64, i64, i64, vp, vp, vp, vp, i64, vp, vp]
         L.mc_matmul_exact_workspace.restype = i64
         L.mc_matmul_exact_workspace.argtypes = [ci, ci, i64, i64, i64]
         L.mc_linreg_workspace.restype = i64
@@ -370,6 +373,31 @@ def mc_linreg_gd_step(X, y_neg, W, lr: float, *, loss=None, workspace=None):
                                  None if loss is None else _dev(loss, "loss"), _stream(W))
     _check(st, "mc_linreg_gd_step")
     return W
+
+
+def mc_linear_fwd_exact(x, W, b=None, *, out=None, workspace=None):
+    """Exact MC-Linear forward y = x W^T + b for binary16 components (int8 matrix
+    cores): the exact value of every output split into nc components by successive
+    rounding.  x: (batch, in) plain, W: (nc, out, in), b: (nc, out) or None ->
+    y: (nc, batch, out)."""
+    torch = _torch()
+    nc, O, I = W.shape
+    if x.dim() != 2 or x.shape[1] != I:
+        raise ValueError("x must be (batch, in)")
+    if x.dtype != W.dtype or (b is not None and (b.dtype != W.dtype or tuple(b.shape) != (nc, O))):
+        raise ValueError("dtype or bias shape mismatch")
+    T = x.shape[0]
+    if out is None:
+        out = torch.empty((nc, T, O), dtype=W.dtype, device=W.device)
+    elif tuple(out.shape) != (nc, T, O) or out.dtype != W.dtype:
+        raise ValueError("out has the wrong shape or dtype")
+    if workspace is None:
+        workspace = torch.empty(max(mc_matmul_exact_workspace(nc, T, O, I), 1), dtype=torch.uint8, device=W.device)
+    st = lib().mc_linear_fwd_exact(_dtype_code(W), nc, T, I, O, _dev(x, "x"), _dev(W, "W"),
+                                   None if b is None else _dev(b, "b"), _dev(workspace, "workspace"),
+                                   workspace.numel() * workspace.element_size(), _dev(out, "out"), _stream(W))
+    _check(st, "mc_linear_fwd_exact")
+    return out
 
 
 def mc_linear_fwd(x, W, b=None, *, out=None):

@@ -358,7 +358,24 @@ int mc_matmul_exact(int dtype, int nc, int64_t M, int64_t N, int64_t K, const vo
   if (overlap(workspace, wb, A, ab) || overlap(workspace, wb, B, bb) || overlap(workspace, wb, C, cb))
     return MCF_E_ALIAS;
   return hip_status(
-      mcf::launch_matmul_exact(nc, M, N, K, A, a_mc, B, b_mc, b_trans, workspace, C, (hipStream_t)stream));
+      mcf::launch_matmul_exact(nc, M, N, K, A, a_mc, B, b_mc, b_trans, nullptr, workspace, C, (hipStream_t)stream));
+}
+
+int mc_linear_fwd_exact(int dtype, int nc, int64_t batch, int64_t in, int64_t out, const void *x, const void *W,
+                        const void *b, void *workspace, int64_t workspace_bytes, void *y, void *stream) {
+  int st = exact_check(dtype, nc, batch, out, in, 0, 1, 1);
+  if (st != MCF_OK) return st;
+  if (batch == 0 || out == 0) return MCF_OK;
+  if (!y || !workspace || (in > 0 && (!x || !W))) return MCF_E_NULL;
+  const int64_t wb = mcf::exact_workspace_bytes(batch, out, in);
+  if (workspace_bytes < wb) return MCF_E_ARG;
+  const int64_t yb = nc * batch * out * 2, xb = batch * in * 2, Wb = nc * out * in * 2, bb = nc * out * 2;
+  if (overlap(y, yb, x, xb) || overlap(y, yb, W, Wb) || (b && overlap(y, yb, b, bb))) return MCF_E_ALIAS;
+  if (overlap(workspace, wb, x, xb) || overlap(workspace, wb, W, Wb) || overlap(workspace, wb, y, yb) ||
+      (b && overlap(workspace, wb, b, bb)))
+    return MCF_E_ALIAS;
+  return hip_status(
+      mcf::launch_matmul_exact(nc, batch, out, in, x, 0, W, 1, 1, b, workspace, y, (hipStream_t)stream));
 }
 
 int64_t mc_linreg_workspace(int dtype, int nc, int64_t n, int64_t d) {

@@ -282,6 +282,7 @@ struct XmArgs {
   int nc;
   uint16_t *C;       // [nc][M][N]
   int cvec;          // rows of C may be written 16 bytes at a time (N % 8 == 0, C aligned)
+  const uint16_t *bias;  // [nc][N] MC row added to every output row, or null
   i128 *partial;     // [S][M][N] when the code path that runs needs S > 1 chunks
   int64_t tiles_n;   // workgroup tiles along N
 };
@@ -321,6 +322,19 @@ __device__ __forceinline__ XLevels x_levels(const uint32_t *stats) {
   return v;
 }
 
+// The bias of column col as an exact integer in units of 2^-24 (0 without a bias);
+// bad is set when one of its components is infinite or NaN.
+__device__ __forceinline__ int64_t bias_units(const XmArgs &g, int64_t col, bool &bad) {
+  if (g.bias == nullptr) return 0;
+  int64_t X = 0;
+  for (int c = 0; c < g.nc; ++c) {
+    const uint32_t b = g.bias[c * g.N + col];
+    if (f16_nonfinite(b)) bad = true;
+    else X += f16_units(b);
+  }
+  return X;
+}
+
 // Branch-free rounding for |rem| < 2^62 (which cannot overflow binary16): as
 // take_f16 with the sign folded in by two's-complement identities.
 __device__ __forceinline__ uint32_t take_f16_fast(int64_t &rem) {
@@ -346,20 +360,32 @@ __device__ __forceinline__ void xm_epilogue(const XmArgs &g, const XLevels &lv, 
                                             int64_t row0, int64_t col0, int64_t chunk, int64_t S, uint16_t *st) {
   constexpr int NCLS = 2 * DM - 1;
   const int lane = threadIdx.x % 64;
-  // V = sum_q acc[q] 256^q 2^shift0 exactly.  First a conservative test that every
-  // value of the wavefront stays below 2^62 in magnitude: each term is below
-  // 2^(bitlen|acc[q]| + 8 q + shift0) and there are at most 11 terms.  Then, when it
+  // V = sum_q acc[q] 256^q 2^shift0 (+ bias 2^24) exactly.  First a conservative test
+  // that every value of the wavefront stays below 2^62 in magnitude: each term is below
+  // 2^(bitlen|acc[q]| + 8 q + shift0) and there are at most 12 terms.  Then, when it
   // holds, V is summed in wrapping 64-bit arithmetic, which is exact because the true
   // sum fits; otherwise in 128-bit integers.
   const int shift0 = 8 * (lv.loA + lv.loB);
   bool fits = true;
+  // each lane's columns: their bias (units of 2^-24, added 24 bits up) joins the sum
+  int64_t bu[WTC];
+  int bhb[WTC];
+#pragma unroll
+  for (int c = 0; c < WTC; ++c) {
+    const int64_t col = col0 + 16 * c + lane % 16;
+    bool bb = false;
+    bu[c] = col < g.N ? bias_units(g, col, bb) : 0;
+    fits = fits && !bb;
+    const uint64_t ab = (uint64_t)(bu[c] < 0 ? -bu[c] : bu[c]);
+    bhb[c] = ab ? 64 - __builtin_clzll(ab) + 24 : 0;
+  }
 #pragma unroll
   for (int r = 0; r < WTR; ++r)
 #pragma unroll
     for (int c = 0; c < WTC; ++c)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        int hb = 0;
+        int hb = bhb[c];
 #pragma unroll
         for (int q = 0; q < NCLS; ++q) {
           const int32_t x = acc[q][r][c][i];
@@ -382,7 +408,7 @@ __device__ __forceinline__ void xm_epilogue(const XmArgs &g, const XLevels &lv, 
       for (int c = 0; c < WTC; ++c)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          uint64_t vu = 0;
+          uint64_t vu = (uint64_t)bu[c] << 24;
 #pragma unroll
           for (int q = 0; q < NCLS; ++q) {
             const int sh = 8 * q + shift0;
@@ -448,8 +474,13 @@ __device__ __forceinline__ void xm_epilogue(const XmArgs &g, const XLevels &lv, 
 #pragma unroll
           for (int q = 0; q < NG; ++q) Vu += (u128)(i128)part[q] << (32 * q);
           const i128 V = (i128)(Vu << shift0);
-          if (S > 1) g.partial[chunk * MN + idx] = V;
-          else store_split(V, g.nc, g.bad_a[row] | g.bad_b[col], g.C, MN, idx);
+          if (S > 1) {
+            g.partial[chunk * MN + idx] = V;  // the bias joins in the finishing kernel
+          } else {
+            bool bb = false;
+            const int64_t b = bias_units(g, col, bb);
+            store_split(V + (i128)((u128)(i128)b << 24), g.nc, g.bad_a[row] | g.bad_b[col] | bb, g.C, MN, idx);
+          }
         }
       }
     }
@@ -619,7 +650,9 @@ __global__ void xm_finish(XmArgs g) {
   i128 V = 0;
   for (int64_t s = 0; s < S; ++s) V += g.partial[s * MN + t];
   const int64_t row = t / g.N, col = t - row * g.N;
-  store_split(V, g.nc, g.bad_a[row] | g.bad_b[col], g.C, MN, t);
+  bool bb = false;
+  const int64_t b = bias_units(g, col, bb);
+  store_split(V + (i128)((u128)(i128)b << 24), g.nc, g.bad_a[row] | g.bad_b[col] | bb, g.C, MN, t);
 }
 
 int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
@@ -657,7 +690,7 @@ XLayout x_layout(int64_t M, int64_t N, int64_t K) {
 int64_t exact_workspace_bytes(int64_t M, int64_t N, int64_t K) { return x_layout(M, N, K).total; }
 
 hipError_t launch_matmul_exact(int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B,
-                               int b_mc, int b_trans, void *W, void *C, hipStream_t stream) {
+                               int b_mc, int b_trans, const void *bias, void *W, void *C, hipStream_t stream) {
   const XLayout L = x_layout(M, N, K);
   char *w = (char *)W;
   uint32_t *stats = (uint32_t *)(w + L.off_stats);
@@ -716,6 +749,7 @@ hipError_t launch_matmul_exact(int nc, int64_t M, int64_t N, int64_t K, const vo
   g.nc = nc;
   g.C = (uint16_t *)C;
   g.cvec = (N % 8 == 0) && ((uintptr_t)C % 16 == 0);
+  g.bias = (const uint16_t *)bias;
   g.partial = (i128 *)(w + L.off_part);
   {
     g.tiles_n = L.Np / 64;

@@ -61,10 +61,11 @@ hipError_t launch_matmul_splitk(int dtype, int nc, int64_t M, int64_t N, int64_t
                                 const void *B, int b_mc, int64_t S, void *W, void *C, hipStream_t stream);
 
 // Exact binary16 product on the int8 matrix cores (exact.hip).  b_trans: B stored as
-// [planes][N][K].  W: a workspace of exact_workspace_bytes(M, N, K) bytes.
+// [planes][N][K].  bias: [nc][N] MC row added exactly before the split, or null.  W: a
+// workspace of exact_workspace_bytes(M, N, K) bytes.
 int64_t exact_workspace_bytes(int64_t M, int64_t N, int64_t K);
 hipError_t launch_matmul_exact(int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B,
-                               int b_mc, int b_trans, void *W, void *C, hipStream_t stream);
+                               int b_mc, int b_trans, const void *bias, void *W, void *C, hipStream_t stream);
 
 // One gradient-descent step of MC-Linear regression (linreg.hip).  s2n, s1n and neg_lr
 // are fl(2/n), fl(1/n) and fl(-lr), already values of the component format.  ws holds

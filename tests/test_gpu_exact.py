@@ -187,3 +187,32 @@ def test_exact_argument_errors(mcf):
     B = B.half()
     with pytest.raises(ValueError):  # workspace too small
         mcf.mc_matmul_exact(A, B, nc=2, workspace=torch.empty(16, dtype=torch.uint8, device="cuda"))
+
+
+@pytest.mark.parametrize("nc", [1, 2, 3])
+def test_exact_linear_with_bias(mcf, nc):
+    """mc_linear_fwd_exact: y = x W^T + b, the bias added to the exact sum."""
+    T, I, O = 70, 37, 45
+    g = np.random.default_rng(3100 + nc)
+    x = g.normal(0, 1, (T, I)).astype(np.float16)
+    W = inputs.split(g.uniform(-1 / np.sqrt(I), 1 / np.sqrt(I), (O, I)), nc, np.float16)
+    b = inputs.split(g.uniform(-1 / np.sqrt(I), 1 / np.sqrt(I), O), nc, np.float16)
+    WT = np.ascontiguousarray(np.swapaxes(W, 1, 2))
+    got = to_host(mcf.mc_linear_fwd_exact(to_dev(x), to_dev(W), to_dev(b)))
+    assert_bits(got, xp.matmul_exact(x[None], WT, nc=nc, a_mc=False, bias=b), f"linear exact nc={nc}")
+    got = to_host(mcf.mc_linear_fwd_exact(to_dev(x), to_dev(W)))
+    assert_bits(got, xp.matmul_exact(x[None], WT, nc=nc, a_mc=False), f"linear exact no bias nc={nc}")
+    b[nc - 1, 7] = np.nan
+    got = to_host(mcf.mc_linear_fwd_exact(to_dev(x), to_dev(W), to_dev(b)))
+    assert np.isnan(got[:, :, 7]).all() and not np.isnan(np.delete(got, 7, axis=2)).any()
+
+
+def test_exact_linear_layer_with_bias_sampled(mcf):
+    """The MC-Linear layer y = x W^T + b at 4096 x 1024 x 1024, binary16 nc = 3."""
+    nc = 3
+    X, W, b = next(inputs.linear_inputs(4096, 1024, 1024, nc, np.float16, seed=3200))
+    got = to_host(mcf.mc_linear_fwd_exact(to_dev(X), to_dev(W), to_dev(b)))
+    r, c = sample_positions(4096, 1024, 60, 3201)
+    WT = np.ascontiguousarray(np.swapaxes(W, 1, 2))
+    assert_bits(got[:, r, c], xp.matmul_exact(X[None], WT, nc=nc, a_mc=False, bias=b, rows=r, cols=c),
+                "linear 4096x1024x1024 with bias")
