@@ -183,6 +183,33 @@ def exact_error_bias(oracle, A, B, bias, C, nc, K, count=64, seed=5):
             "max_err_over_bound": float(np.max(np.abs(err) / lim)), "sampled_outputs": int(count)}
 
 
+def cpu_oracle_other(oracle, inputs):
+    """The CPU oracle on bounded samples of the other workloads, for context beside the
+    GPU lines: binary16 nc = 3 elementwise operations on 2^22 elements, and 32 full rows
+    of the 1024^3 binary16 nc = 3 MC x MC product."""
+    out = {"threads": oracle.threads()}
+    n, nc = 1 << 22, 3
+    s = inputs.elementwise_suite(n, nc, np.float16, seed=0)
+    for name, fn, bpe in (("add_mcn", lambda: oracle.add(s["a"], s["b"], nc=nc), 18),
+                          ("div_mcn", lambda: oracle.div(s["a"], s["d"], nc=nc), 18),
+                          ("mult_mcn", lambda: oracle.mul(s["a"], s["d"], nc=nc), 18),
+                          ("exp_mcn", lambda: oracle.exp(s["e"], nc=nc), 12)):
+        t0 = time.perf_counter()
+        fn()
+        dt = time.perf_counter() - t0
+        out[name] = {"Melem/s": round(n / dt / 1e6, 2), "GB/s": round(bpe * n / dt / 1e9, 3),
+                     "sample": "2^22 elements, binary16 nc = 3", "seconds": round(dt, 3)}
+    A, B = inputs.matmul_normal(1024, 1024, 1024, nc, np.float16, seed=0)
+    rows = np.repeat(np.arange(32), 1024)
+    cols = np.tile(np.arange(1024), 32)
+    t0 = time.perf_counter()
+    oracle.matmul(A, B, nc=nc, rows=rows, cols=cols)
+    dt = time.perf_counter() - t0
+    out["matmul_1024_f16_nc3"] = {"MC-GFLOP/s": round(2.0 * rows.size * 1024 / dt / 1e9, 5),
+                                  "sample": "32 full rows (32768 outputs, K = 1024)", "seconds": round(dt, 3)}
+    return out
+
+
 def cpu_baseline(oracle, A, B, nc, target_s=12.0):
     """The oracle on a bounded sample of output entries of the headline product."""
     M, K = A.shape[1:]
@@ -218,7 +245,8 @@ def bench_elementwise(torch, mcf, inputs, steps=10):
         "div_mcn": (lambda: mcf.mc_div(dev["a"], dev["d"], nc=nc, out=out), 18),
         "exp_mcn": (lambda: mcf.mc_exp(dev["e"], nc=nc, out=out), 12),
         "renormalize": (lambda: mcf.mc_renorm(dev["a"], mode=0, out=out), 12),
-        "square_mcn": (lambda: mcf.mc_square(dev["a"], nc=nc, out=out), 12),
+        # Square-MCN depends on the two leading components only: 4 bytes read, 6 written
+        "square_mcn": (lambda: mcf.mc_square(dev["a"], nc=nc, out=out), 10),
         "mult_mcn_slow": (lambda: mcf.mc_mul_slow(dev["a"], dev["d"], nc=nc, out=out), 18),
     }
     # binary32 Exp-MCN (correctly rounded component exponential), same input recipe
@@ -237,9 +265,9 @@ def bench_elementwise(torch, mcf, inputs, steps=10):
         res[name] = {"us": round(ms * 1e3, 1), "GB/s": round(gbs, 1), "hbm_frac": round(gbs * 1e9 / HBM_PEAK, 3),
                      "Gelem/s": round(n / (ms * 1e-3) / 1e9, 2)}
         if name in ("mult_mcn", "div_mcn", "mult_mcn_slow"):  # VALU-bound: their binding roofline
-            ops = ew_fp_ops({"div_mcn": "div", "mult_mcn": "mult", "mult_mcn_slow": "mult_slow"}[name], nc)
-            res[name]["fp_ops_per_elem"] = ops
-            res[name]["valu_frac"] = round(ops * n / (ms * 1e-3) / VALU_PEAK, 3)
+            nops = ew_fp_ops({"div_mcn": "div", "mult_mcn": "mult", "mult_mcn_slow": "mult_slow"}[name], nc)
+            res[name]["fp_ops_per_elem"] = nops
+            res[name]["valu_frac"] = round(nops * n / (ms * 1e-3) / VALU_PEAK, 3)
         log(f"  elementwise {name}: {ms * 1e3:.1f} us, {gbs:.0f} GB/s")
     return {"workload": "2^26 elements, binary16, nc = 3", "ops": res}
 
@@ -496,6 +524,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-extra", action="store_true", help="only the headline workload")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--only", default="",
+                    help="comma-separated groups of extra workloads to run (pruned, small, linear, exact, linreg, "
+                         "f64, elementwise, splitk, batched, cpu_oracle); default: all")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run one 1 GiB device-to-device copy (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -557,8 +588,11 @@ def main():
                      "ops_per_mac": algo_ops_per_mac(nc, True)},
         "error": err,
     }
+    groups = [g for g in args.only.split(",") if g]
+    want = lambda name: not groups or name in groups
     if not args.no_extra:
         extra = {}
+    if not args.no_extra and want("pruned"):
         log("pruned MC x MC product on the headline operands")
         tA, tB = torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda()
         Cp = torch.empty((nc, M, N), dtype=torch.float32, device="cuda")
@@ -577,6 +611,7 @@ def main():
             "error": exact_error(oracle, A, B, Cph, nc, K, np.float32)}
         log(f"  pruned: {pms:.1f} ms")
         del Cph
+    if not args.no_extra and want("small"):
         A1, B1 = inputs.matmul_uniform(64, 64, 64, 2, np.float32, seed=0)
         C1, ms1, k1 = bench_matmul(torch, mcf, A1, B1, 2, 20, 3)
         extra["matmul_64_f32_nc2"] = {"us": round(k1 * 1e3, 1),
@@ -591,20 +626,31 @@ def main():
                 "valu_frac": round(algo_ops_per_mac(nc3, True) * macs / (k3 * 1e-3) / VALU_PEAK, 3),
                 "error": exact_error(oracle, A3, B3, C3.cpu().numpy(), nc3, 1024, np.float16)}
             log(f"  1024^3 f16 nc={nc3}: {k3:.2f} ms")
+    if not args.no_extra and want("linear"):
         log("MC-Linear")
         extra["linear_4096x1024x1024_f16_nc3"] = bench_linear(torch, mcf, inputs)
+    if not args.no_extra and want("exact"):
         log("exact binary16 products (int8 matrix cores)")
         extra["exact"] = bench_exact(torch, mcf, oracle, inputs)
+    if not args.no_extra and want("linreg"):
         log("linear-regression gradient descent")
         extra["linreg"] = bench_linreg(torch, mcf, inputs)
+    if not args.no_extra and want("f64"):
         log("binary64 components")
         extra["f64"] = bench_f64(torch, mcf, oracle, inputs)
+    if not args.no_extra and want("elementwise"):
         log("elementwise")
         extra["elementwise"] = bench_elementwise(torch, mcf, inputs)
+    if not args.no_extra and want("splitk"):
         log("K-split products")
         extra["splitk"] = bench_splitk(torch, mcf, inputs)
+    if not args.no_extra and want("batched"):
         log("batched products and AddMM")
         extra["batched"] = bench_batched(torch, mcf, inputs)
+    if not args.no_extra and want("cpu_oracle") and not args.no_cpu:
+        log("CPU oracle on the other workloads (bounded samples)")
+        extra["cpu_oracle"] = cpu_oracle_other(oracle, inputs)
+    if not args.no_extra:
         line["extra"] = extra
     if not args.no_cpu:
         log("cpu baseline (oracle)")
