@@ -185,8 +185,9 @@ def exact_error_bias(oracle, A, B, bias, C, nc, K, count=64, seed=5):
 
 def cpu_oracle_other(oracle, inputs):
     """The CPU oracle on bounded samples of the other workloads, for context beside the
-    GPU lines: binary16 nc = 3 elementwise operations on 2^22 elements, and 32 full rows
-    of the 1024^3 binary16 nc = 3 MC x MC product."""
+    GPU lines: binary16 nc = 3 elementwise operations on 2^22 elements, 32 full rows of the
+    1024^3 binary16 nc = 3 MC x MC product and of the 4096x1024x1024 MC-Linear layer, and
+    the whole 64^3 binary32 nc = 2 product."""
     out = {"threads": oracle.threads()}
     n, nc = 1 << 22, 3
     s = inputs.elementwise_suite(n, nc, np.float16, seed=0)
@@ -207,6 +208,21 @@ def cpu_oracle_other(oracle, inputs):
     dt = time.perf_counter() - t0
     out["matmul_1024_f16_nc3"] = {"MC-GFLOP/s": round(2.0 * rows.size * 1024 / dt / 1e9, 5),
                                   "sample": "32 full rows (32768 outputs, K = 1024)", "seconds": round(dt, 3)}
+    A, B = inputs.matmul_uniform(64, 64, 64, 2, np.float32, seed=0)
+    t0 = time.perf_counter()
+    oracle.matmul(A, B, nc=2)
+    dt = time.perf_counter() - t0
+    out["matmul_64_f32_nc2"] = {"MC-GFLOP/s": round(2.0 * 64 ** 3 / dt / 1e9, 5), "sample": "the full product",
+                                "seconds": round(dt, 4)}
+    x, W, b = next(inputs.linear_inputs(4096, 1024, 1024, nc, np.float16, layers=1, seed=0))
+    rows = np.repeat(np.arange(32), 1024)
+    cols = np.tile(np.arange(1024), 32)
+    t0 = time.perf_counter()
+    oracle.linear(x, W, b, nc=nc, rows=rows, cols=cols)
+    dt = time.perf_counter() - t0
+    out["linear_4096x1024x1024_f16_nc3"] = {"MC-GFLOP/s": round(2.0 * rows.size * 1024 / dt / 1e9, 5),
+                                            "sample": "32 full rows of the first layer (32768 outputs, K = 1024)",
+                                            "seconds": round(dt, 3)}
     return out
 
 

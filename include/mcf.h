@@ -37,6 +37,9 @@
  *   reject any overlap of the output with an input.
  * Degenerate sizes.  n = 0 (or M*N = 0) returns MCF_OK without launching; a
  *   reduction length of 0 gives +0 in every output component.
+ * Size limits.  Each entry point states its own; in addition every matrix of a
+ *   product (M*K, K*N, M*N elements per plane) must stay below 2^50 elements, else
+ *   MCF_E_SHAPE.
  * Errors.  Every call returns MCF_OK (0) or a negative mcf_status; on error nothing
  *   is launched.  Launch failures are reported as MCF_E_HIP.  Input values are not
  *   inspected: non-finite components propagate by IEEE rules.

@@ -29,6 +29,15 @@ bool bad_alias(const void *out, int64_t obytes, const void *in, int64_t ibytes) 
 // a 1-D grid, which must stay below 2^31 workgroups.
 bool grid_fits(int64_t M, int64_t N) { return ((M + 15) / 16) * ((N + 15) / 16) < ((int64_t)1 << 31); }
 
+// a * b elements stay below 2^50, so byte counts (times nc and the element size) and
+// offsets never overflow int64; a, b >= 0.
+bool elems_fit(int64_t a, int64_t b) { return b == 0 || a <= ((int64_t)1 << 50) / b; }
+
+// Operand sizes of an M x K by K x N product.
+bool product_fits(int64_t M, int64_t N, int64_t K) {
+  return elems_fit(M, K) && elems_fit(K, N) && elems_fit(M, N);
+}
+
 int hip_status(hipError_t e) { return e == hipSuccess ? MCF_OK : MCF_E_HIP; }
 
 int check_common(int dtype, int nc, int64_t n) {
@@ -63,6 +72,7 @@ int splitk_check(int dtype, int nc, int64_t M, int64_t N, int64_t K, int a_mc, i
   if (M < 0 || N < 0 || K < 0) return MCF_E_SHAPE;
   if (M > ((int64_t)1 << 40) || N > ((int64_t)1 << 40) || K > ((int64_t)1 << 40)) return MCF_E_SHAPE;
   if (M > 0 && N > (((int64_t)1 << 31) - 1) / M) return MCF_E_SHAPE;  // grid of up to M*N workgroups
+  if (!product_fits(M, N, K)) return MCF_E_SHAPE;
   if (slices > mcf::SPLITK_MAX_SLICES) return MCF_E_ARG;
   int64_t s = slices <= 0 ? mcf::splitk_default_slices(M, N, K) : slices;
   if (K > 0 && s > K) s = K;
@@ -176,7 +186,7 @@ int mc_matmul(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A,
   if ((a_mc != 0 && a_mc != 1) || (b_mc != 0 && b_mc != 1) || (!a_mc && !b_mc)) return MCF_E_ARG;
   if (M < 0 || N < 0 || K < 0) return MCF_E_SHAPE;
   if (M > ((int64_t)1 << 20) || N > ((int64_t)1 << 30) || K > ((int64_t)1 << 40)) return MCF_E_SHAPE;
-  if (!grid_fits(M, N)) return MCF_E_SHAPE;
+  if (!grid_fits(M, N) || !product_fits(M, N, K)) return MCF_E_SHAPE;
   if (M == 0 || N == 0) return MCF_OK;
   if (!C || (K > 0 && (!A || !B))) return MCF_E_NULL;
   const int64_t es = elem_size(dtype);
@@ -192,7 +202,7 @@ int mc_matmul_pruned(int dtype, int nc, int64_t M, int64_t N, int64_t K, const v
   if (nc < 1 || nc > MAX_NC) return MCF_E_NC;
   if (M < 0 || N < 0 || K < 0) return MCF_E_SHAPE;
   if (M > ((int64_t)1 << 20) || N > ((int64_t)1 << 30) || K > ((int64_t)1 << 40)) return MCF_E_SHAPE;
-  if (!grid_fits(M, N)) return MCF_E_SHAPE;
+  if (!grid_fits(M, N) || !product_fits(M, N, K)) return MCF_E_SHAPE;
   if (M == 0 || N == 0) return MCF_OK;
   if (!C || (K > 0 && (!A || !B))) return MCF_E_NULL;
   const int64_t es = elem_size(dtype);
@@ -222,7 +232,7 @@ int mc_matmul_batched(int dtype, int nc, int64_t B1, int64_t B2, int64_t M, int6
   if (M < 0 || N < 0 || K < 0 || B1 < 0 || B2 < 0) return MCF_E_SHAPE;
   if (M > ((int64_t)1 << 20) || N > ((int64_t)1 << 30) || K > ((int64_t)1 << 40)) return MCF_E_SHAPE;
   if (B1 > ((int64_t)1 << 40) || B2 > ((int64_t)1 << 40)) return MCF_E_SHAPE;
-  if (!grid_fits(M, N)) return MCF_E_SHAPE;
+  if (!grid_fits(M, N) || !product_fits(M, N, K)) return MCF_E_SHAPE;
   if (B1 == 0 || B2 == 0 || M == 0 || N == 0) return MCF_OK;
   if (B1 > (((int64_t)1 << 40) / B2) / (M * N)) return MCF_E_SHAPE;
   if (a_s1 < 0 || a_s2 < 0 || b_s1 < 0 || b_s2 < 0 || a_plane < 0 || b_plane < 0) return MCF_E_SHAPE;
@@ -266,7 +276,7 @@ int mc_addmm(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, 
   if ((a_mc != 0 && a_mc != 1) || (b_mc != 0 && b_mc != 1) || (!a_mc && !b_mc)) return MCF_E_ARG;
   if (M < 0 || N < 0 || K < 0) return MCF_E_SHAPE;
   if (M > ((int64_t)1 << 20) || N > ((int64_t)1 << 30) || K > ((int64_t)1 << 40)) return MCF_E_SHAPE;
-  if (!grid_fits(M, N)) return MCF_E_SHAPE;
+  if (!grid_fits(M, N) || !product_fits(M, N, K)) return MCF_E_SHAPE;
   if (y_rows != M && y_rows != 1) return MCF_E_SHAPE;
   // the scalars must be values of the component format
   const bool exact = dtype == MCF_F64   ? true
@@ -410,7 +420,7 @@ int mc_linear_fwd(int dtype, int nc, int64_t batch, int64_t in, int64_t out, con
   if (nc < 1 || nc > MAX_NC) return MCF_E_NC;
   if (batch < 0 || in < 0 || out < 0) return MCF_E_SHAPE;
   if (batch > ((int64_t)1 << 20) || out > ((int64_t)1 << 30) || in > ((int64_t)1 << 40)) return MCF_E_SHAPE;
-  if (!grid_fits(batch, out)) return MCF_E_SHAPE;
+  if (!grid_fits(batch, out) || !product_fits(batch, out, in)) return MCF_E_SHAPE;
   if (batch == 0 || out == 0) return MCF_OK;
   if (!y || (in > 0 && (!x || !W))) return MCF_E_NULL;
   const int64_t es = elem_size(dtype);

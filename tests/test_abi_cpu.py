@@ -81,6 +81,10 @@ def test_validation_matrix(L):
     assert L.mc_linear_fwd(0, 3, 4, 4, 4, None, b, None, c, None) == MCF_E_NULL
     assert L.mc_linear_fwd(0, 3, 4, 4, 4, a, b, P(0x300000), c, None) == MCF_E_ALIAS
     assert L.mc_linear_fwd(0, 3, 0, 4, 4, None, None, None, None, None) == MCF_OK
+    # operand matrices beyond 2^50 elements are rejected before any byte count is formed
+    assert L.mc_matmul(0, 3, 1 << 12, 4, 1 << 39, a, 1, b, 1, c, None) == MCF_E_SHAPE  # M K = 2^51
+    assert L.mc_matmul(0, 3, 4, 1 << 30, 1 << 21, a, 1, b, 1, c, None) == MCF_E_SHAPE  # K N = 2^51
+    assert L.mc_linear_fwd(0, 3, 4, 1 << 39, 1 << 12, a, b, None, c, None) == MCF_E_SHAPE  # in out = 2^51
 
 
 def test_validation_splitk(L):
@@ -114,6 +118,7 @@ def test_validation_splitk(L):
     assert f(1, 7, 4, 4, 4096, a, 1, b, 0, 16, None, 0, c, None) == MCF_E_NC
     assert f(1, 3, 4, 4, -1, a, 1, b, 0, 16, None, 0, c, None) == MCF_E_SHAPE
     assert f(1, 3, 1 << 16, 1 << 16, 4, a, 1, b, 0, 16, None, 0, c, None) == MCF_E_SHAPE  # M N > 2^31
+    assert f(1, 3, 1, 1 << 14, 1 << 37, a, 1, b, 0, 16, None, 0, c, None) == MCF_E_SHAPE  # K N = 2^51
     assert f(1, 3, 0, 4, 4096, None, 1, None, 0, 16, None, 0, None, None) == MCF_OK
     assert f(1, 3, 4, 4, 4096, a, 1, b, 0, 1024, None, 0, c, None) == MCF_E_NULL  # workspace needed
     need = ws(1, 3, 4, 4, 4096, 1, 0, 1024)
