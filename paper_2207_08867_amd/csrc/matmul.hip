@@ -417,12 +417,17 @@ struct MmArgs {
 
 // A: [NA][M][K] row-major planes.  B: [NB][K][N] (BT = false) or [NB][N][K] (BT =
 // true).  NA = NC when A is MC else 1, likewise NB.
-// nc <= 3: at least 5 wavefronts per SIMD (at most 96 VGPRs); the binary32 kernels
-// sit just under that bound (the 8192^3 one spills one 8-byte value outside its loop)
-// and one register more would drop them to 4.  nc = 4 needs more registers.
+// Occupancy: with nc <= 3, binary32 kernels run at least 5 wavefronts per SIMD (at most
+// 96 VGPRs); they sit just under that bound (the 8192^3 one spills one 8-byte value
+// outside its loop) and one register more would drop them to 4.  The binary16 kernels
+// (but the pruned ones) run 8, the most a SIMD holds: at 64 VGPRs the few values that
+// no longer fit are per-tile addresses, reloaded once per tile, and the 1024^3
+// products run 4-6% faster than at 5 or 6 wavefronts.  nc = 4 needs more registers.
 template <typename T, int NC, bool AMC, bool BMC, bool BT, int TM, int TN, int KT, int SPOL, int APOL,
           bool GROUP, bool ADDMM, bool PRUNE>
-__global__ __attribute__((amdgpu_flat_work_group_size(1, MM_THREADS), amdgpu_waves_per_eu(NC <= 3 && sizeof(T) <= 4 ? 5 : 1))) void
+__global__ __attribute__((amdgpu_flat_work_group_size(1, MM_THREADS),
+                          amdgpu_waves_per_eu(sizeof(T) == 2 && NC <= 3 && !PRUNE ? 8
+                                              : (NC <= 3 && sizeof(T) <= 4 ? 5 : 1)))) void
 mm_kernel(const T *__restrict__ A, const T *__restrict__ B,
                                                         T *__restrict__ C, const MmArgs<T> g) {
   const int64_t M = g.M, N = g.N, K = g.K;
