@@ -27,7 +27,7 @@ template <typename T, int N>
 __device__ __forceinline__ void scaling_n_kept(const T (&y)[N], T q, T (&out)[N]) {
   T last;
   scaling_kept<T, N, false, false>(y, q, out, last);
-  if (kept_invalid<T, N, false>(out, last)) {
+  if (kept_invalid<T, N, false, true>(out, last)) {
     T h[N + 1];
     scaling_terms<T, N>(y, q, h);
     compact_nz<T, N + 1, N>(h, out);

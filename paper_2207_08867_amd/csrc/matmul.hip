@@ -243,13 +243,13 @@ struct Lane {
             T t[NC], sum[NC], last;
             if constexpr (!AMC) {
               scaling_kept<T, NC, false, TPS>(o.b[j], o.a[i][0], t, last);
-              bad |= kept_invalid<T, NC, TPS>(t, last);
+              bad |= kept_invalid<T, NC, TPS, true>(t, last);
             } else if (TPS && p > 0) {
               scaling_kept<T, NC, true, true>(o.a[i], o.b[j][p], t, last);
-              bad |= kept_invalid<T, NC, true>(t, last);
+              bad |= kept_invalid<T, NC, true, true>(t, last);
             } else {
               scaling_kept<T, NC, false, TPS>(o.a[i], o.b[j][p], t, last);
-              bad |= kept_invalid<T, NC, TPS>(t, last);
+              bad |= kept_invalid<T, NC, TPS, true>(t, last);
             }
             if (AMC && BMC && TPS && p > 0) {
               bad |= add_tiny<T, NC>(acc[p][i][j], t, sum);

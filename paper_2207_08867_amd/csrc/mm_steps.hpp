@@ -187,6 +187,14 @@ __device__ __forceinline__ bool abs_below(float x, float lim) { return __builtin
 __device__ __forceinline__ bool abs_below(_Float16 x, _Float16 lim) { return __builtin_fabsf16(x) < lim; }
 __device__ __forceinline__ bool abs_below(double x, double lim) { return __builtin_fabs(x) < lim; }
 
+// Magnitudes out of order: !(|b| <= |a|), true when |b| > |a| or either is a NaN (one
+// compare with abs modifiers).
+__device__ __forceinline__ bool out_of_order(float a, float b) { return !(__builtin_fabsf(b) <= __builtin_fabsf(a)); }
+__device__ __forceinline__ bool out_of_order(_Float16 a, _Float16 b) {
+  return !(__builtin_fabsf16(b) <= __builtin_fabsf16(a));
+}
+__device__ __forceinline__ bool out_of_order(double a, double b) { return !(__builtin_fabs(b) <= __builtin_fabs(a)); }
+
 // h_0 .. h_{N-1} of ScalingN(x, v) and the last product hp = fl(x_{N-1} v).
 // HEAD_EXACT: the error of x_0 v is known to be zero; TAIL_EXACT: so are the errors
 // of x_i v, i >= 1 (both follow from |product| < exact_limit, established per tile).
@@ -244,28 +252,34 @@ __device__ __forceinline__ void add_kept(const T (&x)[N], const T (&y)[N], T (&h
 // accumulators of the low components of B in an MC x MC product, whose products the
 // tile flag shows to be below it): each sum x_i + y_i is then exact, every Two-Sum
 // error and carry is zero, and the final carry is zero, so the terms are the N sums
-// followed by zero.  Returns true when a lane does not meet that condition or when
-// Simple-Renorm would move a term (a zero before a non-zero); such a lane runs the
-// general step.
+// followed by zero.  Returns true when a lane may not meet that condition or when
+// Simple-Renorm may move a term; such a lane runs the general step.  The test is the
+// magnitude order of the sums (see kept_invalid) and |h_0| < exact_limit: sums in
+// order are all at most |h_0|, so they are below the limit too.
 template <typename T, int N>
 __device__ __forceinline__ bool add_tiny(const T (&x)[N], const T (&y)[N], T (&h)[N]) {
-  bool bad = false;
 #pragma unroll
-  for (int i = 0; i < N; ++i) {
-    h[i] = x[i] + y[i];
-    bad = bad | !abs_below(h[i], (T)exact_limit<T>());
-  }
+  for (int i = 0; i < N; ++i) h[i] = x[i] + y[i];
+  bool bad = !abs_below(h[0], (T)exact_limit<T>());
 #pragma unroll
-  for (int i = 0; i + 1 < N; ++i) bad = bad | ((h[i] == T(0)) & (h[i + 1] != T(0)));
+  for (int i = 0; i + 1 < N; ++i) bad = bad | out_of_order(h[i], h[i + 1]);
   return bad;
 }
 
 // True when Simple-Renorm of the step's nc+1 terms could change h: a non-zero term
 // follows a zero one, or a term is zero and the last operation may have been inexact
 // (LAST_EXACT: known exact for the whole tile; else tested as |last| < exact_limit).
+// ORDERED tests the first condition as magnitudes out of order, |h_{i+1}| > |h_i| for
+// some i (or a NaN): a zero followed by a non-zero is out of order, so this flags a
+// superset of those lanes with one compare per pair instead of three and a mask
+// operation; the extra lanes run the general step, which gives the same result.  It
+// suits ScalingN's terms, whose magnitudes decrease (a later term exceeds an earlier
+// non-zero one only in the subnormal range), but not Add-MCN's: an accumulator's
+// leading component passes near zero during a reduction while its second component
+// still holds the errors gathered before, so there the zero pattern itself is tested.
 // With N = 1 the single kept term is the result whenever it is non-zero, and when it
 // is zero the dropped term is zero too (a zero product or sum is exact).
-template <typename T, int N, bool LAST_EXACT>
+template <typename T, int N, bool LAST_EXACT, bool ORDERED = false>
 __device__ __forceinline__ bool kept_invalid(const T (&h)[N], T last) {
   if constexpr (N == 1) {
     return false;
@@ -277,7 +291,7 @@ __device__ __forceinline__ bool kept_invalid(const T (&h)[N], T last) {
     for (int i = 0; i < N; ++i) z[i] = h[i] == T(0);
     bool bad = false;
 #pragma unroll
-    for (int i = 0; i + 1 < N; ++i) bad = bad | (z[i] & !z[i + 1]);
+    for (int i = 0; i + 1 < N; ++i) bad = bad | (ORDERED ? out_of_order(h[i], h[i + 1]) : (z[i] & !z[i + 1]));
     if constexpr (LAST_EXACT) return bad;
     return bad | (z[N - 1] & !abs_below(last, (T)exact_limit<T>()));
   }
@@ -289,7 +303,7 @@ template <typename T, int N, bool HEAD, bool TAIL>
 __device__ __forceinline__ void kept_scale(const T (&x)[N], T v, T (&t)[N]) {
   T last;
   scaling_kept<T, N, HEAD, TAIL>(x, v, t, last);
-  if (__builtin_expect(kept_invalid<T, N, TAIL>(t, last), 0)) {
+  if (__builtin_expect(kept_invalid<T, N, TAIL, true>(t, last), 0)) {
     T h[N + 1];
     scaling_terms<T, N>(x, v, h);
     compact_nz<T, N + 1, N>(h, t);
