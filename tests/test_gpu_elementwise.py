@@ -240,3 +240,24 @@ def test_div_mult_spread_and_zero_components(mcf, orc, dt, nc, op):
         got = to_host(fn[0](to_dev(x), to_dev(y), nc=nc))
         want = fn[1](x, y, nc=nc)
     assert_bits(got, want, f"{op} spread {dt.__name__} nc={nc}")
+
+
+@pytest.mark.parametrize("dt", DTS)
+@pytest.mark.parametrize("nc", [2, 3])
+@pytest.mark.parametrize("op", ["mul", "div", "mul_slow"])
+def test_div_mult_unordered_components(mcf, orc, dt, nc, op):
+    """Div-MCN and Mult-MCN on component tuples whose magnitudes are out of order (each
+    component drawn independently over 2^-20 .. 2^2): the kept-terms ScalingN steps
+    then see terms out of magnitude order, which their order test sends to the general
+    step.  Bit for bit; non-finite results by class."""
+    n = 12_007
+    g = np.random.default_rng(1300 + nc + 10 * ("mul" in op) + 20 * (dt == np.float32) + 40 * (op == "mul_slow"))
+    def operand():
+        return (g.normal(0.0, 1.0, (nc, n)) * np.exp2(g.integers(-20, 3, (nc, n)))).astype(dt)
+    x, y = operand(), operand()
+    fn = {"mul": (mcf.mc_mul, orc.mul), "div": (mcf.mc_div, orc.div),
+          "mul_slow": (mcf.mc_mul_slow, orc.mul_slow)}[op]
+    with np.errstate(all="ignore"):
+        got = to_host(fn[0](to_dev(x), to_dev(y), nc=nc))
+        want = fn[1](x, y, nc=nc)
+    assert_bits(got, want, f"{op} unordered {dt.__name__} nc={nc}")

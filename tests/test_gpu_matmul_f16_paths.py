@@ -163,3 +163,45 @@ def test_growing_low_accumulators(mcf, orc, nc):
     B = inputs.split(2.0 ** -5 * (1.0 + g.uniform(0.0, 1.0, (K, N))), nc, np.float16)
     got = to_host(mcf.mc_matmul(to_dev(A), to_dev(B), nc=nc))
     assert_bits(got, orc.matmul(A, B, nc=nc), f"growing nc={nc}")
+
+
+def unordered(g, shape, nc, nonfinite=0):
+    """Components drawn independently, each N(0,1) times 2^s with s from -20 .. 2, so
+    that a later component is larger than an earlier non-zero one about half the time
+    (not normalized MC values; the algorithms take any component tuple).  ScalingN's
+    kept terms are then out of magnitude order, the case its order test sends to the
+    general step.  `nonfinite` entries get an infinite or NaN component."""
+    X = (g.normal(0.0, 1.0, (nc,) + shape) * np.exp2(g.integers(-20, 3, (nc,) + shape))).astype(np.float16)
+    if nonfinite:
+        idx = tuple(g.integers(0, d, nonfinite) for d in (nc,) + shape)
+        X[idx] = np.array([np.inf, -np.inf, np.nan], dtype=np.float16)[g.integers(0, 3, nonfinite)]
+    return X
+
+
+@pytest.mark.parametrize("nc", [2, 3])
+@pytest.mark.parametrize("kinds", KINDS)
+@pytest.mark.parametrize("nonfinite", [0, 5])
+def test_unordered_components(mcf, orc, nc, kinds, nonfinite):
+    a_mc, b_mc = kinds
+    M, N, K = 52, 40, 150
+    g = np.random.default_rng(1100 + 10 * nc + 3 * a_mc + b_mc + nonfinite)
+    A = unordered(g, (M, K), nc, nonfinite)
+    B = unordered(g, (K, N), nc, nonfinite)
+    A = A if a_mc else A[:1]
+    B = B if b_mc else B[:1]
+    with np.errstate(all="ignore"):
+        got = to_host(mcf.mc_matmul(to_dev(A), to_dev(B), nc=nc, a_mc=a_mc, b_mc=b_mc))
+        want = orc.matmul(A, B, nc=nc, a_mc=a_mc, b_mc=b_mc)
+    assert_bits(got, want, f"unordered nc={nc} {kinds} nonfinite={nonfinite}")
+
+
+def test_linear_unordered(mcf, orc):
+    T, I, O, nc = 40, 96, 33, 3
+    g = np.random.default_rng(1200)
+    x = (g.normal(0.0, 1.0, (T, I)) * np.exp2(g.integers(-12, 3, (T, I)))).astype(np.float16)
+    W = unordered(g, (O, I), nc)
+    b = unordered(g, (O,), nc)
+    with np.errstate(all="ignore"):
+        got = to_host(mcf.mc_linear_fwd(to_dev(x), to_dev(W), to_dev(b)))
+        want = orc.linear(x, W, b, nc=nc)
+    assert_bits(got, want, "linear unordered")
