@@ -189,9 +189,12 @@ int mc_addmm(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, 
  *   combined left to right with Add-MCN (as mc_matmul).
  * S = 1 gives exactly mc_matmul's result.  Other S give a result of the same
  * accuracy class (the error bound of MM-MCN holds) but not the same bits.
- * slices: S, at most 65536 (else MCF_E_ARG); values above K are taken as K;
+ * slices: S, at most 2^20 (else MCF_E_ARG); values above K are taken as K;
  *   slices <= 0 selects mc_matmul_splitk_slices(M, N, K).
- * workspace: device memory of at least mc_matmul_splitk_workspace(...) bytes, owned
+ * workspace: device memory of at least mc_matmul_splitk_workspace(...) bytes (the
+ *   partial tree roots: G = ceil(S / 256) entries of planes x nc x M x N components
+ *   when S > 256, plus ceil(G / 256) more when G > 256; planes = nc for MC x MC, else
+ *   1), owned
  *   by the caller, not overlapping A, B or C; may be NULL when that size is 0.  Its
  *   contents on entry do not matter; calls sharing a workspace must not overlap
  *   in time.  Too small: MCF_E_ARG; NULL when needed: MCF_E_NULL.
@@ -202,7 +205,7 @@ int mc_matmul_splitk(int dtype, int nc, int64_t M, int64_t N, int64_t K, const v
 
 /* Default slice count of mc_matmul_splitk, a function of the shape only: enough
  * slices for about 2^18 lanes in total (ceil(2^18 / (M N))), at most K / 8 (so a
- * slice holds at least 8 terms when K allows), at most 65536, at least 1.
+ * slice holds at least 8 terms when K allows), at most 2^20, at least 1.
  * Negative sizes: MCF_E_SHAPE. */
 int64_t mc_matmul_splitk_slices(int64_t M, int64_t N, int64_t K);
 

@@ -82,11 +82,8 @@ int splitk_check(int dtype, int nc, int64_t M, int64_t N, int64_t K, int a_mc, i
 
 int64_t splitk_workspace_bytes(int dtype, int nc, int64_t M, int64_t N, int64_t K, int a_mc, int b_mc, int64_t S) {
   if (M == 0 || N == 0 || K == 0) return 0;
-  int KS, G;
-  mcf::splitk_shape(S, &KS, &G);
-  if (G == 1) return 0;
   const int64_t np = (a_mc && b_mc) ? nc : 1;
-  return (int64_t)G * np * nc * M * N * elem_size(dtype);
+  return mcf::splitk_roots(S) * np * nc * M * N * elem_size(dtype);
 }
 
 int exact_check(int dtype, int nc, int64_t M, int64_t N, int64_t K, int a_mc, int b_mc, int b_trans) {

@@ -81,11 +81,8 @@ LrLayout lr_layout(int dtype, int nc, int64_t n, int64_t d) {
   L.rr = L.g + align256(nc * d * es);
   L.sk = L.rr + align256(nc * es);
   // K-split workspaces of r^T X (M = 1, N = d, MC x plain) and r . r (M = N = 1, MC x MC)
-  int KS, G;
-  splitk_shape(splitk_default_slices(1, d, n), &KS, &G);
-  const int64_t w1 = G > 1 ? (int64_t)G * nc * d * es : 0;
-  splitk_shape(splitk_default_slices(1, 1, n), &KS, &G);
-  const int64_t w2 = G > 1 ? (int64_t)G * nc * nc * es : 0;
+  const int64_t w1 = splitk_roots(splitk_default_slices(1, d, n)) * nc * d * es;
+  const int64_t w2 = splitk_roots(splitk_default_slices(1, 1, n)) * nc * nc * es;
   L.total = L.sk + align256(w1 > w2 ? w1 : w2);
   return L;
 }

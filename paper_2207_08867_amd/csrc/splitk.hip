@@ -16,9 +16,11 @@
 // so the lanes of a slice group read consecutive k.  The first log2(KS) tree levels
 // run inside the workgroup (strides < 64 by lane exchange inside a wavefront, 64 and
 // 128 through LDS); when S > KS the G = ceil(S/KS) group results go to a workspace
-// and a second kernel runs the remaining levels the same way.  Because slice groups
-// are aligned blocks of KS leaves, the split between the two kernels never pairs
-// entries across groups: the result equals the tree's definition for every KS.
+// and a second kernel runs the next levels the same way over aligned groups of up to
+// 256 roots (a third launch combines the ceil(G/256) roots of the second when G >
+// 256).  Because every group is an aligned block of the level below, the split
+// between launches never pairs entries across groups: the result equals the tree's
+// definition for every launch shape.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -185,21 +187,36 @@ __global__ __launch_bounds__(SK_THREADS) void sk_kernel(const T *__restrict__ A,
   }
 }
 
-// Phase 2: the remaining tree levels over the G group roots of each output, GW lanes
-// (GW = G rounded up to a power of two) per output.
+// Phase 2: the next tree levels over the G entries of each output in W, in aligned
+// groups of up to 256 (block y of the grid takes entries 256 y .. 256 y + 255), GW
+// lanes per output (GW = the group size rounded up to a power of two).  With one
+// group (G <= 256) the root is the result and goes to C; otherwise group y's root goes
+// to entry y of Wn [ceil(G/256)][NP][NC][M*N].
 template <typename T, int NC, int NP, int APOL>
-__global__ __launch_bounds__(SK_THREADS) void sk_reduce_kernel(const T *__restrict__ W, T *__restrict__ C,
-                                                               int64_t MN, int G, int GW) {
+__global__ __launch_bounds__(SK_THREADS) void sk_reduce_kernel(const T *__restrict__ W, T *__restrict__ Wn,
+                                                               T *__restrict__ C, int64_t MN, int G, int GW) {
   __shared__ T lds[SK_THREADS][NP * NC];
   const int q = threadIdx.x & (GW - 1);
   const int64_t o = (int64_t)blockIdx.x * (SK_THREADS / GW) + threadIdx.x / GW;
+  const int base = (int)blockIdx.y * SK_THREADS;
+  const int count = G - base < SK_THREADS ? G - base : SK_THREADS;
   T acc[NP][NC];
 #pragma unroll
   for (int p = 0; p < NP; ++p)
 #pragma unroll
-    for (int c = 0; c < NC; ++c) acc[p][c] = (o < MN && q < G) ? W[(((int64_t)q * NP + p) * NC + c) * MN + o] : T(0);
-  group_tree<T, NC, NP, APOL>(acc, q, GW, G, lds);
-  if (q == 0 && o < MN) sk_store<T, NC, NP, APOL>(acc, C, MN, o);
+    for (int c = 0; c < NC; ++c)
+      acc[p][c] = (o < MN && q < count) ? W[(((int64_t)(base + q) * NP + p) * NC + c) * MN + o] : T(0);
+  group_tree<T, NC, NP, APOL>(acc, q, GW, count, lds);
+  if (q == 0 && o < MN) {
+    if (G <= SK_THREADS) {
+      sk_store<T, NC, NP, APOL>(acc, C, MN, o);
+    } else {
+#pragma unroll
+      for (int p = 0; p < NP; ++p)
+#pragma unroll
+        for (int c = 0; c < NC; ++c) Wn[(((int64_t)blockIdx.y * NP + p) * NC + c) * MN + o] = acc[p][c];
+    }
+  }
 }
 
 static int pow2_at_least(int64_t v) {
@@ -224,6 +241,13 @@ void splitk_shape(int64_t S, int *KS, int *G) {
   *G = (int)((S + ks - 1) / ks);
 }
 
+int64_t splitk_roots(int64_t S) {
+  int KS, G;
+  splitk_shape(S, &KS, &G);
+  if (G == 1) return 0;
+  return G + (G > SK_THREADS ? (G + SK_THREADS - 1) / SK_THREADS : 0);
+}
+
 template <typename T, int NC, bool AMC, bool BMC>
 static hipError_t sk_launch(int64_t M, int64_t N, int64_t K, const void *A, const void *B, int64_t S, void *W, void *C,
                             hipStream_t s) {
@@ -239,11 +263,22 @@ static hipError_t sk_launch(int64_t M, int64_t N, int64_t K, const void *A, cons
                      (const T *)B, (T *)C, (T *)W, M, N, K, S, KS, G);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || G == 1) return e;
-  const int GW = pow2_at_least(G);
-  dim3 grid2((unsigned)((MN + (SK_THREADS / GW) - 1) / (SK_THREADS / GW)));
-  hipLaunchKernelGGL((sk_reduce_kernel<T, NC, NP, APOL>), grid2, dim3(SK_THREADS), 0, s, (const T *)W, (T *)C, MN, G,
-                     GW);
-  return hipGetLastError();
+  // W: [G] group roots, then [ceil(G/256)] roots of their groups of 256 (G > 256).
+  // S <= SPLITK_MAX_SLICES = 2^20 gives G <= 4096, so the second level has at most
+  // 16 entries and a third launch finishes.
+  T *lvl = (T *)W, *next = (T *)W + (int64_t)G * NP * NC * MN;
+  for (int g = G;;) {
+    const int GW = pow2_at_least(g < SK_THREADS ? g : SK_THREADS);
+    const int groups = (g + SK_THREADS - 1) / SK_THREADS;
+    dim3 grid2((unsigned)((MN + (SK_THREADS / GW) - 1) / (SK_THREADS / GW)), (unsigned)groups);
+    hipLaunchKernelGGL((sk_reduce_kernel<T, NC, NP, APOL>), grid2, dim3(SK_THREADS), 0, s, (const T *)lvl, next,
+                       (T *)C, MN, g, GW);
+    e = hipGetLastError();
+    if (e != hipSuccess || groups == 1) return e;
+    if (groups > SK_THREADS) return hipErrorInvalidValue;  // beyond SPLITK_MAX_SLICES
+    lvl = next;
+    g = groups;
+  }
 }
 
 template <typename T, int NC>

@@ -100,10 +100,11 @@ def test_validation_splitk(L):
     sl = L.mc_matmul_splitk_slices
     sl.restype = ctypes.c_int64
     sl.argtypes = [ctypes.c_int64] * 3
-    # default slice count: about 2^18 lanes, at most K / 8, at most 65536, at least 1
+    # default slice count: about 2^18 lanes, at most K / 8, at most 2^20, at least 1
     assert sl(64, 64, 64) == 8
     assert sl(4096, 1, 4096) == 64
-    assert sl(1, 1, 1 << 24) == 65536
+    assert sl(1, 1, 1 << 24) == 1 << 18
+    assert sl(1, 1, 1 << 30) == 1 << 18  # the 2^20 cap binds explicit slice counts only
     assert sl(1, 1, 100) == 12
     assert sl(1024, 1024, 1024) == 1
     assert sl(1, 1, 3) == 1
@@ -112,7 +113,9 @@ def test_validation_splitk(L):
     assert ws(1, 3, 4, 4, 4096, 1, 0, 256) == 0
     assert ws(1, 3, 4, 4, 4096, 1, 0, 257) == 2 * 1 * 3 * 16 * 4
     assert ws(0, 2, 4, 4, 4096, 1, 1, 1024) == 4 * 2 * 2 * 16 * 2
-    assert ws(1, 3, 4, 4, 4096, 1, 0, 1 << 17) == MCF_E_ARG
+    assert ws(1, 3, 4, 4, 4096, 1, 0, (1 << 20) + 1) == MCF_E_ARG
+    # G = 274 group roots and 2 roots of their groups of 256
+    assert ws(1, 3, 4, 4, 1 << 20, 1, 0, 70000) == (274 + 2) * 1 * 3 * 16 * 4
     assert ws(1, 3, 4, 4, 100, 1, 0, 1000) == 0  # capped at K = 100 slices
     assert f(1, 3, 4, 4, 4096, a, 0, b, 0, 16, None, 0, c, None) == MCF_E_ARG
     assert f(1, 7, 4, 4, 4096, a, 1, b, 0, 16, None, 0, c, None) == MCF_E_NC

@@ -75,6 +75,31 @@ def test_dot_max_slices(mcf, orc):
     check_bound(orc, A, B, got, 2, K, np.float32)
 
 
+@pytest.mark.parametrize("S", [70000, 1 << 20])
+def test_dot_three_levels(mcf, orc, S):
+    """More than 256 slice groups: the second tree level runs over aligned groups of
+    256 roots and a third combines their roots.  S = 70000: 274 groups (the last
+    partial), 2 second-level roots; S = 2^20 (the maximum): 4096 groups, 16 roots;
+    K = 2^21 + 3, so the largest S has two or three steps per slice."""
+    K = (1 << 21) + 3
+    A, B = inputs.matmul_normal(1, 1, K, 2, np.float32, seed=98)
+    got = to_host(mcf.mc_matmul_splitk(to_dev(A), to_dev(B), nc=2, slices=S))
+    want = orc.matmul_splitk(A, B, nc=2, slices=S)
+    assert_bits(got, want, f"dot {S} slices")
+    check_bound(orc, A, B, got, 2, K, np.float32)
+
+
+@pytest.mark.parametrize("dt", [np.float16, np.float32])
+def test_small_outputs_three_levels(mcf, orc, dt):
+    """Several outputs (3 x 2, MC x MC, nc = 3) with 70000 slices: second-level
+    groups of 256 roots per output in a two-dimensional grid, then a third level."""
+    M, N, K, nc = 3, 2, 150_001, 3
+    A, B = inputs.matmul_normal(M, N, K, nc, dt, seed=99)
+    got = to_host(mcf.mc_matmul_splitk(to_dev(A), to_dev(B), nc=nc, slices=70000))
+    want = orc.matmul_splitk(A, B, nc=nc, slices=70000)
+    assert_bits(got, want, f"small outputs {dt.__name__}")
+
+
 @pytest.mark.parametrize("dt", [np.float16, np.float32])
 def test_mv(mcf, orc, dt):
     """MV-MCN (N = 1), M = 1000, K = 4099, default slice count."""
@@ -111,8 +136,8 @@ def test_workspace_reuse_and_degenerate(mcf, orc):
         assert_bits(to_host(mcf.mc_matmul_splitk(tA, tB, nc=3, slices=1000, workspace=ws)), want, "reuse")
     with pytest.raises(ValueError):
         mcf.mc_matmul_splitk(tA, tB, nc=3, slices=1000, workspace=ws[:-1])
-    with pytest.raises(ValueError):
-        mcf.mc_matmul_splitk(tA, tB, nc=3, slices=70000)
+    with pytest.raises(ValueError):  # above the maximum of 2^20 slices
+        mcf.mc_matmul_splitk(tA, tB, nc=3, slices=(1 << 20) + 1)
     Z = to_host(mcf.mc_matmul_splitk(to_dev(np.zeros((3, 5, 0), np.float32)), to_dev(np.zeros((3, 0, 6), np.float32)),
                                      nc=3, slices=8))
     assert Z.shape == (3, 5, 6) and (Z == 0).all() and not np.signbit(Z).any()
@@ -122,9 +147,10 @@ def test_workspace_reuse_and_degenerate(mcf, orc):
 
 def test_bench_shapes(mcf, orc):
     """The K-split launch configurations the benchmark times (default slice counts):
-    Dot of two binary32 nc = 2 MC vectors at the maximum of 65536 slices (256
-    workgroups of 256 slices, a 256-lane second-level tree) with K = 2^22 + 5 (the
-    benchmark's 2^24 takes the same launch; the one-output oracle is sequential),
+    Dot of two binary32 nc = 2 MC vectors at 2^18 slices (1024 workgroups of 256
+    slices, a second tree level over groups of 256 roots and a third over the 4
+    roots of those) with K = 2^22 + 5 (the benchmark's 2^24 takes the same launch;
+    the one-output oracle is sequential),
     bitwise and within the bound; MV of an 8192 x 8192 binary32 nc = 3 MC matrix by a
     plain vector, in full on the GPU, on 48 sampled rows."""
     K = (1 << 22) + 5
