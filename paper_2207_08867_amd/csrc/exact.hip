@@ -132,6 +132,39 @@ __global__ void xs_init(uint32_t *stats, uint8_t *bad_a, int64_t na, uint8_t *ba
 // digit d_s is byte s of Y with its top bit flipped.
 constexpr uint64_t XBIAS = 0x808080808080ull;
 
+// The exact integers (units of 2^-24) of entries (row, k0 .. k0+3) of an operand with
+// P planes; p points at entry (row, k0) of plane 0.  All loads are issued first.
+template <int P>
+__device__ __forceinline__ void slice_entries(const SliceOp &o, const uint16_t *p, int64_t k0, int64_t K,
+                                              int64_t (&X)[4], bool &bad) {
+  uint32_t bits[P][4];
+  if (o.vec && k0 + 4 <= K) {
+#pragma unroll
+    for (int c = 0; c < P; ++c) {
+      const uint2 v = *(const uint2 *)(p + c * o.plane);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) bits[c][j] = ((j < 2 ? v.x : v.y) >> (16 * (j % 2))) & 0xFFFFu;
+    }
+  } else {
+    // an entry beyond K reads the operand's first entry instead and is discarded
+#pragma unroll
+    for (int c = 0; c < P; ++c)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const bool ok = k0 + j < K;
+        const uint32_t v = ok ? p[c * o.plane + j * o.ks] : o.src[0];
+        bits[c][j] = ok ? v : 0u;
+      }
+  }
+#pragma unroll
+  for (int c = 0; c < P; ++c)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (f16_nonfinite(bits[c][j])) bad = true;
+      else X[j] += f16_units(bits[c][j]);
+    }
+}
+
 // Lane t writes bytes 4 (t % 4) .. 4 (t % 4) + 3 of 16-byte chunk t / 4 of every level
 // plane.  In fragment order chunk u is row block rb = (u / 64) % RB, k block
 // kb = u / (64 RB), and inside the block lane l = u % 64 holds row 16 rb + l % 16,
@@ -154,29 +187,15 @@ __global__ __launch_bounds__(XS_THREADS) void xs_slice(SliceOp a, SliceOp b, int
     int64_t X[4] = {0, 0, 0, 0};
     bool bad = false;
     if (row < o.R) {
+      // Every load of the lane is issued before any is used, so the lane waits for
+      // memory once rather than once per plane (the plane count is uniform per
+      // workgroup: one operand per workgroup).
       const uint16_t *p = o.src + row * o.rs + k0 * o.ks;
-      if (o.vec && k0 + 4 <= K) {
-        for (int c = 0; c < o.planes; ++c) {
-          const uint2 v = *(const uint2 *)(p + c * o.plane);
-          const uint32_t w[2] = {v.x, v.y};
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const uint32_t bits = (w[j / 2] >> (16 * (j % 2))) & 0xFFFFu;
-            if (f16_nonfinite(bits)) bad = true;
-            else X[j] += f16_units(bits);
-          }
-        }
-      } else {
-        for (int c = 0; c < o.planes; ++c) {
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            if (k0 + j < K) {
-              const uint32_t bits = p[c * o.plane + j * o.ks];
-              if (f16_nonfinite(bits)) bad = true;
-              else X[j] += f16_units(bits);
-            }
-          }
-        }
+      switch (o.planes) {
+        case 1: slice_entries<1>(o, p, k0, K, X, bad); break;
+        case 2: slice_entries<2>(o, p, k0, K, X, bad); break;
+        case 3: slice_entries<3>(o, p, k0, K, X, bad); break;
+        default: slice_entries<4>(o, p, k0, K, X, bad); break;
       }
       if (bad) {
         o.bad[row] = 1;
