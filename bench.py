@@ -513,14 +513,34 @@ def bench_linreg(torch, mcf, inputs, steps=3000):
         torch.cuda.synchronize()
         us = s.elapsed_time(e) * 1e3 / (steps - 1)
         name = f"{'f16' if dt == np.float16 else 'f32'}_nc{nc}"
+        # the same steps replayed from a HIP graph of 100 captured steps (the loop is
+        # launch-bound: five kernels per step), checked bit for bit against the eager run
+        tWg = torch.from_numpy(np.ascontiguousarray(W0)).cuda()
+        lossg, wsg = torch.empty_like(loss), torch.empty_like(ws)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for _ in range(100):
+                mcf.mc_linreg_gd_step(tX, ty, tWg, lr, loss=lossg, workspace=wsg)
+        torch.cuda.synchronize()
+        sg, eg = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        sg.record()
+        for _ in range(steps // 100):
+            graph.replay()
+        eg.record()
+        torch.cuda.synchronize()
+        us_graph = sg.elapsed_time(eg) * 1e3 / (steps // 100 * 100)
+        same = bool(torch.equal(tWg.view(torch.int16 if dt == np.float16 else torch.int32),
+                                tW.view(torch.int16 if dt == np.float16 else torch.int32)))
+        del graph
         # the same loss in float64 from the final weights (a binary16 MC loss underflows
         # to 0 below the smallest subnormal, 2^-24)
         w = tW.double().sum(dim=0).cpu().numpy()
         r64 = X.astype(np.float64) @ w + y_neg.astype(np.float64)
-        out[name] = {"us_per_step": round(us, 2), "loss_first": first, "loss_last": float(loss.double().sum()),
+        out[name] = {"us_per_step": round(us, 2), "us_per_step_graph": round(us_graph, 2),
+                     "graph_matches_eager": same, "loss_first": first, "loss_last": float(loss.double().sum()),
                      "loss_last_float64": float(np.mean(r64 * r64))}
-        log(f"  linreg {name}: {us:.1f} us/step, loss {first:.3g} -> {out[name]['loss_last']:.3g} "
-            f"(float64 {out[name]['loss_last_float64']:.3g})")
+        log(f"  linreg {name}: {us:.1f} us/step ({us_graph:.1f} from a graph, same bits: {same}), "
+            f"loss {first:.3g} -> {out[name]['loss_last']:.3g} (float64 {out[name]['loss_last_float64']:.3g})")
     # float64 gradient descent on the binary32 data, for context
     X, y_neg, W0, _ = inputs.linreg_inputs(n, d, 1, np.float32, seed=0)
     X64, y64, w = X.astype(np.float64), -y_neg.astype(np.float64), W0[0].astype(np.float64)
@@ -529,7 +549,8 @@ def bench_linreg(torch, mcf, inputs, steps=3000):
         w = w - lr * (2.0 / n) * (X64.T @ r)
     r = X64 @ w - y64
     out["float64_reference_loss_last"] = float(np.mean(r * r))
-    out["workload"] = f"n = {n}, d = {d}, lr = {lr}, {steps} steps; one mc_linreg_gd_step call per step"
+    out["workload"] = (f"n = {n}, d = {d}, lr = {lr}, {steps} steps; one mc_linreg_gd_step call per step, "
+                       f"eager and replayed from a HIP graph of 100 captured steps")
     return out
 
 
