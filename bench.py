@@ -568,7 +568,7 @@ def main():
                     help="also run one 1 GiB device-to-device copy (reference for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py: this build runs on one GPU only; the MC product shards by output blocks "
+        print("bench.py: this library runs on one GPU only; the MC product shards by output blocks "
               "with no communication, so there is no multi-GPU path to measure", file=sys.stderr)
         sys.exit(2)
 
