@@ -675,9 +675,9 @@ static hipError_t mm_launch(const MmArgs<T> &g, int64_t batches, const void *A, 
   } else {
     if constexpr (BT)  // MC-Linear: two rows of x per lane share each weight value
       return mm_launch_tile<T, NC, AMC, BMC, BT, 2, 1, SR_SUFFIX, SR_SUFFIX>(g, batches, A, B, C, s);
-    // nc = 2: 32-step LDS tiles halve the per-tile staging and barriers, which weigh
-    // more against its short steps (8% faster on 1024^3; flat or slower at nc >= 3)
-    constexpr int KT = NC == 2 ? 32 : 16;
+    // 32-step LDS tiles halve the per-tile staging and barriers (1024^3: nc = 2 8%
+    // faster than 16 steps, nc = 3 4% at eight wavefronts per SIMD; 64 steps slower)
+    constexpr int KT = NC <= 3 ? 32 : 16;
     return mm_launch_tile<T, NC, AMC, BMC, BT, 1, 1, SR_SUFFIX, SR_SUFFIX, KT, PRUNE>(g, batches, A, B, C, s);
   }
 }
