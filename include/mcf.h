@@ -32,6 +32,10 @@
  * Streams.  Work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and
  *   runs asynchronously; nothing synchronises.  Calls on different streams are
  *   independent.  The library is reentrant.
+ * Graph capture.  A call launches kernels only (no allocation, memset or
+ *   synchronisation), so it may be captured into a HIP graph on `stream` -- except
+ *   the first binary16 mc_exp call on a device, which builds the exponential table and
+ *   waits for it; make that call once before capturing.
  * Aliasing.  Elementwise calls allow `out` to be exactly `x` or `y` (in place);
  *   any other overlap of out with an input is rejected (MCF_E_ALIAS).  Matrix calls
  *   reject any overlap of the output with an input.
