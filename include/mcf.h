@@ -9,10 +9,11 @@
  * Conventions shared by every entry point
  * ---------------------------------------
  * Memory.  All tensor pointers are DEVICE pointers owned by the caller; the library
- *   allocates nothing per call and keeps no state besides a per-device binary16
- *   exponential table (128 KiB, built on the first mc_exp call on a device).  Calls
- *   that need scratch memory (mc_matmul_splitk, mc_matmul_exact, mc_linreg_gd_step)
- *   take a caller-owned workspace.
+ *   allocates nothing per call and keeps no state besides two static per-device
+ *   arrays: a binary16 exponential table (128 KiB, built on the first mc_exp call on
+ *   a device) and the 8 MiB scratch of mc_matmul_splitk_noalloc.  Calls that need
+ *   scratch memory (mc_matmul_splitk, mc_matmul_exact, mc_linreg_gd_step) take a
+ *   caller-owned workspace.
  * Layout.  Dense, component-major ("planar"): component c of element i of an MC
  *   array of n elements is at element offset c*n + i.  A plain tensor is one plane.
  *   Matrices are row-major inside each plane.  The paper's interleaved layout
@@ -67,7 +68,8 @@ typedef enum {
   MCF_E_DTYPE = -4, /* unknown format, or an operation not provided for it */
   MCF_E_ALIAS = -5, /* output overlaps an input in a way that is not allowed */
   MCF_E_HIP = -6,   /* the HIP runtime reported an error */
-  MCF_E_ARG = -7    /* any other invalid argument (operand kinds, mode) */
+  MCF_E_ARG = -7,   /* any other invalid argument (operand kinds, mode) */
+  MCF_E_SCRATCH = -8 /* the call needs more than the library's static scratch */
 } mcf_status;
 
 /* Addition (Section 2.1; Appendix A.2.1).
@@ -206,6 +208,25 @@ int mc_addmm(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, 
  * M * N below 2^31. */
 int mc_matmul_splitk(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B,
                      int b_mc, int64_t slices, void *workspace, int64_t workspace_bytes, void *C, void *stream);
+
+/* Allocation-free form of mc_matmul_splitk, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).  Same arguments, result and rules as mc_matmul_splitk, but the partial
+ * tree roots go to a static per-device scratch array inside the library (8 MiB,
+ * held by every device the library runs on until the process ends) instead of a
+ * caller workspace; the call allocates nothing.
+ * Limit: calls whose mc_matmul_splitk_workspace(...) exceeds 8 MiB (8388608 bytes)
+ *   return MCF_E_SCRATCH and launch nothing.  With the default slice count the roots
+ *   take at most 0.25 MiB (binary64, nc = 4, MC x MC), so the limit binds only for
+ *   large explicit slice counts on many outputs.
+ * Sharing: every call on a device uses that device's one scratch array, so calls on
+ *   one device that overlap in time (different streams, or different host threads)
+ *   race and give undefined results; serialise them.  The contents left by earlier
+ *   calls do not matter (nothing is read before it is written).
+ * The device is the one that runs `stream` (the current device for NULL).  The first
+ * call on a device looks up the array's device address (no allocation). */
+int mc_matmul_splitk_noalloc(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc,
+                             const void *B, int b_mc, int64_t slices, void *C, void *stream);
 
 /* Default slice count of mc_matmul_splitk, a function of the shape only: enough
  * slices for about 2^18 lanes in total (ceil(2^18 / (M N))), at most K / 8 (so a

@@ -19,7 +19,7 @@ import os
 
 __all__ = [
     "mc_add", "mc_mul", "mc_div", "mc_exp", "mc_renorm", "mc_matmul", "mc_matmul_splitk",
-    "mc_matmul_splitk_slices", "mc_matmul_splitk_workspace", "mc_linear_fwd", "mc_status_str",
+    "mc_matmul_splitk_slices", "mc_matmul_splitk_workspace", "mc_matmul_splitk_noalloc", "mc_linear_fwd", "mc_status_str",
     "mc_matmul_batched", "mc_bmm", "mc_addmm", "matmul_mcn", "mc_mul_slow", "mc_square", "mc_matmul_pruned",
     "mc_matmul_exact", "mc_matmul_exact_workspace", "mc_linreg_workspace", "mc_linreg_gd_step",
     "mc_linear_fwd_exact", "lib", "LIB_PATH", "MCFError",
@@ -60,6 +60,8 @@ def lib() -> ctypes.CDLL:
         L.mc_matmul.argtypes = [ci, ci, i64, i64, i64, vp, ci, vp, ci, vp, vp]
         L.mc_matmul_splitk.restype = ci
         L.mc_matmul_splitk.argtypes = [ci, ci, i64, i64, i64, vp, ci, vp, ci, i64, vp, i64, vp, vp]
+        L.mc_matmul_splitk_noalloc.restype = ci
+        L.mc_matmul_splitk_noalloc.argtypes = [ci, ci, i64, i64, i64, vp, ci, vp, ci, i64, vp, vp]
         L.mc_matmul_splitk_slices.restype = i64
         L.mc_matmul_splitk_slices.argtypes = [i64, i64, i64]
         L.mc_matmul_splitk_workspace.restype = i64
@@ -97,7 +99,7 @@ def mc_status_str(status: int) -> str:
 def _check(status: int, what: str):
     if status != 0:
         msg = f"{what}: {mc_status_str(status)}"
-        if status in (-1, -2, -3, -4, -5, -7):
+        if status in (-1, -2, -3, -4, -5, -7, -8):
             raise ValueError(msg)
         raise MCFError(msg)
 
@@ -310,6 +312,17 @@ def mc_matmul_splitk(A, B, *, nc: int, a_mc: bool = True, b_mc: bool = True, sli
     st = lib().mc_matmul_splitk(code, nc, M, N, K, _dev(A3, "A"), int(bool(a_mc)), _dev(B3, "B"), int(bool(b_mc)),
                                 int(slices), wp, wn, _dev(out, "out"), _stream(A))
     _check(st, "mc_matmul_splitk")
+    return out
+
+
+def mc_matmul_splitk_noalloc(A, B, *, nc: int, a_mc: bool = True, b_mc: bool = True, slices: int = 0, out=None):
+    """mc_matmul_splitk without a workspace: the library's static per-device scratch
+    (8 MiB) holds the partial tree roots, so nothing is allocated when `out` is
+    given.  Raises ValueError (MCF_E_SCRATCH) when the call needs more scratch."""
+    A3, B3, M, N, K, out = _mm_operands(A, B, nc, a_mc, b_mc, out)
+    st = lib().mc_matmul_splitk_noalloc(_dtype_code(A), nc, M, N, K, _dev(A3, "A"), int(bool(a_mc)), _dev(B3, "B"),
+                                        int(bool(b_mc)), int(slices), _dev(out, "out"), _stream(A))
+    _check(st, "mc_matmul_splitk_noalloc")
     return out
 
 

@@ -345,6 +345,30 @@ int mc_matmul_splitk(int dtype, int nc, int64_t M, int64_t N, int64_t K, const v
       mcf::launch_matmul_splitk(dtype, nc, M, N, K, A, a_mc, B, b_mc, S, workspace, C, (hipStream_t)stream));
 }
 
+int mc_matmul_splitk_noalloc(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc,
+                             const void *B, int b_mc, int64_t slices, void *C, void *stream) {
+  int64_t S = 0;
+  int st = splitk_check(dtype, nc, M, N, K, a_mc, b_mc, slices, &S);
+  if (st != MCF_OK) return st;
+  if (M == 0 || N == 0) return MCF_OK;
+  if (!C || (K > 0 && (!A || !B))) return MCF_E_NULL;
+  const int64_t es = elem_size(dtype);
+  const int64_t cb = nc * M * N * es, ab = (a_mc ? nc : 1) * M * K * es, bb = (b_mc ? nc : 1) * K * N * es;
+  if (overlap(C, cb, A, ab) || overlap(C, cb, B, bb)) return MCF_E_ALIAS;
+  if (K == 0)  // every output is +0
+    return hip_status(mcf::launch_matmul(dtype, nc, M, N, 0, A, a_mc, B, b_mc, 0, nullptr, C, (hipStream_t)stream));
+  const int64_t wb = splitk_workspace_bytes(dtype, nc, M, N, K, a_mc, b_mc, S);
+  if (wb > mcf::SPLITK_SCRATCH_BYTES) return MCF_E_SCRATCH;
+  void *scratch = nullptr;
+  if (wb > 0) {
+    const hipError_t e = mcf::splitk_scratch((hipStream_t)stream, &scratch);
+    if (e != hipSuccess) return MCF_E_HIP;
+    // the static scratch is library memory, so it cannot overlap A, B or C
+  }
+  return hip_status(
+      mcf::launch_matmul_splitk(dtype, nc, M, N, K, A, a_mc, B, b_mc, S, scratch, C, (hipStream_t)stream));
+}
+
 int64_t mc_matmul_exact_workspace(int dtype, int nc, int64_t M, int64_t N, int64_t K) {
   int st = exact_check(dtype, nc, M, N, K, 1, 1, 0);
   if (st != MCF_OK) return st;
@@ -438,6 +462,7 @@ const char *mc_status_str(int status) {
     case MCF_E_ALIAS: return "MCF_E_ALIAS: output overlaps an input";
     case MCF_E_HIP: return "MCF_E_HIP: HIP runtime error";
     case MCF_E_ARG: return "MCF_E_ARG: invalid argument";
+    case MCF_E_SCRATCH: return "MCF_E_SCRATCH: the call needs more scratch than the library's static 8 MiB";
   }
   return "unknown status";
 }

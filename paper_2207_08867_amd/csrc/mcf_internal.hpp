@@ -62,6 +62,11 @@ void splitk_shape(int64_t S, int *KS, int *G);
 int64_t splitk_roots(int64_t S);
 hipError_t launch_matmul_splitk(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc,
                                 const void *B, int b_mc, int64_t S, void *W, void *C, hipStream_t stream);
+// Size of the static per-device scratch that mc_matmul_splitk_noalloc uses in place of
+// a workspace, and its device address on the device of `stream` (looked up once per
+// device).
+constexpr int64_t SPLITK_SCRATCH_BYTES = (int64_t)8 << 20;
+hipError_t splitk_scratch(hipStream_t stream, void **ptr);
 
 // Exact binary16 product on the int8 matrix cores (exact.hip).  b_trans: B stored as
 // [planes][N][K].  bias: [nc][N] MC row added exactly before the split, or null.  W: a

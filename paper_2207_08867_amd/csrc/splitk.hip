@@ -24,6 +24,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "mcf_arith.hpp"
 #include "mcf_internal.hpp"
 #include "mm_steps.hpp"
@@ -306,6 +308,48 @@ hipError_t launch_matmul_splitk(int dtype, int nc, int64_t M, int64_t N, int64_t
   if (dtype == 0) return sk_dispatch<_Float16>(nc, M, N, K, A, a_mc, B, b_mc, S, W, C, stream);
   if (dtype == 2) return sk_dispatch<double>(nc, M, N, K, A, a_mc, B, b_mc, S, W, C, stream);
   return sk_dispatch<float>(nc, M, N, K, A, a_mc, B, b_mc, S, W, C, stream);
+}
+
+// Static scratch of the allocation-free K-split entry point: the partial tree roots
+// of one call live here instead of in a caller workspace.  Each device holds its own
+// copy for the life of the process.  In host code `scratch` names a host-side
+// stand-in, not device memory: the device address is looked up once per device with
+// hipGetSymbolAddress and only that address is ever passed to a kernel.
+__device__ __align__(256) unsigned char scratch[SPLITK_SCRATCH_BYTES];
+
+namespace {
+constexpr int SCRATCH_MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[SCRATCH_MAX_DEVICES] = {};
+}  // namespace
+
+// Device address of `scratch` on the device that runs `stream` (the current device
+// for the null stream); the lookup runs with that device current, once per device.
+hipError_t splitk_scratch(hipStream_t stream, void **ptr) {
+  int dev = 0, cur = 0;
+  hipError_t e = hipGetDevice(&cur);
+  if (e != hipSuccess) return e;
+  dev = cur;
+  if (stream != nullptr) {
+    e = hipStreamGetDevice(stream, &dev);
+    if (e != hipSuccess) return e;
+  }
+  if (dev < 0 || dev >= SCRATCH_MAX_DEVICES) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    if (dev != cur && (e = hipSetDevice(dev)) != hipSuccess) return e;
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (dev != cur) {
+      const hipError_t r = hipSetDevice(cur);
+      if (e == hipSuccess) e = r;
+    }
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 }  // namespace mcf

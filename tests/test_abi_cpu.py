@@ -10,6 +10,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "mcf.h")
 
 MCF_OK, MCF_E_NULL, MCF_E_NC, MCF_E_SHAPE, MCF_E_DTYPE, MCF_E_ALIAS, MCF_E_HIP, MCF_E_ARG = 0, -1, -2, -3, -4, -5, -6, -7
+MCF_E_SCRATCH = -8
 
 
 def declared_functions():
@@ -34,7 +35,7 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_status_strings(L):
-    for code in range(-7, 1):
+    for code in range(-8, 1):
         s = L.mc_status_str(code).decode()
         assert s.startswith("MCF_")
     assert L.mc_status_str(-99).decode() == "unknown status"
@@ -129,3 +130,33 @@ def test_validation_splitk(L):
     assert f(1, 3, 4, 4, 4096, a, 1, b, 0, 1024, P(0x300000 + 4), need, c, None) == MCF_E_ALIAS
     assert f(1, 3, 4, 4, 4096, a, 1, b, 0, 1024, a, need, c, None) == MCF_E_ALIAS
     assert f(1, 3, 4, 4, 4096, a, 1, b, 0, 16, None, 0, P(0x100000 + 8), None) == MCF_E_ALIAS
+
+
+def test_validation_splitk_noalloc(L):
+    """The allocation-free K-split call validates like mc_matmul_splitk and refuses
+    calls whose tree roots exceed its static 8 MiB scratch, before any HIP call."""
+    a, b, c = P(0x100000), P(0x200000), P(0x300000)
+    f = L.mc_matmul_splitk_noalloc
+    f.restype = ctypes.c_int
+    f.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, P, ctypes.c_int, P,
+                  ctypes.c_int, ctypes.c_int64, P, P]
+    ws = L.mc_matmul_splitk_workspace
+    ws.restype = ctypes.c_int64
+    ws.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
+                   ctypes.c_int, ctypes.c_int64]
+    assert f(1, 3, 4, 4, 4096, a, 0, b, 0, 16, c, None) == MCF_E_ARG
+    assert f(1, 7, 4, 4, 4096, a, 1, b, 0, 16, c, None) == MCF_E_NC
+    assert f(5, 3, 4, 4, 4096, a, 1, b, 0, 16, c, None) == MCF_E_DTYPE
+    assert f(1, 3, 4, 4, -1, a, 1, b, 0, 16, c, None) == MCF_E_SHAPE
+    assert f(1, 3, 4, 4, 4096, a, 1, b, 0, (1 << 20) + 1, c, None) == MCF_E_ARG
+    assert f(1, 3, 0, 4, 4096, None, 1, None, 0, 16, None, None) == MCF_OK
+    assert f(1, 3, 4, 4, 4096, None, 1, b, 0, 16, c, None) == MCF_E_NULL
+    assert f(1, 3, 4, 4, 4096, a, 1, b, 0, 16, P(0x100000 + 8), None) == MCF_E_ALIAS
+    # 4 x 4096 outputs at 2^20 slices: 4112 roots of 3 x 16384 binary32 components
+    need = ws(1, 3, 4, 4096, 1 << 20, 1, 0, 1 << 20)
+    assert need == 4112 * 3 * 16384 * 4 > 8 << 20
+    far = [P(k << 40) for k in (1, 2, 3)]  # operands of several GiB must not overlap
+    assert f(1, 3, 4, 4096, 1 << 20, far[0], 1, far[1], 0, 1 << 20, far[2], None) == MCF_E_SCRATCH
+    # the largest roots the default slice count asks for fit with room to spare
+    assert ws(2, 4, 1, 1023, 1 << 30, 1, 1, 0) == 261888 < 8 << 20
+    assert L.mc_status_str(MCF_E_SCRATCH).decode().startswith("MCF_E_SCRATCH")
