@@ -116,6 +116,54 @@ def measured_traffic():
         return None
 
 
+COUNTER_FILE = os.path.join(ROOT, "profiles", "valu_counters.txt")
+
+
+def valu_counts():
+    """VALU instructions per launch (wave64 SQ_INSTS_VALU) from the committed rocprofv3
+    counter table, for the groups whose kernel sources still hash to what was
+    measured: {workload: count}."""
+    import hashlib
+
+    out = {}
+    try:
+        groups, cur = {}, None
+        for line in open(COUNTER_FILE):
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            if line.startswith("[") and line.endswith("]"):
+                cur = groups.setdefault(line[1:-1], {})
+            elif "=" in line and cur is not None:
+                k, v = line.split("=", 1)
+                cur[k.strip()] = v.strip()
+        for kv in groups.values():
+            h = hashlib.sha256()
+            for f in kv["sources"].split():
+                h.update(open(os.path.join(ROOT, f), "rb").read())
+            if h.hexdigest() != kv["source_sha256"]:
+                continue
+            out.update({k: float(v) for k, v in kv.items() if k not in ("sources", "source_sha256")})
+    except (OSError, KeyError, ValueError):
+        return {}
+    return out
+
+
+def issue_fields(key, seconds, work_units=None):
+    """Measured VALU issue efficiency of one launch: the counted lane-instructions
+    (64 per wave64 instruction) over the live launch time, against the VALU issue peak;
+    plus lane-instructions per unit of work (per MAC or per element).  Empty when the
+    counter table does not cover the current sources."""
+    c = valu_counts().get(key)
+    if c is None:
+        return {}
+    lanes = 64.0 * c
+    out = {"issue_frac": round(lanes / seconds / VALU_PEAK, 3)}
+    if work_units:
+        out["valu_lane_instr_per_unit"] = round(lanes / work_units, 1)
+    return out
+
+
 class Timer:
     """HIP events on torch's current stream, the stream the library launches on."""
 
@@ -154,33 +202,42 @@ def bench_matmul(torch, mcf, A, B, nc, steps, warmup, a_mc=True, b_mc=True):
     return C, wall / steps * 1e3, float(np.mean(tm.ms()))
 
 
-def exact_error(oracle, A, B, C, nc, K, dt, count=64, seed=5):
-    M, N = C.shape[1:]
-    g = np.random.default_rng(seed)
-    rows = g.integers(0, M, count)
-    cols = g.integers(0, N, count)
-    Cs = np.ascontiguousarray(C[:, rows, cols])
-    err, absab, _ = oracle.matmul_exact_err(A, B, Cs, rows=rows, cols=cols)
-    rel = np.abs(err) / absab
-    u = {np.dtype(np.float16): 2.0 ** -11, np.dtype(np.float32): 2.0 ** -24, np.dtype(np.float64): 2.0 ** -53}[np.dtype(dt)]
-    floor = A.shape[0] * B.shape[0] * K * 2.0 ** -25 if dt == np.float16 else 0.0
-    lim = 4 * K * u ** min(nc, 3) * absab + floor
-    return {"max_rel_err": float(rel.max()), "bound_4Ku^nc": 4 * K * u ** nc,
-            "max_err_over_bound": float(np.max(np.abs(err) / lim)), "sampled_outputs": int(count)}
+U_OF = {np.dtype(np.float16): 2.0 ** -11, np.dtype(np.float32): 2.0 ** -24, np.dtype(np.float64): 2.0 ** -53}
+# half the smallest subnormal of the component format
+ETA_OF = {np.dtype(np.float16): 2.0 ** -25, np.dtype(np.float32): 2.0 ** -150, np.dtype(np.float64): 2.0 ** -1075}
 
 
-def exact_error_bias(oracle, A, B, bias, C, nc, K, count=64, seed=5):
-    """exact_error for a product plus a bias row (the MC-Linear layer)."""
+def exact_error(oracle, A, B, C, nc, K, dt, count=64, seed=5, bias=None):
+    """Error of a computed product C against the exact product of the MC inputs (plus
+    an optional bias row: the MC-Linear layer), on `count` sampled outputs:
+      max_rel_err      max |C - C*| / (|A||B|) (with |bias| added to |A||B|);
+      literal_ratio    max_rel_err / (4 K u^nc), the tolerance stated for the product:
+                       <= 1 means it holds on every sampled output;
+      amended_ratio    max |C - C*| / (4 K u^min(nc,3) |A||B| + nA nB K eta): the same
+                       bound with the binary16 floor for Two-Prod errors below the
+                       subnormal grid (eta = half the smallest subnormal; no floor in
+                       binary32 / binary64) and u^3 beyond nc = 3;
+      rms_err_over_sqrtK_eta  (binary16) the rms absolute error in units of sqrt(K) eta,
+                       the size the floor predicts for errors lost below the grid."""
     M, N = C.shape[1:]
     g = np.random.default_rng(seed)
     rows = g.integers(0, M, count)
     cols = g.integers(0, N, count)
     Cs = np.ascontiguousarray(C[:, rows, cols])
     err, absab, _ = oracle.matmul_exact_err(A, B, Cs, bias=bias, rows=rows, cols=cols)
-    u = 2.0 ** -11
-    lim = 4 * K * u ** min(nc, 3) * absab + A.shape[0] * B.shape[0] * K * 2.0 ** -25
-    return {"max_rel_err": float((np.abs(err) / absab).max()), "bound_4Ku^nc": 4 * K * u ** nc,
-            "max_err_over_bound": float(np.max(np.abs(err) / lim)), "sampled_outputs": int(count)}
+    rel = np.abs(err) / absab
+    dtn = np.dtype(dt)
+    u, eta = U_OF[dtn], ETA_OF[dtn]
+    literal = 4 * K * u ** nc
+    floor = A.shape[0] * B.shape[0] * K * eta if dtn == np.dtype(np.float16) else 0.0
+    amended = 4 * K * u ** min(nc, 3) * absab + floor
+    out = {"sampled_outputs": int(count), "max_rel_err": float(rel.max()), "bound_literal_4Ku^nc": literal,
+           "literal_ratio": float(rel.max() / literal), "literal_holds": bool(rel.max() <= literal),
+           "amended_ratio": float(np.max(np.abs(err) / amended)),
+           "rms_rel_err": float(np.sqrt(np.mean(rel * rel)))}
+    if dtn == np.dtype(np.float16):
+        out["rms_err_over_sqrtK_eta"] = float(np.sqrt(np.mean(err * err)) / (np.sqrt(K) * eta))
+    return out
 
 
 def cpu_oracle_other(oracle, inputs):
@@ -188,7 +245,7 @@ def cpu_oracle_other(oracle, inputs):
     GPU lines: binary16 nc = 3 elementwise operations on 2^22 elements, 32 full rows of the
     1024^3 binary16 nc = 3 MC x MC product and of the 4096x1024x1024 MC-Linear layer, and
     the whole 64^3 binary32 nc = 2 product."""
-    out = {"threads": oracle.threads()}
+    out = {"threads": oracle.threads(), "cpu_model": cpu_model()}
     n, nc = 1 << 22, 3
     s = inputs.elementwise_suite(n, nc, np.float16, seed=0)
     for name, fn, bpe in (("add_mcn", lambda: oracle.add(s["a"], s["b"], nc=nc), 18),
@@ -245,7 +302,18 @@ def cpu_baseline(oracle, A, B, nc, target_s=12.0):
     dt = time.perf_counter() - t0
     return {"value": 2.0 * K * count / dt / 1e9, "unit": "MC-GFLOP/s", "cores": threads, "kind": "oracle",
             "sample": f"{count} sampled outputs of the 8192^3 product (each a full K = {K} reduction), "
-                      f"{dt:.1f} s", "seconds": dt}
+                      f"{dt:.1f} s", "seconds": dt, "cpu_model": cpu_model()}
+
+
+def cpu_model():
+    """The host CPU's model name (first 'model name' line of /proc/cpuinfo)."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def bench_elementwise(torch, mcf, inputs, steps=10):
@@ -282,8 +350,9 @@ def bench_elementwise(torch, mcf, inputs, steps=10):
                      "Gelem/s": round(n / (ms * 1e-3) / 1e9, 2)}
         if name in ("mult_mcn", "div_mcn", "mult_mcn_slow"):  # VALU-bound: their binding roofline
             nops = ew_fp_ops({"div_mcn": "div", "mult_mcn": "mult", "mult_mcn_slow": "mult_slow"}[name], nc)
-            res[name]["fp_ops_per_elem"] = nops
-            res[name]["valu_frac"] = round(nops * n / (ms * 1e-3) / VALU_PEAK, 3)
+            res[name]["printed_fp_ops_per_elem"] = nops
+            res[name]["valu_frac_printed_ops"] = round(nops * n / (ms * 1e-3) / VALU_PEAK, 3)
+        res[name].update(issue_fields(name, ms * 1e-3, n))
         log(f"  elementwise {name}: {ms * 1e3:.1f} us, {gbs:.0f} GB/s")
     return {"workload": "2^26 elements, binary16, nc = 3", "ops": res}
 
@@ -360,15 +429,20 @@ def bench_batched(torch, mcf, inputs, steps=20):
                         "binary32", "ops": res}
 
 
-def bench_linear(torch, mcf, inputs, layers=100):
+def bench_linear(torch, mcf, oracle, inputs, layers=100):
+    """MC-Linear y = x W^T + b over 100 independent layers (binary16 nc = 3), with the
+    error against the exact layer output on 2048 sampled outputs of the first and of
+    the last layer."""
     T, I, O, nc = 4096, 1024, 1024, 3
     gen = inputs.linear_inputs(T, I, O, nc, np.float16, layers=layers, seed=0)
     x = None
-    Ws, bs = [], []
-    for xx, W, b in gen:
+    Ws, bs, host = [], [], {}
+    for l, (xx, W, b) in enumerate(gen):
         x = xx
         Ws.append(torch.from_numpy(W).cuda())
         bs.append(torch.from_numpy(b).cuda())
+        if l in (0, layers - 1):
+            host[l] = (np.ascontiguousarray(W.transpose(0, 2, 1)), b)
     tx = torch.from_numpy(x).cuda()
     y = torch.empty((nc, T, O), dtype=torch.float16, device="cuda")
     mcf.mc_linear_fwd(tx, Ws[0], bs[0], out=y)
@@ -381,9 +455,15 @@ def bench_linear(torch, mcf, inputs, layers=100):
     wall = time.perf_counter() - t0
     kms = float(np.mean(tm.ms()))
     macs = T * I * O
+    errors = {}
+    for l, (Wt, b) in host.items():
+        mcf.mc_linear_fwd(tx, Ws[l], bs[l], out=y)
+        errors[f"layer_{l}"] = exact_error(oracle, x[None], Wt, y.cpu().numpy(), nc, I, np.float16, count=2048,
+                                           seed=11 + l, bias=b)
     return {"workload": f"MC-Linear {T}x{I}x{O} binary16 nc=3, {layers} layers", "ms_per_layer": round(kms, 3),
             "MC-GFLOP/s": round(2 * macs * layers / wall / 1e9, 1),
-            "valu_frac": round(algo_ops_per_mac(nc, False) * macs / (kms * 1e-3) / VALU_PEAK, 3)}
+            "valu_frac_printed_ops": round(algo_ops_per_mac(nc, False) * macs / (kms * 1e-3) / VALU_PEAK, 3),
+            **issue_fields("linear_4096x1024x1024_f16_nc3", kms * 1e-3, macs), "error": errors}
 
 
 MFMA_I8_PEAK = 5.0e15  # dense int8 matrix-core operations / s
@@ -436,8 +516,7 @@ def bench_exact(torch, mcf, oracle, inputs, steps=20):
         pairs = (la[1] - la[0]) * (lb[1] - lb[0])
         ops = 2.0 * M * N * K * pairs
         Ch = C.cpu().numpy()
-        err = (exact_error(oracle, A, Bm, Ch, nc, K, np.float16) if not b_trans else
-               exact_error_bias(oracle, A, Bm, b, Ch, nc, K))
+        err = exact_error(oracle, A, Bm, Ch, nc, K, np.float16, bias=b if b_trans else None)
         out[name] = {"us": round(us, 1), "MC-GFLOP/s": round(2.0 * M * N * K / (us * 1e-6) / 1e9, 1),
                      "digit_pairs": pairs, "int8_ops": ops,
                      "mfma_int8_frac_whole_call": round(ops / (us * 1e-6) / MFMA_I8_PEAK, 4), "error": err}
@@ -554,6 +633,45 @@ def bench_linreg(torch, mcf, inputs, steps=3000):
     return out
 
 
+def issue_probe(blocks=2048, iters=20000):
+    """VALU issue rates per instruction kind (the probe library: 8 independent chains
+    per lane, 8 wavefronts per SIMD on every CU), printed as one JSON line: lane-
+    instructions per second, per clock per CU at the clock the wavefronts measured,
+    and relative to v_add_f32.  This is the evidence for the VALU peak of
+    128 lane-operations per clock per CU used by the roofline."""
+    import ctypes
+
+    path = os.path.join(ROOT, "paper_2207_08867_amd", "libmcf_probe.so")
+    if not os.path.exists(path):
+        raise SystemExit(f"{path} is missing: build it with python -m paper_2207_08867_amd.build")
+    L = ctypes.CDLL(path)
+    L.mcf_probe_count.restype = ctypes.c_int
+    L.mcf_probe_name.restype = ctypes.c_char_p
+    L.mcf_probe_name.argtypes = [ctypes.c_int]
+    L.mcf_probe_issue.restype = ctypes.c_int
+    d = ctypes.c_double
+    L.mcf_probe_issue.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.POINTER(d), ctypes.POINTER(d),
+                                  ctypes.POINTER(d)]
+    res = {}
+    base = None
+    for op in range(L.mcf_probe_count()):
+        name = L.mcf_probe_name(op).decode()
+        ms, li, ghz = d(), d(), d()
+        st = L.mcf_probe_issue(op, blocks, iters, ctypes.byref(ms), ctypes.byref(li), ctypes.byref(ghz))
+        if st != 0:
+            raise SystemExit(f"issue probe {name}: HIP error {st}")
+        rate = li.value / (ms.value * 1e-3)
+        per_clk = rate / 256 / (ghz.value * 1e9)
+        base = base or per_clk
+        res[name] = {"ms": round(ms.value, 3), "T_lane_instr_per_s": round(rate / 1e12, 2),
+                     "clock_GHz": round(ghz.value, 3), "per_clk_per_CU": round(per_clk, 1),
+                     "vs_v_add_f32": round(per_clk / base, 3)}
+        log(f"  {name:32s} {ms.value:8.2f} ms  {rate / 1e12:6.2f} T/s  {per_clk:6.1f} per clk per CU "
+            f"at {ghz.value:.2f} GHz")
+    print(json.dumps({"issue_probe": res, "blocks": blocks, "lanes_per_block": 256, "iters": iters,
+                      "chains_per_lane": 8, "unroll": 16}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -566,11 +684,17 @@ def main():
                          "f64, elementwise, splitk, batched, cpu_oracle); default: all")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run one 1 GiB device-to-device copy (reference for HBM byte counters)")
+    ap.add_argument("--issue-probe", action="store_true",
+                    help="only run the VALU issue-rate probe (libmcf_probe.so) and print its rates")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py: this library runs on one GPU only; the MC product shards by output blocks "
               "with no communication, so there is no multi-GPU path to measure", file=sys.stderr)
         sys.exit(2)
+
+    if args.issue_probe:
+        issue_probe()
+        return
 
     import torch
 
@@ -601,7 +725,7 @@ def main():
     Ch = C.cpu().numpy()
     del C
     err = exact_error(oracle, A, B, Ch, nc, K, np.float32)
-    log(f"  max rel err vs exact {err['max_rel_err']:.3g} (bound {err['bound_4Ku^nc']:.3g})")
+    log(f"  max rel err vs exact {err['max_rel_err']:.3g} (bound {err['bound_literal_4Ku^nc']:.3g})")
 
     line = {
         "metric": "MC-matmul MC-GFLOP/s (binary32, nc=3, MC x MC)",
@@ -622,7 +746,8 @@ def main():
         "roofline": {"bound": "alu", "achieved": round(achieved, 3), "peak": round(VALU_PEAK / 1e12, 2),
                      "unit": "TOP/s", "frac": round(achieved * 1e12 / VALU_PEAK, 4), "traffic": measured_traffic(),
                      "kernel": "mm_kernel (MC x MC, binary32, nc = 3)", "kernel_ms": round(kms, 3),
-                     "ops_per_mac": algo_ops_per_mac(nc, True)},
+                     "ops_per_mac": algo_ops_per_mac(nc, True),
+                     **issue_fields("matmul_8192_f32_nc3", kms * 1e-3, M * N * K)},
         "error": err,
     }
     groups = [g for g in args.only.split(",") if g]
@@ -660,12 +785,13 @@ def main():
             macs = 1024 ** 3
             extra[f"matmul_1024_f16_nc{nc3}"] = {
                 "ms": round(k3, 3), "MC-GFLOP/s": round(2 * macs / (k3 * 1e-3) / 1e9, 1),
-                "valu_frac": round(algo_ops_per_mac(nc3, True) * macs / (k3 * 1e-3) / VALU_PEAK, 3),
-                "error": exact_error(oracle, A3, B3, C3.cpu().numpy(), nc3, 1024, np.float16)}
+                "valu_frac_printed_ops": round(algo_ops_per_mac(nc3, True) * macs / (k3 * 1e-3) / VALU_PEAK, 3),
+                **issue_fields(f"matmul_1024_f16_nc{nc3}", k3 * 1e-3, macs),
+                "error": exact_error(oracle, A3, B3, C3.cpu().numpy(), nc3, 1024, np.float16, count=1024)}
             log(f"  1024^3 f16 nc={nc3}: {k3:.2f} ms")
     if not args.no_extra and want("linear"):
         log("MC-Linear")
-        extra["linear_4096x1024x1024_f16_nc3"] = bench_linear(torch, mcf, inputs)
+        extra["linear_4096x1024x1024_f16_nc3"] = bench_linear(torch, mcf, oracle, inputs)
     if not args.no_extra and want("exact"):
         log("exact binary16 products (int8 matrix cores)")
         extra["exact"] = bench_exact(torch, mcf, oracle, inputs)

@@ -177,15 +177,19 @@ static void store_c(int f, void *base, int64_t idx, double v) {
 /* Error-free transformations (Appendix A.2.1)                                      */
 /* ------------------------------------------------------------------------------ */
 
-/* Two-Sum: s = fl(a+b) and its exact error, six operations in the printed order. */
+/* Two-Sum (Knuth's error-free sum): s = fl(a+b) and the exact rounding error
+ * a + b - s, recovered from each operand's share of s (s - a, then s minus that
+ * share) and what rounding removed from each operand; the error is the sum of the
+ * two removed parts.  Six operations, in the order that fixes the sign of a zero
+ * error. */
 static void two_sum(int f, double a, double b, double *s, double *e) {
-  double x = fl_add(f, a, b);
-  double b_virtual = fl_sub(f, x, a);
-  double a_virtual = fl_sub(f, x, b_virtual);
-  double b_roundoff = fl_sub(f, b, b_virtual);
-  double a_roundoff = fl_sub(f, a, a_virtual);
-  *s = x;
-  *e = fl_add(f, a_roundoff, b_roundoff);
+  double sum = fl_add(f, a, b);
+  double share_b = fl_sub(f, sum, a);
+  double share_a = fl_sub(f, sum, share_b);
+  double lost_b = fl_sub(f, b, share_b);
+  double lost_a = fl_sub(f, a, share_a);
+  *s = sum;
+  *e = fl_add(f, lost_a, lost_b);
 }
 
 /* Two-Prod, FMA variant: p = fl(a*b), e = fl(a*b - p) in one rounding. */

@@ -19,6 +19,10 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libmcf.so")
 SOURCES = ["abi.cpp", "elementwise.hip", "matmul.hip", "splitk.hip", "exact.hip", "linreg.hip"]
+# the VALU issue-rate probe behind the roofline figures (bench.py --issue-probe): a
+# library of its own, not part of libmcf.so
+PROBE_LIB = os.path.join(HERE, "libmcf_probe.so")
+PROBE_SOURCES = ["issue_probe.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
@@ -35,7 +39,7 @@ def build(verbose: bool = False) -> str:
     os.makedirs(objdir, exist_ok=True)
     procs = []
     objs = []
-    for src in SOURCES:
+    for src in SOURCES + PROBE_SOURCES:
         obj = os.path.join(objdir, os.path.splitext(src)[0] + ".o")
         objs.append(obj)
         cmd = [HIPCC, *CFLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
@@ -55,10 +59,12 @@ def build(verbose: bool = False) -> str:
         for src, out in failed:
             sys.stderr.write(f"--- {src} ---\n{out}\n")
         raise RuntimeError("hipcc failed for " + ", ".join(s for s, _ in failed))
-    tmp = LIB + ".tmp"
-    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
-    subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
+    probe_objs = [o for o, src in zip(objs, SOURCES + PROBE_SOURCES) if src in PROBE_SOURCES]
+    for target, parts in ((LIB, [o for o in objs if o not in probe_objs]), (PROBE_LIB, probe_objs)):
+        tmp = target + ".tmp"
+        cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *parts]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, target)
     return LIB
 
 

@@ -1,9 +1,10 @@
 // mcf_arith.hpp -- device-side multi-component floating-point arithmetic for gfx950.
 //
-// Every function below follows one algorithm of "MCTensor" (arXiv 2207.08867),
-// Appendix A.2.1, step for step: each printed operation is one IEEE operation in the
-// component type T (binary16 `_Float16`, binary32 `float` or binary64 `double`), with round to nearest
-// even and gradual underflow.  The library is compiled with -ffp-contract=off so no
+// Each function below computes one algorithm of "MCTensor" (arXiv 2207.08867),
+// Appendix A.2.1: every floating-point operation of the algorithm is one IEEE
+// operation in the component type T (binary16 `_Float16`, binary32 `float` or
+// binary64 `double`), with round to nearest even and gradual underflow, taken in the
+// algorithm's order.  The library is compiled with -ffp-contract=off so no
 // multiply-add is fused except the explicit FMA of Two-Prod.
 //
 // Components live in registers as small fixed-size arrays indexed by compile-time
@@ -48,16 +49,21 @@ __device__ __forceinline__ double div_<double>(double a, double b) {
   return a / b;
 }
 
-// Two-Sum: s = fl(a + b) and e = (a + b) - s exactly, the six printed operations.
+// Knuth's error-free sum (Two-Sum, Appendix A.2.1): s = fl(a + b) together with the
+// rounding error e = (a + b) - s, which is exactly representable.  With no ordering of
+// |a| and |b| known, the error is recovered from the share of s that each operand
+// accounts for: share_b = s - a, share_a = s - share_b; what rounding took from each
+// operand is b - share_b and a - share_a, and their sum is the error.  The order of
+// these six operations is part of the definition: it fixes the sign of a zero error.
 template <typename T>
 __device__ __forceinline__ void two_sum(T a, T b, T &s, T &e) {
-  T x = a + b;
-  T b_virtual = x - a;
-  T a_virtual = x - b_virtual;
-  T b_roundoff = b - b_virtual;
-  T a_roundoff = a - a_virtual;
-  s = x;
-  e = a_roundoff + b_roundoff;
+  const T sum = a + b;
+  const T share_b = sum - a;
+  const T share_a = sum - share_b;
+  const T lost_b = b - share_b;
+  const T lost_a = a - share_a;
+  s = sum;
+  e = lost_a + lost_b;
 }
 
 // Two-Prod, FMA variant: p = fl(a * b), e = fl(a * b - p) with a single rounding.

@@ -2,9 +2,11 @@
 
 Each output is accumulated over k in MM-MCN order on the GPU as in the oracle, so
 the comparison is bitwise.  The error against the exact product of the MC inputs
-is checked as well: max_ij |C_ij - C*_ij| / (|A||B|)_ij <= 4 K u^nc, plus in
-binary16 a floor of nA nB K 2^-25 for Two-Prod errors that fall below the
-subnormal grid.  Small cases span several 32x32 tiles with ragged edges; the
+is checked as well: max_ij |C_ij - C*_ij| / (|A||B|)_ij <= 4 K u^nc as written
+for the workloads (64^3 binary32 nc = 2, 1024^3 binary16 nc = 2, the MC-Linear
+layers, 8192^3 binary32 nc = 3); elsewhere, and for 1024^3 binary16 nc = 3, with a
+floor of nA nB K 2^-25 for Two-Prod errors that fall below the binary16 subnormal
+grid.  Small cases span several 32x32 tiles with ragged edges; the
 full-size workloads are checked on sampled outputs.
 """
 import numpy as np
@@ -29,14 +31,16 @@ def mcf():
     return m
 
 
-def check_bound(orc, A, B, C, nc, K, dt, rows=None, cols=None, bias=None):
+def check_bound(orc, A, B, C, nc, K, dt, rows=None, cols=None, bias=None, literal=False):
     """Error against the exact product.  ScalingN and Add-MCN round their level-1
     carry, fl(e1 + e2), whose error is of order u^3 of the operands, so beyond
-    nc = 3 the attainable accuracy stays at u^3: the bound uses u^min(nc, 3)."""
+    nc = 3 the attainable accuracy stays at u^3: the bound uses u^min(nc, 3).
+    literal=True checks the product's stated tolerance exactly as written,
+    |C - C*| <= 4 K u^nc (|A||B|), with no binary16 floor."""
     err, absab, _ = orc.matmul_exact_err(A, B, C, rows=rows, cols=cols, bias=bias)
     u = U[dt]
-    floor = A.shape[0] * B.shape[0] * K * 2.0 ** -25 if dt == np.float16 else 0.0
-    lim = 4 * K * u ** min(nc, 3) * absab + floor
+    floor = A.shape[0] * B.shape[0] * K * 2.0 ** -25 if dt == np.float16 and not literal else 0.0
+    lim = 4 * K * u ** (nc if literal else min(nc, 3)) * absab + floor
     ratio = np.abs(err) / np.where(lim > 0, lim, 1)
     assert (np.abs(err) <= lim).all(), f"bound exceeded: worst ratio {ratio.max():.3g}"
     return float(np.max(np.abs(err) / np.where(absab > 0, absab, 1)))
@@ -72,23 +76,49 @@ def test_config_64_fp32_nc2_exact(mcf, orc):
     A, B = inputs.matmul_uniform(64, 64, 64, 2, np.float32, seed=0)
     got = to_host(mcf.mc_matmul(to_dev(A), to_dev(B), nc=2))
     assert_bits(got, orc.matmul(A, B, nc=2), "64^3")
-    worst = check_bound(orc, A, B, got, 2, 64, np.float32)
+    worst = check_bound(orc, A, B, got, 2, 64, np.float32, literal=True)
     assert worst < 2.0 ** -40
 
 
-@pytest.mark.parametrize("nc", [2, 3])
-def test_config_1024_fp16(mcf, orc, nc):
-    """M = N = K = 1024, binary16, entries N(0, 1/K): 512 sampled outputs bitwise
-    against the oracle and within the bound of the exact product."""
+def config_1024_fp16(mcf, orc, nc, samples=2044):
     n = 1024
     A, B = inputs.matmul_normal(n, n, n, nc, np.float16, seed=0)
     got = to_host(mcf.mc_matmul(to_dev(A), to_dev(B), nc=nc))
     g = np.random.default_rng(60 + nc)
-    rows = np.concatenate([g.integers(0, n, 500), [0, 0, n - 1, n - 1]])
-    cols = np.concatenate([g.integers(0, n, 500), [0, n - 1, 0, n - 1]])
+    rows = np.concatenate([g.integers(0, n, samples), [0, 0, n - 1, n - 1]])
+    cols = np.concatenate([g.integers(0, n, samples), [0, n - 1, 0, n - 1]])
     want = orc.matmul(A, B, nc=nc, rows=rows, cols=cols)
     assert_bits(got[:, rows, cols], want, f"1024^3 nc={nc}")
-    check_bound(orc, A, B, np.ascontiguousarray(got[:, rows, cols]), nc, n, np.float16, rows=rows, cols=cols)
+    return A, B, np.ascontiguousarray(got[:, rows, cols]), rows, cols
+
+
+def test_config_1024_fp16_nc2(mcf, orc):
+    """M = N = K = 1024, binary16, nc = 2, entries N(0, 1/K): 2048 sampled outputs
+    bitwise against the oracle and within the stated tolerance 4 K u^2 of the exact
+    product as written (no floor)."""
+    A, B, C, rows, cols = config_1024_fp16(mcf, orc, 2)
+    worst = check_bound(orc, A, B, C, 2, 1024, np.float16, rows=rows, cols=cols, literal=True)
+    assert worst < 4 * 1024 * 2.0 ** -22
+
+
+def test_config_1024_fp16_nc3(mcf, orc):
+    """The same at nc = 3.  binary16 components lose every Two-Prod error below the
+    subnormal grid (2^-24), which the paper names as the limit of MC binary16 (Section
+    2.4): the error is of the order of sqrt(K) eta (eta = 2^-25), about 11x the stated
+    4 K u^3 on these inputs, and no smaller than at nc = 2.  Checked: bitwise parity,
+    the bound with the binary16 floor nA nB K 2^-25, the rms errors of nc = 3 and
+    nc = 2 within a factor 2 of each other (the paper's observation that more binary16
+    components gain nothing), and that the literal tolerance is indeed missed here."""
+    A, B, C, rows, cols = config_1024_fp16(mcf, orc, 3)
+    worst3 = check_bound(orc, A, B, C, 3, 1024, np.float16, rows=rows, cols=cols)
+    A2, B2, C2, rows2, cols2 = config_1024_fp16(mcf, orc, 2)
+    check_bound(orc, A2, B2, C2, 2, 1024, np.float16, rows=rows2, cols=cols2)
+    rms = []
+    for a, b, c, r, q in ((A, B, C, rows, cols), (A2, B2, C2, rows2, cols2)):
+        err, _, _ = orc.matmul_exact_err(a, b, c, rows=r, cols=q)
+        rms.append(float(np.sqrt(np.mean(err * err))))
+    assert 0.5 <= rms[0] / rms[1] <= 2.0, rms
+    assert worst3 > 4 * 1024 * 2.0 ** -33  # the binary16 floor, not the component count, limits nc = 3
 
 
 @pytest.mark.parametrize("kinds", [(True, True), (True, False), (False, True)])
@@ -110,17 +140,18 @@ def test_large_output_tile_path(mcf, orc, kinds):
 
 def test_config_8192_fp32_nc3_sampled(mcf, orc):
     """The 8192^3 binary32 nc = 3 MC x MC workload in the benchmark's launch
-    configuration: 192 sampled outputs bitwise against the oracle and within
-    4 K u^3 of the exact product."""
+    configuration: 1024 sampled outputs bitwise against the oracle and within the
+    stated tolerance 4 K u^3 of the exact product."""
     n, nc = 8192, 3
     A, B = inputs.matmul_normal(n, n, n, nc, np.float32, seed=0)
     got = to_host(mcf.mc_matmul(to_dev(A), to_dev(B), nc=nc))
     g = np.random.default_rng(46)
-    rows = np.concatenate([g.integers(0, n, 188), [0, 0, n - 1, n - 1]])
-    cols = np.concatenate([g.integers(0, n, 188), [0, n - 1, 0, n - 1]])
+    rows = np.concatenate([g.integers(0, n, 1020), [0, 0, n - 1, n - 1]])
+    cols = np.concatenate([g.integers(0, n, 1020), [0, n - 1, 0, n - 1]])
     want = orc.matmul(A, B, nc=nc, rows=rows, cols=cols)
     assert_bits(got[:, rows, cols], want, "8192^3")
-    check_bound(orc, A, B, np.ascontiguousarray(got[:, rows, cols]), nc, n, np.float32, rows=rows, cols=cols)
+    check_bound(orc, A, B, np.ascontiguousarray(got[:, rows, cols]), nc, n, np.float32, rows=rows, cols=cols,
+                literal=True)
 
 
 @pytest.mark.parametrize("bias", [True, False])
@@ -132,20 +163,35 @@ def test_linear_small(mcf, orc, bias):
         assert_bits(got, want, f"linear {dt.__name__} bias={bias}")
 
 
-def test_linear_config_layer(mcf, orc):
-    """Batch 4096, in 1024, out 1024, binary16 nc = 3: the first layer's 512 sampled
-    outputs bitwise, and within 4 K u^3 (+ floor) of the exact result."""
+@pytest.fixture(scope="module")
+def linear_layers():
+    """Layers 0 and 99 of the MC-Linear workload (batch 4096, in 1024, out 1024,
+    binary16 nc = 3, 100 layers drawn in order from seed 0)."""
+    keep = {}
+    for l, (x, W, b) in enumerate(inputs.linear_inputs(4096, 1024, 1024, 3, np.float16, layers=100, seed=0)):
+        if l in (0, 99):
+            keep[l] = (x, W, b)
+    return keep
+
+
+@pytest.mark.parametrize("layer", [0, 99])
+def test_linear_config_layer(mcf, orc, linear_layers, layer):
+    """Batch 4096, in 1024, out 1024, binary16 nc = 3: 4096 sampled outputs of the
+    first and of the last layer bitwise against the oracle, and within the stated
+    tolerance 4 K u^3 (|x||W| + |b|) of the exact result as written (no floor: with a
+    plain x only about two of the three Two-Prods per step lose their error below the
+    subnormal grid, and |x||W| is about 20 times larger than in the 1024^3 product)."""
     T, I, O = 4096, 1024, 1024
-    x, W, b = next(inputs.linear_inputs(T, I, O, 3, np.float16, seed=0))
+    x, W, b = linear_layers[layer]
     got = to_host(mcf.mc_linear_fwd(to_dev(x), to_dev(W), to_dev(b)))
-    g = np.random.default_rng(71)
-    rows = g.integers(0, T, 512)
-    cols = g.integers(0, O, 512)
+    g = np.random.default_rng(71 + layer)
+    rows = np.concatenate([g.integers(0, T, 4092), [0, 0, T - 1, T - 1]])
+    cols = np.concatenate([g.integers(0, O, 4092), [0, O - 1, 0, O - 1]])
     want = orc.linear(x, W, b, nc=3, rows=rows, cols=cols)
-    assert_bits(got[:, rows, cols], want, "linear layer")
+    assert_bits(got[:, rows, cols], want, f"linear layer {layer}")
     Bm = np.ascontiguousarray(W.transpose(0, 2, 1))
     check_bound(orc, x[None], Bm, np.ascontiguousarray(got[:, rows, cols]), 3, I, np.float16, rows=rows, cols=cols,
-                bias=b)
+                bias=b, literal=True)
 
 
 def test_deterministic_and_errors(mcf):
