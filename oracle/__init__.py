@@ -80,6 +80,12 @@ def lib() -> ctypes.CDLL:
         L.mcf_oracle_matmul_exact_err.restype = ci
         L.mcf_oracle_matmul_exact_err.argtypes = [ci, ci, i64, i64, i64, vp, ci, vp, ci, vp, ci,
                                                   vp, vp, i64, vp, vp, vp, vp]
+        L.mcf_oracle_scaled_elementwise.restype = ci
+        L.mcf_oracle_scaled_elementwise.argtypes = [ci, ci, i64, vp, ci, vp, ci, vp]
+        L.mcf_oracle_scaled_matmul.restype = ci
+        L.mcf_oracle_scaled_matmul.argtypes = [ci, i64, i64, i64, vp, ci, vp, ci, vp, vp, i64, vp]
+        L.mcf_oracle_scaled_linear.restype = ci
+        L.mcf_oracle_scaled_linear.argtypes = [ci, i64, i64, i64, vp, vp, vp, vp, vp, i64, vp]
         L.mcf_oracle_exact_diff.restype = None
         L.mcf_oracle_exact_diff.argtypes = [ci, i64, vp, ci, vp, ci, vp]
         if L.mcf_oracle_check_env() != 0:
@@ -496,3 +502,87 @@ def exact_diff(x, y=None):
     out = np.empty(n)
     lib().mcf_oracle_exact_diff(fmt, n, _ptr(x), x.shape[0], _ptr(y), 0 if y is None else y.shape[0], _ptr(out))
     return out.reshape(x.shape[1:])
+
+
+# ---------------------------------------------------------------------------------
+# binary16 with scaled low components (reading SC1): component c of a stored value is
+# a binary16 number standing for 2^(-11 c) times itself
+# ---------------------------------------------------------------------------------
+
+SCALE_SHIFT = 11
+
+
+def unscale(x) -> np.ndarray:
+    """float64 values of the components of a scaled binary16 MC array (nc, ...):
+    component c times 2^(-11 c) (exact)."""
+    x = np.asarray(x, dtype=np.float16).astype(np.float64)
+    sh = np.ldexp(1.0, -SCALE_SHIFT * np.arange(x.shape[0])).reshape((-1,) + (1,) * (x.ndim - 1))
+    return x * sh
+
+
+def scaled_add(x, y, *, nc):
+    """Add-MCN of two scaled binary16 MC arrays (nc, n)."""
+    return _scaled_ew(0, x, y, nc, True, True)
+
+
+def scaled_mul(x, y, *, nc, x_mc=True, y_mc=False):
+    """ScalingN of a scaled binary16 MC array by a plain binary16 one (either order)."""
+    return _scaled_ew(1, x, y, nc, x_mc, y_mc)
+
+
+def _scaled_ew(op, x, y, nc, x_mc, y_mc):
+    x = _planar(x, np.float16)
+    y = _planar(y, np.float16)
+    n = x.shape[-1]
+    x = x.reshape((nc if x_mc else 1), n)
+    y = y.reshape((nc if y_mc else 1), n)
+    out = np.empty((nc, n), dtype=np.float16)
+    rc = lib().mcf_oracle_scaled_elementwise(op, nc, n, _ptr(x), int(x_mc), _ptr(y), int(y_mc), _ptr(out))
+    if rc != 0:
+        raise ValueError("oracle: bad arguments")
+    return out
+
+
+def scaled_matmul(A, B, *, nc, a_mc=True, b_mc=True, rows=None, cols=None):
+    """C = A x B on scaled binary16 planes (MC x plain, plain x MC: MM-MCN; MC x MC:
+    level-aligned parts of the linearity over B's components).  A: (nc|1, M, K),
+    B: (nc|1, K, N); returns (nc, M, N) or (nc, count)."""
+    A = _planar(A, np.float16)
+    B = _planar(B, np.float16)
+    if A.ndim == 2:
+        A = A[None]
+    if B.ndim == 2:
+        B = B[None]
+    M, K = A.shape[1:]
+    K2, N = B.shape[1:]
+    if K2 != K or A.shape[0] != (nc if a_mc else 1) or B.shape[0] != (nc if b_mc else 1):
+        raise ValueError("scaled_matmul: shape mismatch")
+    r, c, count = _positions(M, N, rows, cols)
+    out = np.empty((nc, count), dtype=np.float16)
+    rc = lib().mcf_oracle_scaled_matmul(nc, M, N, K, _ptr(A), int(a_mc), _ptr(B), int(b_mc), _ptr(r), _ptr(c),
+                                        count, _ptr(out))
+    if rc != 0:
+        raise ValueError("oracle: bad arguments")
+    return out.reshape(nc, M, N) if rows is None else out
+
+
+def scaled_linear(X, W, bias=None, *, nc, rows=None, cols=None):
+    """MC-Linear forward on scaled binary16 planes: X plain (T, I), W (nc, O, I),
+    bias (nc, O) or None."""
+    X = _planar(X, np.float16)
+    W = _planar(W, np.float16)
+    T, I = X.shape[-2:]
+    O = W.shape[1]
+    if W.shape != (nc, O, I):
+        raise ValueError("scaled_linear: shape mismatch")
+    if bias is not None:
+        bias = _planar(bias, np.float16)
+        if bias.shape != (nc, O):
+            raise ValueError("scaled_linear: bias shape mismatch")
+    r, c, count = _positions(T, O, rows, cols)
+    out = np.empty((nc, count), dtype=np.float16)
+    rc = lib().mcf_oracle_scaled_linear(nc, T, I, O, _ptr(X), _ptr(W), _ptr(bias), _ptr(r), _ptr(c), count,
+                                        _ptr(out))
+    if rc != 0:
+        raise ValueError("oracle: bad arguments")
+    return out.reshape(nc, T, O) if rows is None else out

@@ -776,6 +776,210 @@ int mcf_oracle_linear(int f, int nc, int64_t T, int64_t I, int64_t O, const void
 }
 
 /* ------------------------------------------------------------------------------ */
+/* binary16 components with scaled low components (reading SC1)                      */
+/* ------------------------------------------------------------------------------ */
+
+/* The paper observes that binary16 components cannot hold errors below the smallest
+ * subnormal, 2^-24, and that scaling the smaller components by a factor 2^-k would
+ * capture smaller errors (Section 2.4).  Reading SC1: component c of a stored value is
+ * a binary16 number y_c that stands for x_c = 2^(-11 c) y_c, so level c of a value lives
+ * on the binary16 grid scaled by 2^(-11 c) -- one binary16 precision below level c-1.
+ * The algorithms are the paper's, with every quantity given a level and every fl()
+ * taken in the binary16 format of the level of its result,
+ *     fl_l(v) = 2^(-11 l) RN16(2^(11 l) v):
+ *   - the terms an operation combines share one level l (component i of an operand
+ *     at slot level L is at level L + i; a product x_i v is at the sum of the levels);
+ *   - the rounding error of an operation at level l -- the second output of Two-Sum
+ *     or Two-Prod -- and the carry summed from such errors belong to level l + 1;
+ *   - Simple-Renorm moving a value to an earlier slot j rounds it into level j.
+ * Only operations whose operands pair equal levels are defined this way: Add-MCN,
+ * ScalingN, and the products and MC-Linear built from them. */
+#define SC_SHIFT 11
+
+static double fl_lv(int lv, double v) {
+  return ldexp(round_to(FMT_F16, ldexp(v, SC_SHIFT * lv), 0), -SC_SHIFT * lv);
+}
+
+/* Two-Sum at level lv: the six operations of Knuth's error-free sum, each rounded at
+ * level lv; the error they return is exact and is used at level lv + 1. */
+static void sc_two_sum(int lv, double a, double b, double *s, double *e) {
+  double sum = fl_lv(lv, a + b);
+  double share_b = fl_lv(lv, sum - a);
+  double share_a = fl_lv(lv, sum - share_b);
+  double lost_b = fl_lv(lv, b - share_b);
+  double lost_a = fl_lv(lv, a - share_a);
+  *s = sum;
+  *e = fl_lv(lv, lost_a + lost_b);
+}
+
+/* Two-Prod (FMA variant) at level lv: p = fl_lv(a b); the fused remainder a b - p,
+ * exact in double, is rounded once at level lv + 1. */
+static void sc_two_prod(int lv, double a, double b, double *p, double *e) {
+  *p = fl_lv(lv, a * b);
+  *e = fl_lv(lv + 1, a * b - *p);
+}
+
+/* Simple-Renorm of h[0..m-1] (h[i] at level L + i) into r slots: the first r non-zero
+ * values in order, the one landing in slot j rounded into level L + j; +0 padding. */
+static void sc_simple_renorm(const double *h, int m, int r, int L, double *b) {
+  int k = 0;
+  for (int i = 0; i < r; ++i) b[i] = 0.0;
+  for (int i = 0; i < m; ++i) {
+    if (h[i] != 0.0 && k < r) {
+      b[k] = fl_lv(L + k, h[i]);
+      k += 1;
+    }
+  }
+}
+
+/* ScalingN without expand: x[0..m-1] at levels L.. times a plain value v at level mu. */
+static void sc_scaling_n(const double *x, int m, int L, double v, int mu, double *out) {
+  double h[MAXC + 1];
+  double e = 0.0;
+  for (int i = 0; i < m; ++i) {
+    const int lv = L + i + mu;
+    double hp, e1, e2;
+    sc_two_prod(lv, x[i], v, &hp, &e1);
+    sc_two_sum(lv, hp, e, &h[i], &e2);
+    e = fl_lv(lv + 1, e1 + e2);
+  }
+  h[m] = e;
+  sc_simple_renorm(h, m + 1, m, L + mu, out);
+}
+
+/* Add-MCN of x and y, both n components at levels L.. */
+static void sc_add_mcn(const double *x, const double *y, int n, int L, double *out) {
+  double h[MAXC + 1];
+  double e = 0.0;
+  for (int i = 0; i < n; ++i) {
+    const int lv = L + i;
+    double hp, e1, e2;
+    sc_two_sum(lv, x[i], y[i], &hp, &e1);
+    sc_two_sum(lv, hp, e, &h[i], &e2);
+    e = fl_lv(lv + 1, e1 + e2);
+  }
+  h[n] = e;
+  sc_simple_renorm(h, n + 1, n, L, out);
+}
+
+static double sc_load(const void *base, int c, int64_t idx) {
+  return ldexp(f16_decode(((const uint16_t *)base)[idx]), -SC_SHIFT * c);
+}
+
+static void sc_store(void *base, int c, int64_t idx, double v) {
+  ((uint16_t *)base)[idx] = f16_encode(ldexp(v, SC_SHIFT * c));
+}
+
+/* Elementwise: op 0 = Add-MCN of two MC values, op 1 = ScalingN of an MC value by a
+ * plain one (either order).  Arrays are scaled binary16 planes [nc or 1][n]. */
+int mcf_oracle_scaled_elementwise(int op, int nc, int64_t n, const void *x, int x_mc, const void *y, int y_mc,
+                                  void *out) {
+  if (nc < 1 || nc > MAXC) return -1;
+  if (op == 0 && !(x_mc && y_mc)) return -1;
+  if (op == 1 && x_mc == y_mc) return -1;
+  if (op != 0 && op != 1) return -1;
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < n; ++i) {
+    double a[MAXC], b[MAXC], r[MAXC];
+    for (int c = 0; c < (x_mc ? nc : 1); ++c) a[c] = sc_load(x, c, (int64_t)c * n + i);
+    for (int c = 0; c < (y_mc ? nc : 1); ++c) b[c] = sc_load(y, c, (int64_t)c * n + i);
+    if (op == 0)
+      sc_add_mcn(a, b, nc, 0, r);
+    else if (x_mc)
+      sc_scaling_n(a, nc, 0, b[0], 0, r);
+    else
+      sc_scaling_n(b, nc, 0, a[0], 0, r);
+    for (int c = 0; c < nc; ++c) sc_store(out, c, (int64_t)c * n + i, r[c]);
+  }
+  return 0;
+}
+
+/* MM-MCN for one output over the first m components of the MC factor (A when a_mc,
+ * else B), the plain factor being component `bcomp` of B (at level bcomp) or the
+ * plain operand (level 0): acc = ScalingN(first term), then Add-MCN of each further
+ * ScalingN term in k order.  The accumulator's slot c is at level mu + c. */
+static void sc_mm_entry_plain(const mm_args *g, int m, int64_t i, int64_t j, int bcomp, double *acc) {
+  const int mu = (g->a_mc && g->b_mc) ? bcomp : 0;
+  for (int c = 0; c < m; ++c) acc[c] = 0.0;
+  for (int64_t k = 0; k < g->K; ++k) {
+    double mc[MAXC], term[MAXC], t[MAXC], v;
+    if (g->a_mc) {
+      for (int c = 0; c < m; ++c) mc[c] = sc_load(g->A, c, c * g->a_plane + i * g->lda_m + k * g->lda_k);
+      v = sc_load(g->B, bcomp, bcomp * g->b_plane + k * g->ldb_k + j * g->ldb_n);
+    } else {
+      for (int c = 0; c < m; ++c) mc[c] = sc_load(g->B, c, c * g->b_plane + k * g->ldb_k + j * g->ldb_n);
+      v = sc_load(g->A, 0, i * g->lda_m + k * g->lda_k);
+    }
+    sc_scaling_n(mc, m, 0, v, mu, term);
+    if (k == 0) {
+      for (int c = 0; c < m; ++c) acc[c] = term[c];
+    } else {
+      sc_add_mcn(acc, term, m, mu, t);
+      for (int c = 0; c < m; ++c) acc[c] = t[c];
+    }
+  }
+}
+
+/* One output.  MC x plain and plain x MC: MM-MCN.  MC x MC (reading SC1 with the
+ * linearity over B's components of the unscaled product): component b of B sits at
+ * level b, so its part A B^(b) has levels b, b+1, ...; the levels below the format's
+ * last one (nc - 1) are kept, i.e. the part is MM-MCN over the first nc - b
+ * components of A with nc - b components at levels b .. nc-1.  Each part, placed at
+ * its levels (b leading zero slots), is added left to right with Add-MCN:
+ *   C = P_0 (+) (0, P_1) (+) (0, 0, P_2) (+) ... */
+static void sc_mm_entry(const mm_args *g, int nc, int64_t i, int64_t j, double *out) {
+  sc_mm_entry_plain(g, nc, i, j, 0, out);
+  if (!(g->a_mc && g->b_mc)) return;
+  for (int b = 1; b < nc; ++b) {
+    double part[MAXC], y[MAXC], t[MAXC];
+    sc_mm_entry_plain(g, nc - b, i, j, b, part);
+    for (int c = 0; c < nc; ++c) y[c] = c < b ? 0.0 : part[c - b];
+    sc_add_mcn(out, y, nc, 0, t);
+    for (int c = 0; c < nc; ++c) out[c] = t[c];
+  }
+}
+
+/* C = A x B on scaled binary16 planes, at the `count` positions (as mcf_oracle_matmul). */
+int mcf_oracle_scaled_matmul(int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B,
+                             int b_mc, const int64_t *rows, const int64_t *cols, int64_t count, void *out) {
+  if (nc < 1 || nc > MAXC || (!a_mc && !b_mc)) return -1;
+  mm_args g = {FMT_F16, A, a_mc, B, b_mc, K, K, 1, N, 1, M * K, K * N};
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t t = 0; t < count; ++t) {
+    int64_t i = rows ? rows[t] : t / N;
+    int64_t j = rows ? cols[t] : t % N;
+    double r[MAXC];
+    sc_mm_entry(&g, nc, i, j, r);
+    for (int c = 0; c < nc; ++c) sc_store(out, c, (int64_t)c * count + t, r[c]);
+  }
+  return 0;
+}
+
+/* MC-Linear forward on scaled binary16 planes: Y[t][o] = MM-MCN over i of
+ * ScalingN(W[o][i], X[t][i]) (X plain, level 0), then Add-MCN with bias[o]. */
+int mcf_oracle_scaled_linear(int nc, int64_t T, int64_t I, int64_t O, const void *X, const void *W,
+                             const void *bias, const int64_t *rows, const int64_t *cols, int64_t count,
+                             void *out) {
+  if (nc < 1 || nc > MAXC) return -1;
+  mm_args g = {FMT_F16, X, 0, W, 1, I, I, 1, 1, I, T * I, O * I};
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t t = 0; t < count; ++t) {
+    int64_t i = rows ? rows[t] : t / O;
+    int64_t j = rows ? cols[t] : t % O;
+    double r[MAXC];
+    sc_mm_entry_plain(&g, nc, i, j, 0, r);
+    if (bias) {
+      double b[MAXC], s2[MAXC];
+      for (int c = 0; c < nc; ++c) b[c] = sc_load(bias, c, (int64_t)c * O + j);
+      sc_add_mcn(r, b, nc, 0, s2);
+      for (int c = 0; c < nc; ++c) r[c] = s2[c];
+    }
+    for (int c = 0; c < nc; ++c) sc_store(out, c, (int64_t)c * count + t, r[c]);
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------------ */
 /* Exact arithmetic checker                                                          */
 /* ------------------------------------------------------------------------------ */
 

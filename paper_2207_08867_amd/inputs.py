@@ -31,6 +31,25 @@ def split(x: np.ndarray, nc: int, dtype) -> np.ndarray:
     return out
 
 
+SCALE_SHIFT = 11  # level c of a scaled binary16 value is stored times 2^(11 c)
+
+
+def split_scaled(x: np.ndarray, nc: int) -> np.ndarray:
+    """Split float64 values into nc binary16 components with scaled low components:
+    c_0 = RN(x), and c_i = RN(2^(11 i) r_i) for the residual r_i = x - sum_{j<i}
+    2^(-11 j) c_j, so component i stands for 2^(-11 i) c_i.  Each residual is exact in
+    float64 (at most 44 bits are split off), so level i holds the next binary16
+    precision of x instead of underflowing below 2^-24."""
+    x = np.asarray(x, dtype=np.float64)
+    out = np.empty((nc,) + x.shape, dtype=np.float16)
+    r = x.copy()
+    with np.errstate(over="ignore"):
+        for c in range(nc):
+            out[c] = np.ldexp(r, SCALE_SHIFT * c).astype(np.float16)
+            r -= np.ldexp(out[c].astype(np.float64), -SCALE_SHIFT * c)
+    return out
+
+
 def expansion(g: np.random.Generator, shape, nc: int, dtype, scale: float = 1.0) -> np.ndarray:
     """MC values with every component in use (for formats where splitting a float64
     draw would leave the low components zero, such as binary64): c_0 ~ N(0, scale^2)
@@ -72,6 +91,15 @@ def matmul_normal(M, N, K, nc, dtype, seed=0):
     return A, B
 
 
+def matmul_normal_scaled(M, N, K, nc, seed=0):
+    """The same draws as matmul_normal, split into scaled binary16 components."""
+    g = rng(seed)
+    s = 1.0 / np.sqrt(K)
+    A = split_scaled(g.normal(0.0, s, (M, K)), nc)
+    B = split_scaled(g.normal(0.0, s, (K, N)), nc)
+    return A, B
+
+
 def elementwise_inputs(op: str, n: int, nc: int, dtype, seed=0):
     """Operands for the elementwise workload on n elements.
 
@@ -102,6 +130,18 @@ def linear_inputs(T, I, O, nc, dtype, layers=1, seed=0):
     for _ in range(layers):
         W = split(g.uniform(-lim, lim, (O, I)), nc, dtype)
         b = split(g.uniform(-lim, lim, (O,)), nc, dtype)
+        yield x, W, b
+
+
+def linear_inputs_scaled(T, I, O, nc, layers=1, seed=0):
+    """The MC-Linear workload's draws (as linear_inputs) with W and b split into
+    scaled binary16 components; x stays a plain binary16 tensor."""
+    g = rng(seed)
+    x = g.normal(0.0, 1.0, (T, I)).astype(np.float16)
+    lim = 1.0 / np.sqrt(I)
+    for _ in range(layers):
+        W = split_scaled(g.uniform(-lim, lim, (O, I)), nc)
+        b = split_scaled(g.uniform(-lim, lim, (O,)), nc)
         yield x, W, b
 
 
