@@ -525,6 +525,65 @@ def bench_exact(torch, mcf, oracle, inputs, steps=20):
     return out
 
 
+def bench_scaled(torch, mcf, oracle, inputs, steps=5):
+    """binary16 with scaled low components (component c stands for 2^(-11 c) times its
+    stored value): the 1024^3 MC x MC product at nc = 2 and 3 on the same draws as the
+    binary16 lines, and one 4096x1024x1024 MC-Linear layer at nc = 3, each with its
+    error against the exact result (the stated tolerance as written)."""
+    out = {}
+    for nc in (2, 3):
+        A, B = inputs.matmul_normal_scaled(1024, 1024, 1024, nc, seed=0)
+        tA, tB = torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda()
+        C = torch.empty((nc, 1024, 1024), dtype=torch.float16, device="cuda")
+        run = lambda: mcf.mc_matmul(tA, tB, nc=nc, out=C, scaled=True)
+        for _ in range(2):
+            run()
+        tm = Timer(torch)
+        for _ in range(steps):
+            tm.run(run)
+        ms = float(np.median(tm.ms()))
+        Ch = C.cpu().numpy()
+        g = np.random.default_rng(5)
+        rows, cols = g.integers(0, 1024, 1024), g.integers(0, 1024, 1024)
+        err, absab, _ = oracle.matmul_exact_err(oracle.unscale(A), oracle.unscale(B),
+                                                oracle.unscale(np.ascontiguousarray(Ch[:, rows, cols])),
+                                                rows=rows, cols=cols)
+        rel = np.abs(err) / absab
+        lit = 4 * 1024 * 2.0 ** (-11 * nc)
+        out[f"matmul_1024_f16s_nc{nc}"] = {
+            "ms": round(ms, 3), "MC-GFLOP/s": round(2 * 1024 ** 3 / (ms * 1e-3) / 1e9, 1),
+            "error": {"sampled_outputs": 1024, "max_rel_err": float(rel.max()), "bound_literal_4Ku^nc": lit,
+                      "literal_ratio": float(rel.max() / lit), "literal_holds": bool(rel.max() <= lit),
+                      "rms_rel_err": float(np.sqrt(np.mean(rel * rel)))}}
+        log(f"  scaled 1024^3 nc={nc}: {ms:.2f} ms, literal ratio {rel.max() / lit:.3g}")
+        del tA, tB, C
+    x, W, b = next(inputs.linear_inputs_scaled(4096, 1024, 1024, 3, seed=0))
+    tx, tW, tb = (torch.from_numpy(v).cuda() for v in (x, W, b))
+    y = torch.empty((3, 4096, 1024), dtype=torch.float16, device="cuda")
+    run = lambda: mcf.mc_linear_fwd(tx, tW, tb, out=y, scaled=True)
+    for _ in range(2):
+        run()
+    tm = Timer(torch)
+    for _ in range(steps):
+        tm.run(run)
+    ms = float(np.median(tm.ms()))
+    yh = y.cpu().numpy()
+    g = np.random.default_rng(6)
+    rows, cols = g.integers(0, 4096, 1024), g.integers(0, 1024, 1024)
+    Wt = np.ascontiguousarray(W.transpose(0, 2, 1))
+    err, absab, _ = oracle.matmul_exact_err(x[None].astype(np.float64), oracle.unscale(Wt),
+                                            oracle.unscale(np.ascontiguousarray(yh[:, rows, cols])),
+                                            bias=oracle.unscale(b), rows=rows, cols=cols)
+    rel = np.abs(err) / absab
+    lit = 4 * 1024 * 2.0 ** -33
+    out["linear_4096x1024x1024_f16s_nc3"] = {
+        "ms": round(ms, 3), "MC-GFLOP/s": round(2 * 4096 * 1024 * 1024 / (ms * 1e-3) / 1e9, 1),
+        "error": {"sampled_outputs": 1024, "max_rel_err": float(rel.max()), "literal_ratio": float(rel.max() / lit),
+                  "literal_holds": bool(rel.max() <= lit)}}
+    log(f"  scaled MC-Linear layer: {ms:.2f} ms, literal ratio {rel.max() / lit:.3g}")
+    return out
+
+
 def bench_f64(torch, mcf, oracle, inputs, steps=10):
     """binary64 components (the paper's MC float64): 2^26-element Add-MCN, ScalingN and
     Div-MCN at nc = 2 (HBM bandwidth; Div-MCN also against the binary64 VALU rate), and
@@ -681,7 +740,7 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--only", default="",
                     help="comma-separated groups of extra workloads to run (pruned, small, linear, exact, linreg, "
-                         "f64, elementwise, splitk, batched, cpu_oracle); default: all")
+                         "scaled, f64, elementwise, splitk, batched, cpu_oracle); default: all")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run one 1 GiB device-to-device copy (reference for HBM byte counters)")
     ap.add_argument("--issue-probe", action="store_true",
@@ -798,6 +857,9 @@ def main():
     if not args.no_extra and want("linreg"):
         log("linear-regression gradient descent")
         extra["linreg"] = bench_linreg(torch, mcf, inputs)
+    if not args.no_extra and want("scaled"):
+        log("binary16 with scaled low components")
+        extra["scaled"] = bench_scaled(torch, mcf, oracle, inputs)
     if not args.no_extra and want("f64"):
         log("binary64 components")
         extra["f64"] = bench_f64(torch, mcf, oracle, inputs)

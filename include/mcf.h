@@ -25,6 +25,19 @@
  *   correctly rounded; the binary16 and binary32 component exponentials are correctly
  *   rounded.  mc_exp does not take MCF_F64 (MCF_E_DTYPE); mc_matmul_exact takes
  *   MCF_F16 only.
+ *   MCF_F16S = binary16 components with scaled low components (Section 2.4 names
+ *   scaling the smaller components as the way past binary16's smallest subnormal):
+ *   component c is stored as the binary16 number y_c and stands for 2^(-11 c) y_c.
+ *   The algorithms are the same, with every quantity at a level and every rounding
+ *   taken in the binary16 format of its level, fl_l(v) = 2^(-11 l) RN16(2^(11 l) v):
+ *   the operands of an operation share a level (component i of an operand is at
+ *   level i; a product is at the sum of its factors' levels), the errors of Two-Sum
+ *   and Two-Prod and the carry built from them are at the next level, and a value
+ *   Simple-Renorm moves to an earlier slot j is rounded into level j.  Only
+ *   operations whose operands pair equal levels take MCF_F16S: mc_add (MC, MC
+ *   only), mc_mul (MC, T and T, MC only), mc_matmul (MC x MC by the level-aligned
+ *   parts described there) and mc_linear_fwd; every other call returns MCF_E_DTYPE.
+ *   Non-finite components are outside this format's contract.
  * Operand kinds.  Binary operations take an MC value and a plain tensor in either
  *   order, or two MC values (Section 2.1).  The flags x_mc / y_mc / a_mc / b_mc are 1
  *   for an MC operand of nc planes and 0 for a plain tensor of one plane; at least
@@ -58,7 +71,7 @@
 extern "C" {
 #endif
 
-typedef enum { MCF_F16 = 0, MCF_F32 = 1, MCF_F64 = 2 } mcf_dtype;
+typedef enum { MCF_F16 = 0, MCF_F32 = 1, MCF_F64 = 2, MCF_F16S = 3 } mcf_dtype;
 
 typedef enum {
   MCF_OK = 0,
@@ -138,6 +151,11 @@ int mc_renorm(int dtype, int nc_in, int nc_out, int64_t n, const void *x, void *
  * operands MC (not defined by the paper, whose matrix operators multiply an MC
  * matrix by a plain one) the product is taken by linearity over the components of
  * B: C = MM(A, B^(0)) (+) MM(A, B^(1)) (+) ... with (+) = Add-MCN.
+ * MCF_F16S, both operands MC: B^(b) is at level b, so the part A B^(b) has levels
+ * b, b+1, ..., of which the format keeps those below nc: the part is MM-MCN over the
+ * first nc - b components of A with nc - b components at levels b .. nc-1, and the
+ * parts, each placed at its levels (b leading zero components), are added left to
+ * right: C = P_0 (+) (0, P_1) (+) (0, 0, P_2) ...
  * A: [nc or 1][M][K], B: [nc or 1][K][N], C: [nc][M][N]. */
 int mc_matmul(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B,
               int b_mc, void *C, void *stream);

@@ -28,7 +28,7 @@ __all__ = [
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmcf.so")
 _lib = None
 
-MCF_F16, MCF_F32, MCF_F64 = 0, 1, 2
+MCF_F16, MCF_F32, MCF_F64, MCF_F16S = 0, 1, 2, 3
 
 
 class MCFError(RuntimeError):
@@ -110,6 +110,16 @@ def _torch():
     return torch
 
 
+def _code(t, scaled: bool) -> int:
+    """Format code of a tensor; scaled=True: binary16 with scaled low components
+    (component c stands for 2^(-11 c) times its stored value), float16 tensors only."""
+    if scaled:
+        if t.dtype != _torch().float16:
+            raise TypeError("scaled components need float16 tensors")
+        return MCF_F16S
+    return _dtype_code(t)
+
+
 def _dtype_code(t) -> int:
     torch = _torch()
     if t.dtype == torch.float16:
@@ -142,7 +152,7 @@ def _logical_shape(t, nc, is_mc, name):
     return tuple(t.shape)
 
 
-def _binary(fn_name, x, y, nc, x_mc, y_mc, out):
+def _binary(fn_name, x, y, nc, x_mc, y_mc, out, scaled=False):
     torch = _torch()
     if x.dtype != y.dtype or x.device != y.device:
         raise ValueError("operands must share dtype and device")
@@ -162,20 +172,22 @@ def _binary(fn_name, x, y, nc, x_mc, y_mc, out):
         out = torch.empty((nc,) + sx, dtype=x.dtype, device=x.device)
     elif out.shape != (nc,) + sx or out.dtype != x.dtype:
         raise ValueError("out has the wrong shape or dtype")
-    st = getattr(lib(), fn_name)(_dtype_code(x), nc, n, _dev(x, "x"), int(bool(x_mc)), _dev(y, "y"),
+    st = getattr(lib(), fn_name)(_code(x, scaled), nc, n, _dev(x, "x"), int(bool(x_mc)), _dev(y, "y"),
                                  int(bool(y_mc)), _dev(out, "out"), _stream(x))
     _check(st, fn_name)
     return out
 
 
-def mc_add(x, y, *, nc: int, x_mc: bool = True, y_mc: bool = True, out=None):
-    """Add-MCN for (MC, MC); Grow-ExpN for (MC, T) and (T, MC)."""
-    return _binary("mc_add", x, y, nc, x_mc, y_mc, out)
+def mc_add(x, y, *, nc: int, x_mc: bool = True, y_mc: bool = True, out=None, scaled: bool = False):
+    """Add-MCN for (MC, MC); Grow-ExpN for (MC, T) and (T, MC).  scaled=True: float16
+    components with scaled low components (MC, MC only)."""
+    return _binary("mc_add", x, y, nc, x_mc, y_mc, out, scaled)
 
 
-def mc_mul(x, y, *, nc: int, x_mc: bool = True, y_mc: bool = True, out=None):
-    """Mult-MCN (fast) for (MC, MC); ScalingN for (MC, T) and (T, MC)."""
-    return _binary("mc_mul", x, y, nc, x_mc, y_mc, out)
+def mc_mul(x, y, *, nc: int, x_mc: bool = True, y_mc: bool = True, out=None, scaled: bool = False):
+    """Mult-MCN (fast) for (MC, MC); ScalingN for (MC, T) and (T, MC).  scaled=True:
+    float16 components with scaled low components ((MC, T) and (T, MC) only)."""
+    return _binary("mc_mul", x, y, nc, x_mc, y_mc, out, scaled)
 
 
 def mc_div(x, y, *, nc: int, x_mc: bool = True, y_mc: bool = True, out=None):
@@ -259,10 +271,11 @@ def _mm_operands(A, B, nc, a_mc, b_mc, out):
     return A3, B3, M, N, K, out
 
 
-def mc_matmul(A, B, *, nc: int, a_mc: bool = True, b_mc: bool = True, out=None):
-    """C = A B in MM-MCN order.  A: (nc|1, M, K), B: (nc|1, K, N) -> (nc, M, N)."""
+def mc_matmul(A, B, *, nc: int, a_mc: bool = True, b_mc: bool = True, out=None, scaled: bool = False):
+    """C = A B in MM-MCN order.  A: (nc|1, M, K), B: (nc|1, K, N) -> (nc, M, N).
+    scaled=True: float16 components with scaled low components."""
     A3, B3, M, N, K, out = _mm_operands(A, B, nc, a_mc, b_mc, out)
-    st = lib().mc_matmul(_dtype_code(A), nc, M, N, K, _dev(A3, "A"), int(bool(a_mc)), _dev(B3, "B"),
+    st = lib().mc_matmul(_code(A, scaled), nc, M, N, K, _dev(A3, "A"), int(bool(a_mc)), _dev(B3, "B"),
                          int(bool(b_mc)), _dev(out, "out"), _stream(A))
     _check(st, "mc_matmul")
     return out
@@ -413,9 +426,10 @@ def mc_linear_fwd_exact(x, W, b=None, *, out=None, workspace=None):
     return out
 
 
-def mc_linear_fwd(x, W, b=None, *, out=None):
+def mc_linear_fwd(x, W, b=None, *, out=None, scaled: bool = False):
     """MC-Linear forward y = x W^T + b.  x: (batch, in) plain, W: (nc, out, in),
-    b: (nc, out) or None -> y: (nc, batch, out)."""
+    b: (nc, out) or None -> y: (nc, batch, out).  scaled=True: float16 W, b and y with
+    scaled low components (x is a plain float16 tensor)."""
     torch = _torch()
     nc, O, I = W.shape
     if x.dim() != 2 or x.shape[1] != I:
@@ -428,7 +442,7 @@ def mc_linear_fwd(x, W, b=None, *, out=None):
     elif out.shape != (nc, T, O) or out.dtype != W.dtype:
         raise ValueError("out has the wrong shape or dtype")
     bp = _dev(b, "b") if b is not None else None
-    st = lib().mc_linear_fwd(_dtype_code(W), nc, T, I, O, _dev(x, "x"), _dev(W, "W"), bp, _dev(out, "out"),
+    st = lib().mc_linear_fwd(_code(W, scaled), nc, T, I, O, _dev(x, "x"), _dev(W, "W"), bp, _dev(out, "out"),
                              _stream(W))
     _check(st, "mc_linear_fwd")
     return out

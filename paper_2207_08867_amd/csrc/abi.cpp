@@ -10,7 +10,7 @@ namespace {
 
 constexpr int MAX_NC = 4;
 
-int64_t elem_size(int dtype) { return dtype == MCF_F16 ? 2 : (dtype == MCF_F64 ? 8 : 4); }
+int64_t elem_size(int dtype) { return (dtype == MCF_F16 || dtype == MCF_F16S) ? 2 : (dtype == MCF_F64 ? 8 : 4); }
 
 bool overlap(const void *a, int64_t abytes, const void *b, int64_t bbytes) {
   if (abytes <= 0 || bbytes <= 0) return false;
@@ -60,6 +60,24 @@ int binary_op(int op, int dtype, int nc, int64_t n, const void *x, int x_mc, con
   const int64_t ob = nc * n * es, xb = (x_mc ? nc : 1) * n * es, yb = (y_mc ? nc : 1) * n * es;
   if (bad_alias(out, ob, x, xb) || bad_alias(out, ob, y, yb)) return MCF_E_ALIAS;
   return hip_status(mcf::launch_elementwise(dtype, op, nc, nc, n, x, x_mc, y, y_mc, out, (hipStream_t)stream));
+}
+
+// binary16 with scaled low components: Add-MCN of two MC operands (op EW_ADD) and
+// ScalingN of an MC operand by a plain one, in either order (op EW_MUL).  The other
+// operand kinds pair values of different levels and are not provided (MCF_E_DTYPE).
+int scaled_binary_op(int op, int nc, int64_t n, const void *x, int x_mc, const void *y, int y_mc, void *out,
+                     void *stream) {
+  if (nc < 1 || nc > MAX_NC) return MCF_E_NC;
+  if (n < 0 || n > ((int64_t)1 << 40)) return MCF_E_SHAPE;
+  if ((x_mc != 0 && x_mc != 1) || (y_mc != 0 && y_mc != 1) || (!x_mc && !y_mc)) return MCF_E_ARG;
+  if (op == mcf::EW_ADD ? !(x_mc && y_mc) : (x_mc && y_mc)) return MCF_E_DTYPE;
+  if (n == 0) return MCF_OK;
+  if (!x || !y || !out) return MCF_E_NULL;
+  const int64_t ob = nc * n * 2, xb = (x_mc ? nc : 1) * n * 2, yb = (y_mc ? nc : 1) * n * 2;
+  if (bad_alias(out, ob, x, xb) || bad_alias(out, ob, y, yb)) return MCF_E_ALIAS;
+  if (op == mcf::EW_MUL && !x_mc)  // the MC operand goes first
+    return hip_status(mcf::launch_scaled_elementwise(op, nc, n, y, x, out, (hipStream_t)stream));
+  return hip_status(mcf::launch_scaled_elementwise(op, nc, n, x, y, out, (hipStream_t)stream));
 }
 
 // Shared validation of the K-split product; *S receives the slice count used
@@ -123,11 +141,13 @@ extern "C" {
 
 int mc_add(int dtype, int nc, int64_t n, const void *x, int x_mc, const void *y, int y_mc, void *out,
            void *stream) {
+  if (dtype == MCF_F16S) return scaled_binary_op(mcf::EW_ADD, nc, n, x, x_mc, y, y_mc, out, stream);
   return binary_op(mcf::EW_ADD, dtype, nc, n, x, x_mc, y, y_mc, out, stream);
 }
 
 int mc_mul(int dtype, int nc, int64_t n, const void *x, int x_mc, const void *y, int y_mc, void *out,
            void *stream) {
+  if (dtype == MCF_F16S) return scaled_binary_op(mcf::EW_MUL, nc, n, x, x_mc, y, y_mc, out, stream);
   return binary_op(mcf::EW_MUL, dtype, nc, n, x, x_mc, y, y_mc, out, stream);
 }
 
@@ -178,7 +198,7 @@ int mc_renorm(int dtype, int nc_in, int nc_out, int64_t n, const void *x, void *
 
 int mc_matmul(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B,
               int b_mc, void *C, void *stream) {
-  if (dtype != MCF_F16 && dtype != MCF_F32 && dtype != MCF_F64) return MCF_E_DTYPE;
+  if (dtype != MCF_F16 && dtype != MCF_F32 && dtype != MCF_F64 && dtype != MCF_F16S) return MCF_E_DTYPE;
   if (nc < 1 || nc > MAX_NC) return MCF_E_NC;
   if ((a_mc != 0 && a_mc != 1) || (b_mc != 0 && b_mc != 1) || (!a_mc && !b_mc)) return MCF_E_ARG;
   if (M < 0 || N < 0 || K < 0) return MCF_E_SHAPE;
@@ -190,6 +210,9 @@ int mc_matmul(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A,
   const int64_t cb = nc * M * N * es;
   if (overlap(C, cb, A, (a_mc ? nc : 1) * M * K * es) || overlap(C, cb, B, (b_mc ? nc : 1) * K * N * es))
     return MCF_E_ALIAS;
+  if (dtype == MCF_F16S)
+    return hip_status(
+        mcf::launch_scaled_matmul(nc, M, N, K, A, a_mc, B, b_mc, 0, nullptr, C, (hipStream_t)stream));
   return hip_status(mcf::launch_matmul(dtype, nc, M, N, K, A, a_mc, B, b_mc, 0, nullptr, C, (hipStream_t)stream));
 }
 
@@ -437,7 +460,7 @@ int mc_linreg_gd_step(int dtype, int nc, int64_t n, int64_t d, const void *X, co
 
 int mc_linear_fwd(int dtype, int nc, int64_t batch, int64_t in, int64_t out, const void *x, const void *W,
                   const void *b, void *y, void *stream) {
-  if (dtype != MCF_F16 && dtype != MCF_F32 && dtype != MCF_F64) return MCF_E_DTYPE;
+  if (dtype != MCF_F16 && dtype != MCF_F32 && dtype != MCF_F64 && dtype != MCF_F16S) return MCF_E_DTYPE;
   if (nc < 1 || nc > MAX_NC) return MCF_E_NC;
   if (batch < 0 || in < 0 || out < 0) return MCF_E_SHAPE;
   if (batch > ((int64_t)1 << 20) || out > ((int64_t)1 << 30) || in > ((int64_t)1 << 40)) return MCF_E_SHAPE;
@@ -449,6 +472,8 @@ int mc_linear_fwd(int dtype, int nc, int64_t batch, int64_t in, int64_t out, con
   if (overlap(y, yb, x, batch * in * es) || overlap(y, yb, W, nc * out * in * es) ||
       (b && overlap(y, yb, b, nc * out * es)))
     return MCF_E_ALIAS;
+  if (dtype == MCF_F16S)
+    return hip_status(mcf::launch_scaled_matmul(nc, batch, out, in, x, 0, W, 1, 1, b, y, (hipStream_t)stream));
   return hip_status(mcf::launch_matmul(dtype, nc, batch, out, in, x, 0, W, 1, 1, b, y, (hipStream_t)stream));
 }
 

@@ -75,6 +75,15 @@ int64_t exact_workspace_bytes(int64_t M, int64_t N, int64_t K);
 hipError_t launch_matmul_exact(int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B,
                                int b_mc, int b_trans, const void *bias, void *W, void *C, hipStream_t stream);
 
+// binary16 with scaled low components (scaled.hip): component c stands for 2^(-11 c)
+// times its stored value.  Elementwise: op EW_ADD = Add-MCN of two MC operands, EW_MUL
+// = ScalingN of the MC operand x by the plain operand y.  Product: kinds as
+// launch_matmul (b_trans with a plain A only: MC-Linear), bias [nc][N] or null.
+hipError_t launch_scaled_elementwise(int op, int nc, int64_t n, const void *x, const void *y, void *out,
+                                     hipStream_t stream);
+hipError_t launch_scaled_matmul(int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B,
+                                int b_mc, int b_trans, const void *bias, void *C, hipStream_t stream);
+
 // One gradient-descent step of MC-Linear regression (linreg.hip).  s2n, s1n and neg_lr
 // are fl(2/n), fl(1/n) and fl(-lr), already values of the component format.  ws holds
 // linreg_workspace_bytes(...) bytes.

@@ -51,7 +51,7 @@ def test_validation_elementwise(L):
     for f in (L.mc_add, L.mc_mul, L.mc_div):
         assert f(0, 0, 10, x, 1, y, 1, o, None) == MCF_E_NC
         assert f(0, 5, 10, x, 1, y, 1, o, None) == MCF_E_NC
-        assert f(3, 3, 10, x, 1, y, 1, o, None) == MCF_E_DTYPE  # 3: no such format
+        assert f(4, 3, 10, x, 1, y, 1, o, None) == MCF_E_DTYPE  # 4: no such format
         assert f(0, 3, -1, x, 1, y, 1, o, None) == MCF_E_SHAPE
         assert f(0, 3, 10, x, 0, y, 0, o, None) == MCF_E_ARG
         assert f(0, 3, 10, x, 2, y, 1, o, None) == MCF_E_ARG
@@ -61,7 +61,7 @@ def test_validation_elementwise(L):
         assert f(1, 3, 10, P(0x10000), 1, y, 1, P(0x10004), None) == MCF_E_ALIAS
         # out overlapping a plain y that is shorter than out
         assert f(1, 3, 10, x, 1, P(0x30000), 0, o, None) == MCF_E_ALIAS
-    assert L.mc_exp(3, 3, 10, x, o, None) == MCF_E_DTYPE
+    assert L.mc_exp(4, 3, 10, x, o, None) == MCF_E_DTYPE
     assert L.mc_exp(2, 3, 10, x, o, None) == MCF_E_DTYPE  # binary64: no component exponential
     assert L.mc_exp(1, 3, 10, x, P(0x10004), None) == MCF_E_ALIAS
     assert L.mc_exp(0, 3, 0, None, None, None) == MCF_OK
@@ -160,3 +160,28 @@ def test_validation_splitk_noalloc(L):
     # the largest roots the default slice count asks for fit with room to spare
     assert ws(2, 4, 1, 1023, 1 << 30, 1, 1, 0) == 261888 < 8 << 20
     assert L.mc_status_str(MCF_E_SCRATCH).decode().startswith("MCF_E_SCRATCH")
+
+
+def test_scaled_format_rejections(L):
+    """binary16 with scaled low components (dtype 3) is provided for Add-MCN (MC, MC),
+    ScalingN, the product and MC-Linear only; every other call is MCF_E_DTYPE before
+    any HIP call."""
+    x, y, o = P(0x100000), P(0x200000), P(0x300000)
+    for name in ("mc_add", "mc_mul", "mc_div"):
+        f = getattr(L, name)
+        f.restype = ctypes.c_int
+        f.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int64, P, ctypes.c_int, P, ctypes.c_int, P, P]
+    assert L.mc_add(3, 3, 10, x, 1, y, 0, o, None) == MCF_E_DTYPE  # Grow-ExpN
+    assert L.mc_add(3, 3, 10, x, 0, y, 1, o, None) == MCF_E_DTYPE
+    assert L.mc_mul(3, 3, 10, x, 1, y, 1, o, None) == MCF_E_DTYPE  # Mult-MCN
+    assert L.mc_div(3, 3, 10, x, 1, y, 1, o, None) == MCF_E_DTYPE
+    assert L.mc_add(3, 3, 10, x, 0, y, 0, o, None) == MCF_E_ARG
+    assert L.mc_add(3, 5, 10, x, 1, y, 1, o, None) == MCF_E_NC
+    assert L.mc_add(3, 3, 0, None, 1, None, 1, None, None) == MCF_OK
+    assert L.mc_add(3, 3, 10, x, 1, P(0x100000 + 2), 1, x, None) == MCF_E_ALIAS
+    assert L.mc_exp(3, 3, 10, x, o, None) == MCF_E_DTYPE
+    assert L.mc_renorm(3, 3, 3, 10, x, o, 0, None) == MCF_E_DTYPE
+    assert L.mc_square(3, 3, 10, x, o, None) == MCF_E_DTYPE
+    assert L.mc_matmul_pruned(3, 3, 4, 4, 4, x, y, o, None) == MCF_E_DTYPE
+    assert L.mc_matmul(4, 3, 4, 4, 4, x, 1, y, 1, o, None) == MCF_E_DTYPE
+    assert L.mc_matmul(3, 3, 4, 4, 4, x, 1, y, 1, P(0x100000 + 8), None) == MCF_E_ALIAS
