@@ -33,8 +33,8 @@ _lib = None
 def build(force: bool = True) -> str:
     """Compile the oracle with gcc (no contraction, no fast-math, OpenMP)."""
     if force or not os.path.exists(_LIB_PATH):
-        cmd = ["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-fopenmp",
-               "-fPIC", "-shared", "-Wall", "-o", _LIB_PATH + ".tmp", _SRC, "-lm"]
+        cmd = ["gcc", "-O2", "-std=gnu11", "-ffp-contract=off", "-fno-fast-math", "-fopenmp",
+               "-fPIC", "-shared", "-Wall", "-o", _LIB_PATH + ".tmp", _SRC, "-lquadmath", "-lm"]
         subprocess.run(cmd, check=True)
         os.replace(_LIB_PATH + ".tmp", _LIB_PATH)
     return _LIB_PATH
@@ -86,6 +86,12 @@ def lib() -> ctypes.CDLL:
         L.mcf_oracle_scaled_matmul.argtypes = [ci, i64, i64, i64, vp, ci, vp, ci, vp, vp, i64, vp]
         L.mcf_oracle_scaled_linear.restype = ci
         L.mcf_oracle_scaled_linear.argtypes = [ci, i64, i64, i64, vp, vp, vp, vp, vp, i64, vp]
+        L.mcf_oracle_exp64_first.restype = None
+        L.mcf_oracle_exp64_first.argtypes = [i64, vp, vp, vp]
+        L.mcf_oracle_exp_mcn_given.restype = ci
+        L.mcf_oracle_exp_mcn_given.argtypes = [ci, ci, i64, vp, vp]
+        L.mcf_oracle_exp64_near_midpoints.restype = i64
+        L.mcf_oracle_exp64_near_midpoints.argtypes = [dbl, dbl, ctypes.c_uint64, i64, dbl, vp, i64]
         L.mcf_oracle_exact_diff.restype = None
         L.mcf_oracle_exact_diff.argtypes = [ci, i64, vp, ci, vp, ci, vp]
         if L.mcf_oracle_check_env() != 0:
@@ -239,8 +245,61 @@ def div(x, y, *, nc, x_mc=True, y_mc=True):
 
 
 def exp(x, *, nc):
-    """Exp-MCN."""
+    """Exp-MCN (binary64 components: component exponentials from fl_exp64)."""
+    if np.dtype(np.asarray(x).dtype) == np.float64:
+        x = _planar(x, np.float64)
+        n = x.shape[-1]
+        E = np.ascontiguousarray(fl_exp64(x.reshape(nc, n)))
+        out = np.empty((nc, n), dtype=np.float64)
+        if lib().mcf_oracle_exp_mcn_given(F64, nc, n, _ptr(E), _ptr(out)) != 0:
+            raise ValueError("oracle: bad arguments")
+        return out
     return elementwise(OP_EXP, x, nc=nc)
+
+
+def _exp64_decimal(x: float) -> float:
+    """e^x correctly rounded to binary64 from an 80-digit decimal evaluation (decimal's
+    exp is correctly rounded to the context precision; the conversion of its decimal
+    string to a binary64 number is correctly rounded too).  Raises if the decimal
+    value lies within 10^-70 (relative) of a binary64 rounding boundary, where the two
+    roundings could disagree."""
+    import decimal
+
+    with decimal.localcontext() as ctx:
+        ctx.prec = 80
+        ctx.Emin, ctx.Emax = -999999, 999999
+        v = decimal.Decimal(float(x)).exp()
+        r = float(v)
+        if r != 0.0 and np.isfinite(r):
+            for nb in (np.nextafter(r, np.inf), np.nextafter(r, -np.inf)):
+                if np.isfinite(nb):
+                    mid = (decimal.Decimal(r) + decimal.Decimal(float(nb))) / 2
+                    if abs(v - mid) <= abs(v) * decimal.Decimal("1e-70"):
+                        raise ArithmeticError(f"exp({x!r}) too close to a rounding boundary")
+    return r
+
+
+def fl_exp64(x) -> np.ndarray:
+    """Correctly rounded binary64 e^x, elementwise: binary128 evaluation with a 2^-100
+    margin test (C), the undecided arguments by 80-digit decimal arithmetic."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    flat = x.reshape(-1)
+    out = np.empty_like(flat)
+    unsure = np.zeros(flat.size, dtype=np.int32)
+    lib().mcf_oracle_exp64_first(flat.size, _ptr(flat), _ptr(out), _ptr(unsure))
+    for i in np.nonzero(unsure)[0]:
+        out[i] = _exp64_decimal(flat[i])
+    return out.reshape(x.shape)
+
+
+def exp64_near_midpoints(lo: float, hi: float, seed: int, tries: int, rel: float, max_out: int = 4096):
+    """Random binary64 x in [lo, hi] whose e^x lies within rel (relative) of a binary64
+    rounding boundary (test inputs that drive a correctly rounded exponential's slow
+    path).  Returns the inputs found (at most max_out)."""
+    out = np.zeros(max_out, dtype=np.float64)
+    n = int(lib().mcf_oracle_exp64_near_midpoints(float(lo), float(hi), int(seed), int(tries), float(rel),
+                                                  _ptr(out), max_out))
+    return out[:min(n, max_out)]
 
 
 def renorm(x, *, nc, nc_out=None, mode=0):

@@ -26,8 +26,11 @@
  *     remainder's sign used to break a tie (see fl_fma); binary64: the C library's
  *     fma, which rounds once.
  *   - binary64 components: every double operation above is already the correctly
- *     rounded binary64 result, and fl(.) is the identity on doubles.  No component
- *     exponential is provided for binary64 (Exp-MCN rejects it).
+ *     rounded binary64 result, and fl(.) is the identity on doubles.  The binary64
+ *     component exponential is e^x in binary128 (libquadmath's expq), accepted when a
+ *     2^-100 relative margin around it rounds to one binary64 value; the few other
+ *     arguments are decided in oracle/__init__.py with 80-digit decimal arithmetic, and
+ *     Exp-MCN then takes the component exponentials as inputs.
  *   - exp : the component exponential is taken to be correctly rounded (the paper
  *     calls torch.exp and fixes no accuracy); computed as fl(.) of a double
  *     (binary16) or long double (binary32) exponential.  Exhaustive pinning for
@@ -40,6 +43,7 @@
  * binary32 data as float.
  */
 #include <math.h>
+#include <quadmath.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -773,6 +777,83 @@ int mcf_oracle_linear(int f, int nc, int64_t T, int64_t I, int64_t O, const void
     scatter(f, out, nc, count, t, r);
   }
   return 0;
+}
+
+/* ------------------------------------------------------------------------------ */
+/* Correctly rounded binary64 exponential (first step) and Exp-MCN from given         */
+/* component exponentials                                                             */
+/* ------------------------------------------------------------------------------ */
+
+/* e^a in binary128, rounded to binary64 when every value within 2^-100 (relative) of it
+ * rounds to the same binary64 number; *unsure = 1 otherwise. */
+static double exp64_first(double a, int *unsure) {
+  *unsure = 0;
+  if (isnan(a)) return a;
+  if (a > 710.0) return INFINITY; /* e^710 exceeds the largest binary64 number */
+  if (a < -746.0) return 0.0;     /* e^-746 is below half the smallest subnormal */
+  __float128 q = expq((__float128)a);
+  __float128 d = q * (__float128)ldexp(1.0, -100);
+  double lo = (double)(q - d), hi = (double)(q + d);
+  if (lo != hi) *unsure = 1;
+  return (double)q;
+}
+
+void mcf_oracle_exp64_first(int64_t n, const double *x, double *out, int32_t *unsure) {
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < n; ++i) {
+    int u;
+    out[i] = exp64_first(x[i], &u);
+    unsure[i] = u;
+  }
+}
+
+/* Exp-MCN (Appendix A.2.1, reading E1) from the component exponentials E[c][i] (values
+ * of the format f): h = (E_0), then h = ScalingN(h, E_c) with expand. */
+int mcf_oracle_exp_mcn_given(int f, int nc, int64_t n, const void *E, void *out) {
+  if (nc < 1 || nc > MAXC) return -1;
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < n; ++i) {
+    double h[MAXC + 1], t[MAXC + 1];
+    int m = 1;
+    h[0] = load_c(f, E, i);
+    for (int c = 1; c < nc; ++c) {
+      scaling_n(f, h, m, load_c(f, E, (int64_t)c * n + i), 1, t);
+      m += 1;
+      for (int k = 0; k < m; ++k) h[k] = t[k];
+    }
+    for (int c = 0; c < nc; ++c) store_c(f, out, (int64_t)c * n + i, h[c]);
+  }
+  return 0;
+}
+
+/* Test-input search: random binary64 x uniform in [lo, hi] (a SplitMix64 sequence from
+ * seed) whose e^x lies within rel (relative, rel >> 2^-100) of a binary64 rounding
+ * boundary.  Writes up to max_out of them to out and returns how many were found. */
+int64_t mcf_oracle_exp64_near_midpoints(double lo, double hi, uint64_t seed, int64_t tries, double rel,
+                                        double *out, int64_t max_out) {
+  int64_t found = 0;
+#pragma omp parallel for schedule(static)
+  for (int64_t t = 0; t < tries; ++t) {
+    uint64_t z = seed + (uint64_t)t * 0x9e3779b97f4a7c15ull;
+    z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+    z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+    z = z ^ (z >> 31);
+    double x = lo + (hi - lo) * ((double)(z >> 11) * ldexp(1.0, -53));
+    __float128 q = expq((__float128)x);
+    double r = (double)q;
+    if (r == 0.0 || isinf(r)) continue;
+    __float128 up = ((__float128)r + (__float128)nextafter(r, INFINITY)) / 2;
+    __float128 dn = ((__float128)r + (__float128)nextafter(r, -INFINITY)) / 2;
+    __float128 d1 = fabsq(q - up), d2 = fabsq(q - dn);
+    __float128 d = d1 < d2 ? d1 : d2;
+    if (d < q * (__float128)rel) {
+      int64_t k;
+#pragma omp atomic capture
+      k = found++;
+      if (k < max_out) out[k] = x;
+    }
+  }
+  return found;
 }
 
 /* ------------------------------------------------------------------------------ */

@@ -13,6 +13,8 @@ hyperbolic models), against references that share none of its code:
 """
 from fractions import Fraction
 
+import os
+
 import numpy as np
 import pytest
 
@@ -116,6 +118,66 @@ def test_matmul_mc_bound(orc, nc):
             assert abs(float(e) - err[i * N + j]) <= 2.0 ** -50 * abs(float(e)) + 1e-300
 
 
-def test_exp_rejects_binary64(orc):
-    with pytest.raises(ValueError):
-        orc.exp(np.zeros((2, 4)), nc=2)
+def _decimal_exp(x):
+    """e^x from 90-digit decimal arithmetic, converted to binary64 (both steps correctly
+    rounded; the arguments used here are not within 10^-80 of a rounding boundary)."""
+    import decimal
+
+    with decimal.localcontext() as ctx:
+        ctx.prec = 90
+        ctx.Emin, ctx.Emax = -999999, 999999
+        return float(decimal.Decimal(float(x)).exp())
+
+
+def test_exp64_correctly_rounded_sample(orc):
+    """The binary64 component exponential against decimal arithmetic: the whole finite
+    range, the subnormal results, tiny arguments, boundaries and special values."""
+    g = np.random.default_rng(40)
+    xs = np.concatenate([g.uniform(-745.2, 709.8, 6000), g.uniform(-1, 1, 3000), g.uniform(-746, -708, 2000),
+                         g.normal(0, 1, 2000) * np.exp2(g.integers(-80, 0, 2000)),
+                         [0.0, -0.0, 709.782712893384, 709.7827128933841, -745.1332191019411,
+                          -745.1332191019412, -708.3964185322641, 1e-300, -1e-300, 2.0 ** -53, -(2.0 ** -54)]])
+    got = orc.fl_exp64(xs)
+    want = np.array([_decimal_exp(x) for x in xs])
+    assert np.array_equal(got, want)
+    assert not np.signbit(got).any()
+    sp = orc.fl_exp64(np.array([np.inf, -np.inf, np.nan, 800.0, -800.0]))
+    assert sp[0] == np.inf and sp[1] == 0.0 and np.isnan(sp[2]) and sp[3] == np.inf and sp[4] == 0.0
+
+
+def test_exp64_near_rounding_boundaries(orc):
+    """Arguments whose e^x lies within 2^-72 of a rounding boundary (the fixture written
+    by tests/golden/make_exp64_near_midpoints.py) are rounded as decimal arithmetic
+    rounds them."""
+    path = os.path.join(os.path.dirname(__file__), "golden", "exp64_near_midpoints.txt")
+    xs = np.array([float.fromhex(l) for l in open(path) if l.strip() and not l.startswith("#")])
+    assert len(xs) > 200
+    assert np.array_equal(orc.fl_exp64(xs), np.array([_decimal_exp(x) for x in xs]))
+
+
+def test_exp_mcn_binary64(orc):
+    """Exp-MCN over binary64 components: nc = 1 is the correctly rounded exponential;
+    exp((x_0, 0, ...)) = (e^x_0, 0, ...); and the result equals the exact product of the
+    component exponentials up to the carry roundings of the ScalingN chain."""
+    g = np.random.default_rng(41)
+    n = 1500
+    x1 = g.uniform(-20, 20, (1, n))
+    assert np.array_equal(orc.exp(x1, nc=1)[0], orc.fl_exp64(x1[0]))
+    x = np.zeros((3, n))
+    x[0] = x1[0]
+    r = orc.exp(x, nc=3)
+    assert np.array_equal(r[0], orc.fl_exp64(x1[0])) and not r[1:].any()
+    for nc in (2, 3):
+        x = np.zeros((nc, n))
+        x[0] = g.uniform(-20, 20, n)
+        for c in range(1, nc):
+            x[c] = g.uniform(-1, 1, n) * np.exp2(-20 * c)
+        r = orc.exp(x, nc=nc)
+        E = orc.fl_exp64(x)
+        u = Fraction(2) ** -53
+        for i in range(n):
+            prod = Fraction(1)
+            for c in range(nc):
+                prod *= Fraction(float(E[c, i]))
+            got = sum(Fraction(float(r[c, i])) for c in range(nc))
+            assert abs(got - prod) <= 8 * u ** nc * prod, i
