@@ -585,8 +585,9 @@ def bench_scaled(torch, mcf, oracle, inputs, steps=5):
 
 
 def bench_f64(torch, mcf, oracle, inputs, steps=10):
-    """binary64 components (the paper's MC float64): 2^26-element Add-MCN, ScalingN and
-    Div-MCN at nc = 2 (HBM bandwidth; Div-MCN also against the binary64 VALU rate), and
+    """binary64 components (the paper's MC float64): 2^26-element Add-MCN, ScalingN,
+    Div-MCN and Exp-MCN at nc = 2 (HBM bandwidth; Div-MCN also against the binary64 VALU
+    rate), and
     the 1024^3 MC x MC product at nc = 2 (VALU: binary64 adds and FMAs issue at half the
     binary32 rate)."""
     g = np.random.default_rng(0)
@@ -598,7 +599,8 @@ def bench_f64(torch, mcf, oracle, inputs, steps=10):
     out = torch.empty((nc, n), dtype=torch.float64, device="cuda")
     ops = {"add_mcn": (lambda: mcf.mc_add(a, b, nc=nc, out=out), 48),
            "scaling_n": (lambda: mcf.mc_mul(a, v, nc=nc, y_mc=False, out=out), 40),
-           "div_mcn": (lambda: mcf.mc_div(a, d, nc=nc, out=out), 48)}
+           "div_mcn": (lambda: mcf.mc_div(a, d, nc=nc, out=out), 48),
+           "exp_mcn": (lambda: mcf.mc_exp(a, nc=nc, out=out), 32)}
     res = {}
     for name, (fn, bpe) in ops.items():
         for _ in range(2):

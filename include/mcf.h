@@ -22,9 +22,8 @@
  *   IEEE binary64 (the paper's MC float64).  Every step of every algorithm is one IEEE
  *   round-to-nearest-even operation in the component format with gradual underflow;
  *   FMA appears only where the algorithm names it (Two-Prod); component division is
- *   correctly rounded; the binary16 and binary32 component exponentials are correctly
- *   rounded.  mc_exp does not take MCF_F64 (MCF_E_DTYPE); mc_matmul_exact takes
- *   MCF_F16 only.
+ *   correctly rounded; the component exponentials are correctly rounded in every
+ *   format.  mc_matmul_exact takes MCF_F16 only.
  *   MCF_F16S = binary16 components with scaled low components (Section 2.4 names
  *   scaling the smaller components as the way past binary16's smallest subnormal):
  *   component c is stored as the binary16 number y_c and stands for 2^(-11 c) y_c.
@@ -128,10 +127,11 @@ int mc_square(int dtype, int nc, int64_t n, const void *x, void *out, void *stre
 
 /* Exponential, Exp-MCN (Appendix A.2.1): h = exp(x_0) (one component), then for
  * i = 1 .. nc-1, h = ScalingN(h, exp(x_i), expand) growing h by one component per
- * step.  The component exponential is correctly rounded in both formats (binary16
+ * step.  The component exponential is correctly rounded in every format (binary16
  * by table lookup; binary32 from a binary64 evaluation, with a double-double one
- * where that lies too close to a rounding boundary).  x, out: [nc][n]; out == x
- * allowed.  MCF_F64: MCF_E_DTYPE. */
+ * where that lies too close to a rounding boundary; binary64 by a double-double
+ * table-driven evaluation, with a 192-bit fixed-point one where that lies too close
+ * to a rounding boundary).  x, out: [nc][n]; out == x allowed. */
 int mc_exp(int dtype, int nc, int64_t n, const void *x, void *out, void *stream);
 
 /* Renormalization (Appendix A.2.1).

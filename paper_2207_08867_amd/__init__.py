@@ -224,7 +224,7 @@ def mc_square(x, *, nc: int, out=None):
 
 
 def mc_exp(x, *, nc: int, out=None):
-    """Exp-MCN (binary16 components)."""
+    """Exp-MCN (every component format; the component exponential is correctly rounded)."""
     torch = _torch()
     s = _logical_shape(x, nc, True, "x")
     n = x.numel() // nc

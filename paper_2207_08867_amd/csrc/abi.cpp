@@ -177,9 +177,9 @@ int mc_exp(int dtype, int nc, int64_t n, const void *x, void *out, void *stream)
   if (n == 0) return MCF_OK;
   if (!x || !out) return MCF_E_NULL;
   const int64_t b = nc * n * elem_size(dtype);
-  if (dtype == MCF_F64) return MCF_E_DTYPE;  // no correctly rounded binary64 component exponential
   if (bad_alias(out, b, x, b)) return MCF_E_ALIAS;
   if (dtype == MCF_F16) return hip_status(mcf::launch_exp_f16(nc, n, x, out, (hipStream_t)stream));
+  if (dtype == MCF_F64) return hip_status(mcf::launch_exp_f64(nc, n, x, out, (hipStream_t)stream));
   return hip_status(mcf::launch_exp_f32(nc, n, x, out, (hipStream_t)stream));
 }
 

@@ -24,6 +24,9 @@ hipError_t launch_exp_f16(int nc, int64_t n, const void *x, void *out, hipStream
 // Exp-MCN over binary32 components (correctly rounded component exponential).
 hipError_t launch_exp_f32(int nc, int64_t n, const void *x, void *out, hipStream_t stream);
 
+// Exp-MCN over binary64 components (correctly rounded component exponential, exp64.hip).
+hipError_t launch_exp_f64(int nc, int64_t n, const void *x, void *out, hipStream_t stream);
+
 // A product launch in full generality (validated by the ABI layer): batches
 // B1 x B2 with per-operand batch strides (0 broadcasts) and plane strides; C dense
 // [nc][B1][B2][M][N]; b_trans: B stored [planes][N][K]; epilogue mode 0 none, 1

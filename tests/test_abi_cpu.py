@@ -62,7 +62,7 @@ def test_validation_elementwise(L):
         # out overlapping a plain y that is shorter than out
         assert f(1, 3, 10, x, 1, P(0x30000), 0, o, None) == MCF_E_ALIAS
     assert L.mc_exp(4, 3, 10, x, o, None) == MCF_E_DTYPE
-    assert L.mc_exp(2, 3, 10, x, o, None) == MCF_E_DTYPE  # binary64: no component exponential
+    assert L.mc_exp(2, 3, 10, x, P(0x10008), None) == MCF_E_ALIAS
     assert L.mc_exp(1, 3, 10, x, P(0x10004), None) == MCF_E_ALIAS
     assert L.mc_exp(0, 3, 0, None, None, None) == MCF_OK
     assert L.mc_renorm(0, 3, 4, 10, x, o, 0, None) == MCF_E_NC

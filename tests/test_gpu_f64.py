@@ -1,7 +1,10 @@
 """GPU parity with binary64 components (the paper's MC float64), bitwise against the
 CPU oracle: every elementwise operation and kind, the products (MM-MCN, MC-Linear,
 K-split, batched, AddMM, pruned) and the linear-regression step, nc 1..4 (products
-1..3), ragged sizes; Exp-MCN rejects binary64."""
+1..3), ragged sizes; Exp-MCN with the correctly rounded binary64 component
+exponential."""
+import os
+
 import numpy as np
 import pytest
 
@@ -52,11 +55,45 @@ def test_elementwise_f64(mcf, orc, nc):
         assert_bits(to_host(got), want, f"{name} f64 nc={nc}")
 
 
-def test_exp_rejects_f64(mcf):
-    import torch
+def _near_midpoints():
+    path = os.path.join(os.path.dirname(__file__), "golden", "exp64_near_midpoints.txt")
+    return np.array([float.fromhex(l) for l in open(path) if l.strip() and not l.startswith("#")])
 
-    with pytest.raises(ValueError):
-        mcf.mc_exp(torch.zeros((2, 8), dtype=torch.float64, device="cuda"), nc=2)
+
+def test_exp64_component_exponential(mcf, orc):
+    """nc = 1 Exp-MCN is the correctly rounded binary64 e^x: 2^24 random arguments over
+    the whole range (about 2^-15 of them take the 192-bit fixed-point stage), the range
+    of subnormal results, tiny arguments, boundaries, special values, and the 255
+    arguments whose e^x lies within 2^-72 of a rounding boundary (every one takes the
+    fixed-point stage)."""
+    g = np.random.default_rng(4100)
+    xs = np.concatenate([g.uniform(-745.2, 709.8, 1 << 24), g.uniform(-746, -708, 1 << 16),
+                         g.normal(0, 1, 1 << 14) * np.exp2(g.integers(-80, 0, 1 << 14)),
+                         [0.0, -0.0, 709.782712893384, 709.7827128933841, -745.1332191019411,
+                          -745.1332191019412, -708.3964185322641, 2.0 ** -53, -(2.0 ** -54), np.inf, -np.inf,
+                          np.nan, 800.0, -800.0, 1e-300, -1e-300],
+                         _near_midpoints()])
+    got = to_host(mcf.mc_exp(to_dev(xs[None]), nc=1))[0]
+    assert_bits(got, orc.fl_exp64(xs), "binary64 e^x")
+
+
+@pytest.mark.parametrize("nc", [2, 3, 4])
+def test_exp_mcn_f64(mcf, orc, nc):
+    """Exp-MCN over binary64 expansions (components from a draw of e^x-sized
+    arguments), with the near-boundary arguments as leading and as lower components."""
+    n = 20011
+    g = np.random.default_rng(4200 + nc)
+    x = np.zeros((nc, n))
+    x[0] = g.uniform(-30, 30, n)
+    for c in range(1, nc):
+        x[c] = g.uniform(-1, 1, n) * np.exp2(-18 * c)
+    nm = _near_midpoints()
+    x[0, : nm.size] = nm
+    x[1, nm.size: 2 * nm.size] = nm / 1024
+    tx = to_dev(x)
+    assert_bits(to_host(mcf.mc_exp(tx, nc=nc)), orc.exp(x, nc=nc), f"Exp-MCN f64 nc={nc}")
+    mcf.mc_exp(tx, nc=nc, out=tx)  # in place
+    assert_bits(to_host(tx), orc.exp(x, nc=nc), f"Exp-MCN f64 nc={nc} in place")
 
 
 @pytest.mark.parametrize("nc", [1, 2, 3])
