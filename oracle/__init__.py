@@ -478,6 +478,27 @@ def linear(X, W, bias=None, *, nc, rows=None, cols=None):
     return out.reshape(nc, T, O) if rows is None else out
 
 
+def linear_bwd(x, W, dY, *, nc, dy_mc=True):
+    """MC-Linear backward from the output gradient dY, as the oracle's MM-MCN products:
+    dX = dY W; dW = dY^T x and db = dY^T 1 with dY^T carried in nc components (+0 low
+    components when dY is plain).  x: (T, I) plain; W: (nc, O, I); dY: (nc, T, O) or
+    plain (T, O).  Returns (dX (nc, T, I), dW (nc, O, I), db (nc, O))."""
+    dtype = np.dtype(W.dtype)
+    x = _planar(x, dtype)
+    W = _planar(W, dtype)
+    Y = _planar(dY, dtype)
+    if not dy_mc:
+        Y = Y.reshape((1,) + Y.shape[-2:])
+    T, I = x.shape
+    O = W.shape[1]
+    dX = matmul(Y, W, nc=nc, a_mc=dy_mc, b_mc=True)
+    Yt = np.zeros((nc, O, T), dtype=dtype)
+    Yt[: Y.shape[0]] = np.transpose(Y, (0, 2, 1))
+    dW = matmul(Yt, x[None], nc=nc, a_mc=True, b_mc=False)
+    db = matmul(Yt, np.ones((1, T, 1), dtype=dtype), nc=nc, a_mc=True, b_mc=False)[:, :, 0]
+    return dX, dW, np.ascontiguousarray(db)
+
+
 def linreg_gd_step(X, y_neg, W, lr, *, slices_g, slices_l):
     """One gradient-descent step of MC-Linear regression with the mean-squared error
     (the precision experiment of Section 2.4), written as the composition of this
