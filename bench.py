@@ -460,7 +460,20 @@ def bench_linear(torch, mcf, oracle, inputs, layers=100):
         mcf.mc_linear_fwd(tx, Ws[l], bs[l], out=y)
         errors[f"layer_{l}"] = exact_error(oracle, x[None], Wt, y.cpu().numpy(), nc, I, np.float16, count=2048,
                                            seed=11 + l, bias=b)
+    # the backward of one layer (dX = dY W, dW = dY^T x, db), dY a plain gradient and an MC one
+    bwd = {}
+    g = np.random.default_rng(12)
+    dYmc = torch.from_numpy(inputs.split(g.normal(0.0, 1 / 32, (T, O)), nc, np.float16)).cuda()
+    ws = torch.empty(mcf.mc_linear_bwd_workspace(0, nc, T, I, O), dtype=torch.uint8, device="cuda")
+    for kind, dY, mc in (("plain_dY", dYmc[0].contiguous(), False), ("mc_dY", dYmc, True)):
+        run = lambda: mcf.mc_linear_bwd(tx, Ws[0], dY, dy_mc=mc, workspace=ws)
+        run()
+        tb = Timer(torch)
+        for _ in range(3):
+            tb.run(run)
+        bwd[kind] = {"ms": round(float(np.median(tb.ms())), 3)}
     return {"workload": f"MC-Linear {T}x{I}x{O} binary16 nc=3, {layers} layers", "ms_per_layer": round(kms, 3),
+            "backward_one_layer": bwd,
             "MC-GFLOP/s": round(2 * macs * layers / wall / 1e9, 1),
             "valu_frac_printed_ops": round(algo_ops_per_mac(nc, False) * macs / (kms * 1e-3) / VALU_PEAK, 3),
             **issue_fields("linear_4096x1024x1024_f16_nc3", kms * 1e-3, macs), "error": errors}

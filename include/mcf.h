@@ -311,6 +311,34 @@ int64_t mc_matmul_exact_workspace(int dtype, int nc, int64_t M, int64_t N, int64
 int mc_linear_fwd(int dtype, int nc, int64_t batch, int64_t in, int64_t out, const void *x, const void *W,
                   const void *b, void *y, void *stream);
 
+/* MC-Linear backward (the layer of Section 2.3, y = x W^T + b): given the gradient dY
+ * of the loss with respect to y, computes
+ *   dX = dY W          [batch][in]  (MM-MCN; dY MC: by linearity over W's components)
+ *   dW = dY^T x        [out][in]    (MM-MCN over the batch index, in batch order)
+ *   db = sum_t dY[t]   [out]        (Add-MCN of the rows of dY in batch order: MM-MCN
+ *                                    against a column of ones, ScalingN by 1 being exact)
+ * The paper keeps the gradient of an MC value as a plain tensor -- the gradient of
+ * its leading component (Section 2.1) -- and takes it from automatic differentiation;
+ * here the gradients are MC values whose leading components are those plain
+ * gradients, accumulated with MM-MCN's error propagation.  A plain dY (dy_mc = 0)
+ * enters dW and db as an MC value with +0 low components.
+ * x: [batch][in] plain; W: [nc][out][in]; dY: [nc or 1][batch][out] (dy_mc 1 or 0);
+ * dX: [nc][batch][in], dW: [nc][out][in], db: [nc][out] -- each may be NULL (not
+ * computed); outputs must not overlap the inputs, each other or the workspace.
+ * workspace: device memory of at least mc_linear_bwd_workspace(...) bytes when dW or
+ *   db is requested (dY^T staged in nc planes and a column of ones), owned by the
+ *   caller, not overlapping the inputs; contents on entry do not matter; calls sharing
+ *   it must not overlap in time.  Too small: MCF_E_ARG; NULL when needed: MCF_E_NULL.
+ * dtype: MCF_F16, MCF_F32, MCF_F64.  Sizes: batch, out <= 2^20, in <= 2^30 (and the
+ * product limits of mc_matmul). */
+int mc_linear_bwd(int dtype, int nc, int64_t batch, int64_t in, int64_t out, const void *x, const void *W,
+                  const void *dY, int dy_mc, void *dX, void *dW, void *db, void *workspace, int64_t workspace_bytes,
+                  void *stream);
+
+/* Workspace bytes mc_linear_bwd needs when dW or db is requested, or a negative
+ * mcf_status for sizes it would reject. */
+int64_t mc_linear_bwd_workspace(int dtype, int nc, int64_t batch, int64_t in, int64_t out);
+
 /* One gradient-descent step of the paper's linear-regression precision experiment
  * (Section 2.4): an MC-Linear layer without bias, W (out = 1 row of d weights), fitted
  * to targets y with the mean-squared error L(W) = (1/n) sum_i (x_i . W - y_i)^2.

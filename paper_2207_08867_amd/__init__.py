@@ -22,7 +22,7 @@ __all__ = [
     "mc_matmul_splitk_slices", "mc_matmul_splitk_workspace", "mc_matmul_splitk_noalloc", "mc_linear_fwd", "mc_status_str",
     "mc_matmul_batched", "mc_bmm", "mc_addmm", "matmul_mcn", "mc_mul_slow", "mc_square", "mc_matmul_pruned",
     "mc_matmul_exact", "mc_matmul_exact_workspace", "mc_linreg_workspace", "mc_linreg_gd_step",
-    "mc_linear_fwd_exact", "lib", "LIB_PATH", "MCFError",
+    "mc_linear_fwd_exact", "mc_linear_bwd", "mc_linear_bwd_workspace", "lib", "LIB_PATH", "MCFError",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmcf.so")
@@ -84,6 +84,10 @@ def lib() -> ctypes.CDLL:
         L.mc_linreg_workspace.argtypes = [ci, ci, i64, i64]
         L.mc_linreg_gd_step.restype = ci
         L.mc_linreg_gd_step.argtypes = [ci, ci, i64, i64, vp, vp, vp, ctypes.c_double, vp, i64, vp, vp]
+        L.mc_linear_bwd.restype = ci
+        L.mc_linear_bwd.argtypes = [ci, ci, i64, i64, i64, vp, vp, vp, ci, vp, vp, vp, vp, i64, vp]
+        L.mc_linear_bwd_workspace.restype = i64
+        L.mc_linear_bwd_workspace.argtypes = [ci, ci, i64, i64, i64]
         L.mc_linear_fwd.restype = ci
         L.mc_linear_fwd.argtypes = [ci, ci, i64, i64, i64, vp, vp, vp, vp, vp]
         L.mc_status_str.restype = ctypes.c_char_p
@@ -446,6 +450,43 @@ def mc_linear_fwd(x, W, b=None, *, out=None, scaled: bool = False):
                              _stream(W))
     _check(st, "mc_linear_fwd")
     return out
+
+
+def mc_linear_bwd_workspace(dtype_code: int, nc: int, batch: int, in_: int, out: int) -> int:
+    w = lib().mc_linear_bwd_workspace(dtype_code, nc, batch, in_, out)
+    _check(int(w) if w < 0 else 0, "mc_linear_bwd_workspace")
+    return int(w)
+
+
+def mc_linear_bwd(x, W, dY, *, dy_mc: bool = True, dx: bool = True, dw: bool = True, db: bool = True,
+                  workspace=None):
+    """MC-Linear backward: dX = dY W, dW = dY^T x, db = column sums of dY (MM-MCN order).
+    x: (batch, in) plain, W: (nc, out, in), dY: (nc, batch, out) or plain (batch, out).
+    Returns (dX (nc, batch, in), dW (nc, out, in), db (nc, out)), None for the outputs
+    not requested.  `workspace`: optional device byte tensor (allocated here if needed)."""
+    torch = _torch()
+    nc, O, I = W.shape
+    if x.dim() != 2 or x.shape[1] != I:
+        raise ValueError("x must be (batch, in)")
+    T = x.shape[0]
+    if tuple(dY.shape) != ((nc, T, O) if dy_mc else (T, O)):
+        raise ValueError(f"dY must be {(nc, T, O) if dy_mc else (T, O)}, got {tuple(dY.shape)}")
+    if x.dtype != W.dtype or dY.dtype != W.dtype:
+        raise ValueError("dtype mismatch")
+    code = _dtype_code(W)
+    outs = [torch.empty((nc, T, I), dtype=W.dtype, device=W.device) if dx else None,
+            torch.empty((nc, O, I), dtype=W.dtype, device=W.device) if dw else None,
+            torch.empty((nc, O), dtype=W.dtype, device=W.device) if db else None]
+    if (dw or db) and workspace is None:
+        workspace = torch.empty(max(mc_linear_bwd_workspace(code, nc, T, I, O), 1), dtype=torch.uint8,
+                                device=W.device)
+    wp = _dev(workspace, "workspace") if workspace is not None else None
+    wn = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    ptr = [(_dev(o, "out") if o is not None else None) for o in outs]
+    st = lib().mc_linear_bwd(code, nc, T, I, O, _dev(x, "x"), _dev(W, "W"), _dev(dY, "dY"), int(bool(dy_mc)),
+                             ptr[0], ptr[1], ptr[2], wp, wn, _stream(W))
+    _check(st, "mc_linear_bwd")
+    return tuple(outs)
 
 
 def _batch_strides(t, name, batch, rows, cols):

@@ -19,7 +19,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libmcf.so")
 SOURCES = ["abi.cpp", "elementwise.hip", "matmul.hip", "splitk.hip", "exact.hip", "linreg.hip", "scaled.hip",
-           "exp64.hip"]
+           "exp64.hip", "linear_bwd.hip"]
 # the VALU issue-rate probe behind the roofline figures (bench.py --issue-probe): a
 # library of its own, not part of libmcf.so
 PROBE_LIB = os.path.join(HERE, "libmcf_probe.so")

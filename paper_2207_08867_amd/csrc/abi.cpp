@@ -128,6 +128,18 @@ int linreg_check(int dtype, int nc, int64_t n, int64_t d) {
   return MCF_OK;
 }
 
+int linear_bwd_check(int dtype, int nc, int64_t batch, int64_t in, int64_t out) {
+  if (dtype != MCF_F16 && dtype != MCF_F32 && dtype != MCF_F64) return MCF_E_DTYPE;
+  if (nc < 1 || nc > MAX_NC) return MCF_E_NC;
+  if (batch < 0 || in < 0 || out < 0) return MCF_E_SHAPE;
+  // the products dX (batch x in, reduction out), dW (out x in, reduction batch) and db
+  // (out x 1, reduction batch) and the staging grid (batch / 32 tiles in a y dimension)
+  if (batch > ((int64_t)1 << 20) || out > ((int64_t)1 << 20) || in > ((int64_t)1 << 30)) return MCF_E_SHAPE;
+  if (!grid_fits(batch, in) || !grid_fits(out, in) || !product_fits(batch, in, out) || !product_fits(out, in, batch))
+    return MCF_E_SHAPE;
+  return MCF_OK;
+}
+
 // The component-format rounding of a binary64 value.
 double round_to_format(int dtype, double v) {
   if (dtype == MCF_F16) return (double)(_Float16)v;
@@ -430,6 +442,49 @@ int mc_linear_fwd_exact(int dtype, int nc, int64_t batch, int64_t in, int64_t ou
     return MCF_E_ALIAS;
   return hip_status(
       mcf::launch_matmul_exact(nc, batch, out, in, x, 0, W, 1, 1, b, workspace, y, (hipStream_t)stream));
+}
+
+int64_t mc_linear_bwd_workspace(int dtype, int nc, int64_t batch, int64_t in, int64_t out) {
+  const int st = linear_bwd_check(dtype, nc, batch, in, out);
+  if (st != MCF_OK) return st;
+  return mcf::linear_bwd_workspace_bytes(dtype, nc, batch, out);
+}
+
+int mc_linear_bwd(int dtype, int nc, int64_t batch, int64_t in, int64_t out, const void *x, const void *W,
+                  const void *dY, int dy_mc, void *dX, void *dW, void *db, void *workspace, int64_t workspace_bytes,
+                  void *stream) {
+  const int st = linear_bwd_check(dtype, nc, batch, in, out);
+  if (st != MCF_OK) return st;
+  if (dy_mc != 0 && dy_mc != 1) return MCF_E_ARG;
+  const int64_t es = elem_size(dtype);
+  // outputs with no elements are not computed
+  const int64_t dxb = nc * batch * in * es, dwb = nc * out * in * es, dbb = nc * out * es;
+  if (dxb == 0) dX = nullptr;
+  if (dwb == 0) dW = nullptr;
+  if (dbb == 0) db = nullptr;
+  if (!dX && !dW && !db) return MCF_OK;
+  const int64_t xb = batch * in * es, Wb = nc * out * in * es, yb = (dy_mc ? nc : 1) * batch * out * es;
+  if ((dX || dW) && in > 0 && batch > 0 && (!x || !W)) return MCF_E_NULL;
+  if (batch > 0 && out > 0 && !dY) return MCF_E_NULL;
+  const bool staged = dW || db;
+  const int64_t wb = staged ? mcf::linear_bwd_workspace_bytes(dtype, nc, batch, out) : 0;
+  if (staged) {
+    if (!workspace) return MCF_E_NULL;
+    if (workspace_bytes < wb) return MCF_E_ARG;
+  }
+  const void *ins[3] = {x, W, dY};
+  const int64_t inb[3] = {xb, Wb, yb};
+  void *outs[4] = {dX, dW, db, staged ? workspace : nullptr};
+  const int64_t outb[4] = {dxb, dwb, dbb, wb};
+  for (int o = 0; o < 4; ++o) {
+    if (!outs[o]) continue;
+    for (int i = 0; i < 3; ++i)
+      if (ins[i] && overlap(outs[o], outb[o], ins[i], inb[i])) return MCF_E_ALIAS;
+    for (int p = o + 1; p < 4; ++p)
+      if (outs[p] && overlap(outs[o], outb[o], outs[p], outb[p])) return MCF_E_ALIAS;
+  }
+  return hip_status(mcf::launch_linear_bwd(dtype, nc, batch, in, out, x, W, dY, dy_mc, dX, dW, db, workspace,
+                                           (hipStream_t)stream));
 }
 
 int64_t mc_linreg_workspace(int dtype, int nc, int64_t n, int64_t d) {

@@ -87,6 +87,13 @@ hipError_t launch_scaled_elementwise(int op, int nc, int64_t n, const void *x, c
 hipError_t launch_scaled_matmul(int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc, const void *B,
                                 int b_mc, int b_trans, const void *bias, void *C, hipStream_t stream);
 
+// MC-Linear backward (linear_bwd.hip): dX = dY W, dW = dY^T x, db = column sums of dY
+// (each output optional); dY is [nc or 1][batch][out] (dy_mc).  ws holds
+// linear_bwd_workspace_bytes(...) bytes (dY^T promoted to nc planes, a column of ones).
+int64_t linear_bwd_workspace_bytes(int dtype, int nc, int64_t batch, int64_t out);
+hipError_t launch_linear_bwd(int dtype, int nc, int64_t batch, int64_t in, int64_t out, const void *x, const void *W,
+                             const void *dY, int dy_mc, void *dX, void *dW, void *db, void *ws, hipStream_t stream);
+
 // One gradient-descent step of MC-Linear regression (linreg.hip).  s2n, s1n and neg_lr
 // are fl(2/n), fl(1/n) and fl(-lr), already values of the component format.  ws holds
 // linreg_workspace_bytes(...) bytes.
