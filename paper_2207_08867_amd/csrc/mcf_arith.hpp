@@ -137,16 +137,18 @@ __device__ __forceinline__ void grow_expn(const T (&x)[N], T v, T (&out)[N]) {
 }
 
 // ScalingN: an M-component value times a plain value v; R = M (expand off) or M+1.
-// The first Two-Sum adds the initial carry +0: Two-Sum(hp, +0) = (hp + 0, +0) for any
-// finite hp, so h_0 = hp and the carry is e1, up to the sign of a zero -- and
-// Simple-Renorm drops every zero term and pads with +0, so the result is the same.
-// (With an infinite or NaN term the elided steps could only turn an infinity into a
-// NaN; results are then non-finite either way.)
+// The first Two-Sum adds the initial carry +0: Two-Sum(hp, +0) = (hp + 0, e2) with
+// e2 = +0 for finite hp and NaN for infinite or NaN hp (its hp - hp step), so h_0 = hp
+// up to the sign of a zero (Simple-Renorm drops zeros) and the carry e1 + e2 is
+// e1 + (hp - hp): two operations in place of the Two-Sum, the same value in every
+// case -- a product that overflows although both factors are finite leaves a NaN
+// carry, not the infinite Two-Prod error.
 template <typename T, int M, int R>
 __device__ __forceinline__ void scaling_n(const T (&x)[M], T v, T (&out)[R]) {
   T h[M + 1];
   T e;
   two_prod(x[0], v, h[0], e);
+  e = e + (h[0] - h[0]);
 #pragma unroll
   for (int i = 1; i < M; ++i) {
     T hp, e1, e2;
@@ -158,8 +160,9 @@ __device__ __forceinline__ void scaling_n(const T (&x)[M], T v, T (&out)[R]) {
   simple_renorm<T, M + 1, R>(h, out);
 }
 
-// Add-MCN: sum of two N-component values (first Two-Sum with the +0 carry elided as
-// in scaling_n).
+// Add-MCN: sum of two N-component values.  The first Two-Sum with the +0 carry is
+// elided: its error would be NaN only for infinite or NaN hp, and then the Two-Sum
+// error e1 that forms hp is NaN already.
 template <typename T, int N>
 __device__ __forceinline__ void add_mcn(const T (&x)[N], const T (&y)[N], T (&out)[N]) {
   T h[N + 1];

@@ -93,8 +93,9 @@ __device__ __forceinline__ void sc_scaling_general(const h16 (&x)[M], h16 v, h16
 }
 
 // ScalingN, kept terms only; false when a kept term is zero (the caller then runs the
-// complete algorithm).  The Two-Sum of the first product with the zero carry only
-// changes the sign of a zero, and so does the carry fl(e1 + 0).
+// complete algorithm).  The Two-Sum of the first product p with the zero carry only
+// changes the sign of a zero for finite p, and its error is NaN for infinite or NaN p:
+// the carry is e1 + (p - p) in every case.
 template <int M>
 __device__ __forceinline__ bool sc_scaling_fast(const h16 (&x)[M], h16 v, h16 (&h)[M]) {
   h16 e;
@@ -102,7 +103,7 @@ __device__ __forceinline__ bool sc_scaling_fast(const h16 (&x)[M], h16 v, h16 (&
     h16 p, e1;
     sc_two_prod(x[0], v, p, e1);
     h[0] = p;
-    e = e1;
+    e = e1 + (p - p);
   }
 #pragma unroll
   for (int i = 1; i < M - 1; ++i) {

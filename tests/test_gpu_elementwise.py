@@ -126,6 +126,15 @@ def test_exp_component_exhaustive(mcf, orc):
     x = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16).view(np.float16)[None].copy()
     got = to_host(mcf.mc_exp(to_dev(x), nc=1))
     assert_bits(got, orc.exp(x, nc=1), "exp16 exhaustive")
+    # every encoding as the second and as the third component (the lower components'
+    # exponentials: arithmetic for |x| <= 2^-9, the table otherwise)
+    for nc in (2, 3):
+        y = np.zeros((nc, 1 << 16), dtype=np.float16)
+        y[0] = np.float16(0.75)
+        y[nc - 1] = x[0]
+        if nc == 3:
+            y[1] = np.float16(-2.0 ** -10)
+        assert_bits(to_host(mcf.mc_exp(to_dev(y), nc=nc)), orc.exp(y, nc=nc), f"exp16 exhaustive, component {nc - 1}")
 
 
 def test_div_f16_component_strided_exhaustive(mcf, orc):
@@ -151,6 +160,36 @@ def test_special_values(mcf, orc):
             assert_bits(to_host(fn(to_dev(x), to_dev(y), nc=3, y_mc=True)), ofn(x, y, nc=3), "special")
             assert_bits(to_host(fn(to_dev(x), to_dev(y[:1]), nc=3, y_mc=False)), ofn(x, y[:1], nc=3, y_mc=False),
                         "special")
+
+
+@pytest.mark.parametrize("dt", DTS)
+def test_overflow_from_finite_operands(mcf, orc, dt):
+    """Leading sums and products that overflow although every operand is finite
+    (|x| in [0.3, 1] of the format's largest value, plain factors in [1, 4]):
+    ScalingN, Add-MCN and Grow-ExpN agree with the algorithm bit for bit -- the
+    infinite leading component and the NaN carries the Two-Sums leave behind it."""
+    g = np.random.default_rng(15)
+    n = 4099
+    big = float(np.finfo(dt).max)
+
+    def sign():
+        return g.choice([-1.0, 1.0], n)
+
+    x = inputs.split(sign() * g.uniform(0.3, 1.0, n) * big, 3, dt)
+    y = inputs.split(sign() * g.uniform(0.3, 1.0, n) * big, 3, dt)
+    v = (sign() * g.uniform(1.0, 4.0, n)).astype(dt)[None]
+    w = (sign() * g.uniform(0.3, 1.0, n) * big).astype(dt)[None]
+    tx, ty, tv, tw = to_dev(x), to_dev(y), to_dev(v), to_dev(w)
+    cases = (
+        ("ScalingN (MC,T)", mcf.mc_mul(tx, tv, nc=3, y_mc=False), orc.mul(x, v, nc=3, y_mc=False)),
+        ("ScalingN (T,MC)", mcf.mc_mul(tv, tx, nc=3, x_mc=False), orc.mul(v, x, nc=3, x_mc=False)),
+        ("Add-MCN", mcf.mc_add(tx, ty, nc=3), orc.add(x, y, nc=3)),
+        ("Grow-ExpN", mcf.mc_add(tx, tw, nc=3, y_mc=False), orc.add(x, w, nc=3, y_mc=False)),
+    )
+    for what, got, want in cases:
+        lead = want[0].astype(np.float64)
+        assert np.isinf(lead).any() and np.isfinite(lead).any(), what  # both kinds occur
+        assert_bits(to_host(got), want, f"{what} overflow")
 
 
 def test_literal_mult_inputs_overflow_class(mcf, orc):

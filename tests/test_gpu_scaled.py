@@ -60,6 +60,22 @@ def test_elementwise_parity(mcf, orc, nc, n):
     assert_bits(to_host(t2), orc.scaled_add(x, y, nc=nc), f"add in place nc={nc}")
 
 
+@pytest.mark.parametrize("nc", [2, 3])
+def test_scaling_overflow(mcf, orc, nc):
+    """ScalingN whose leading product overflows although both factors are finite:
+    bitwise against the algorithm (the NaN carry behind the infinite product)."""
+    g = np.random.default_rng(120 + nc)
+    n = 4099
+    x = inputs.split_scaled(g.choice([-1.0, 1.0], n) * g.uniform(0.3, 1.0, n) * 65504.0, nc)
+    v = (g.choice([-1.0, 1.0], n) * g.uniform(1.0, 4.0, n)).astype(np.float16)
+    want = orc.scaled_mul(x, v[None], nc=nc)
+    lead = want[0].astype(np.float64)
+    assert np.isinf(lead).any() and np.isfinite(lead).any()
+    tx, tv = to_dev(x), to_dev(v)
+    assert_bits(to_host(mcf.mc_mul(tx, tv, nc=nc, y_mc=False, scaled=True)), want, f"scaled overflow nc={nc}")
+    assert_bits(to_host(mcf.mc_mul(tv, tx, nc=nc, x_mc=False, scaled=True)), want, f"scaled overflow T,MC nc={nc}")
+
+
 def test_elementwise_kinds_not_provided(mcf):
     import torch
 

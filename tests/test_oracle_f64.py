@@ -9,7 +9,10 @@ hyperbolic models), against references that share none of its code:
     the numpy tree; MC x MC within 4 K u^nc of the exact product, checked both by the
     oracle's exact checker (its binary64 path splits each product with fma) and by
     fractions on a small case;
-  * Exp-MCN rejects binary64.
+  * the binary64 component exponential against decimal arithmetic (the whole range,
+    subnormal results, boundaries, arguments within 2^-72 of a rounding boundary), and
+    Exp-MCN over it (nc = 1, zero tails, the exact product of the component
+    exponentials within 8 u^nc).
 """
 from fractions import Fraction
 
