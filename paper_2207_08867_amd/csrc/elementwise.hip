@@ -4,7 +4,8 @@
 //
 // Data are component-major planes; each thread moves 16 bytes per plane per step
 // (8 binary16 or 4 binary32 elements) with dwordx4 loads and stores, so one wave
-// reads 1 KiB contiguous per plane: fully coalesced HBM streams.  The arithmetic of
+// reads 1 KiB contiguous per plane: fully coalesced HBM streams (the few longest
+// per-element algorithms take one element per lane: see ew_one_per_lane).  The arithmetic of
 // each element is the per-element algorithm of mcf_arith.hpp (Div-MCN and Mult-MCN
 // through div_steps.hpp, which returns the same bits with fewer operations).
 #include <hip/hip_runtime.h>
@@ -191,15 +192,28 @@ static int ew_blocks(int64_t work) {
   return (int)b;
 }
 
+// Instantiations whose per-element body is so long that the compiler does not unroll
+// the loop over a 16-byte chunk's elements: their operand and result packs, indexed by
+// the loop counter, would live in scratch memory (binary16 Mult-MCN-Slow at nc = 3
+// moved 2.7 GB of it per 2^26 elements, mostly in cache: the steady-state time is 1%
+// lower without it).  They take one element per lane and plane instead.
+template <typename T, int NC, int OP, bool XMC, bool YMC>
+constexpr bool ew_one_per_lane() {
+  if constexpr (OP == EW_MUL_SLOW) return sizeof(T) == 2 ? NC >= 3 : (sizeof(T) == 4 && NC >= 4);
+  if constexpr (OP == EW_MUL && XMC && YMC) return sizeof(T) == 2 && NC >= 4;
+  return false;
+}
+
 template <typename T, int NC, int OP, bool XMC, bool YMC, int NCOUT>
 static hipError_t ew_launch(int64_t n, const void *x, const void *y, void *out, hipStream_t s) {
-  constexpr int W = 16 / sizeof(T);
+  constexpr int W = ew_one_per_lane<T, NC, OP, XMC, YMC>() ? 1 : 16 / sizeof(T);
+  constexpr int VB = W * (int)sizeof(T);
   const T *xp = (const T *)x;
   const T *yp = (const T *)y;
   T *op = (T *)out;
-  // 16-byte vector access needs every plane start aligned to 16 bytes.
-  bool vec = ((n * (int64_t)sizeof(T)) % 16 == 0) && ((uintptr_t)x % 16 == 0) &&
-             (y == nullptr || (uintptr_t)y % 16 == 0) && ((uintptr_t)out % 16 == 0);
+  // vector access of VB bytes needs every plane start aligned to VB bytes
+  bool vec = ((n * (int64_t)sizeof(T)) % VB == 0) && ((uintptr_t)x % VB == 0) &&
+             (y == nullptr || (uintptr_t)y % VB == 0) && ((uintptr_t)out % VB == 0);
   if (vec) {
     hipLaunchKernelGGL((ew_kernel<T, NC, OP, XMC, YMC, NCOUT, W>), dim3(ew_blocks(n / W)), dim3(EW_THREADS), 0, s,
                        xp, yp, op, n);
