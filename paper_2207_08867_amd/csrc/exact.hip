@@ -510,10 +510,10 @@ __device__ __forceinline__ void xm_epilogue(const XmArgs &g, const XLevels &lv, 
 // straight from the digit planes; the fragments of the next k block are loaded while
 // the current one is multiplied.
 //
-// KS = 2: two wavefronts share each tile, one per half of the k blocks (khalf); the
-// second adds its accumulators into the first's through LDS (red: 16 KiB, exact integer
-// sums) and leaves, and the first runs the epilogue.  Every lane of the workgroup must
-// call it then (it holds barriers).
+// KS = 2: two wavefronts share each tile, one per half of the k blocks (khalf); they
+// exchange accumulators through LDS (red: 16 KiB, exact integer sums) so that each
+// holds the complete sums of one tile row, and each rounds its row.  Every lane of the
+// workgroup must call it then (it holds barriers).
 template <int DM, int WTR, int WTC, int KS = 1>
 __device__ __forceinline__ void xm_tile(const XmArgs &g, const XLevels &lv, int64_t row0, int64_t col0,
                                         int64_t chunk, int64_t kb0, int64_t kb1, int64_t S, uint16_t *st,
@@ -584,30 +584,31 @@ __device__ __forceinline__ void xm_tile(const XmArgs &g, const XLevels &lv, int6
     }
   }
   if constexpr (KS == 2) {
-    static_assert(WTR * WTC * 4 <= 16, "reduction buffer too small");
+    // The two wavefronts of a tile split its rows: the one with khalf = h completes tile
+    // row h (exact integer sums of both halves' accumulators, exchanged through LDS) and
+    // rounds it, so both run the epilogue on half the outputs.
+    static_assert(WTR == 2 && WTC * 4 <= 8, "reduction buffer layout");
     const int qw = (threadIdx.x / 64) % 4;
+    v4i mine[NCLS][1][WTC];
 #pragma unroll
     for (int q = 0; q < NCLS; ++q) {
-      if (khalf) {
+      // give away the other half's row, keep this half's row
 #pragma unroll
-        for (int r = 0; r < WTR; ++r)
+      for (int c = 0; c < WTC; ++c)
 #pragma unroll
-          for (int c = 0; c < WTC; ++c)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) red[(qw * 16 + (r * WTC + c) * 4 + i) * 64 + lane] = acc[q][r][c][i];
-      }
+        for (int i = 0; i < 4; ++i) {
+          red[((qw * 2 + khalf) * 8 + c * 4 + i) * 64 + lane] = khalf ? acc[q][0][c][i] : acc[q][1][c][i];
+          mine[q][0][c][i] = khalf ? acc[q][1][c][i] : acc[q][0][c][i];
+        }
       __syncthreads();
-      if (!khalf) {
 #pragma unroll
-        for (int r = 0; r < WTR; ++r)
+      for (int c = 0; c < WTC; ++c)
 #pragma unroll
-          for (int c = 0; c < WTC; ++c)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) acc[q][r][c][i] += red[(qw * 16 + (r * WTC + c) * 4 + i) * 64 + lane];
-      }
+        for (int i = 0; i < 4; ++i) mine[q][0][c][i] += red[((qw * 2 + (1 - khalf)) * 8 + c * 4 + i) * 64 + lane];
       __syncthreads();
     }
-    if (khalf) return;
+    xm_epilogue<DM, 1, WTC>(g, lv, mine, row0 + 16 * khalf, col0, chunk, S, st);
+    return;
   }
   xm_epilogue<DM, WTR, WTC>(g, lv, acc, row0, col0, chunk, S, st);
 }
@@ -623,9 +624,9 @@ __device__ __forceinline__ void xm_tile(const XmArgs &g, const XLevels &lv, int6
 template <int KS>
 __global__ __attribute__((amdgpu_flat_work_group_size(1, 256 * KS), amdgpu_waves_per_eu(2))) void xm_kernel(
     XmArgs g) {
-  // epilogue staging: 2560 bytes per wavefront of the first group; KS = 2 reduction:
-  // 16 KiB, used before the epilogue
-  __shared__ __attribute__((aligned(16))) int8_t smem[KS == 2 ? 16384 : 4 * 2560];
+  // epilogue staging: 2560 bytes per wavefront; KS = 2 exchange: 16 KiB of the same
+  // memory, used before the epilogue
+  __shared__ __attribute__((aligned(16))) int8_t smem[KS == 2 ? 8 * 2560 : 4 * 2560];
   const XLevels lv = x_levels(g.stats);
   const int wave = (threadIdx.x / 64) % 4;
   const int khalf = threadIdx.x / 256;
@@ -639,7 +640,7 @@ __global__ __attribute__((amdgpu_flat_work_group_size(1, 256 * KS), amdgpu_waves
   if (kb0 >= KB && KB > 0) return;  // the grid holds the chunks of the smallest chunk size
   const int64_t kb1 = min(KB, kb0 + CKB);
   const int64_t S = KB == 0 ? 1 : (KB + CKB - 1) / CKB;
-  uint16_t *st = (uint16_t *)(smem + wave * 2560);
+  uint16_t *st = (uint16_t *)(smem + (threadIdx.x / 64) * 2560);
   if (dm == 3) {
     xm_tile<3, 2, 2, KS>(g, lv, tm * 64 + (wave / 2) * 32, tn * 64 + (wave % 2) * 32, chunk, kb0, kb1, S, st, khalf,
                          (int *)smem);
