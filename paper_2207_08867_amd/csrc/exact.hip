@@ -370,6 +370,21 @@ __device__ __forceinline__ uint32_t take_f16_fast(int64_t &rem) {
   return ((uint32_t)sgn & 0x8000u) | (uint32_t)((qe - 24) * 1024 + (int)n);
 }
 
+// take_f16_fast for a remainder held as a binary64 value (d = rem 2^-48, exact: the
+// remainder is an integer below 2^53 in magnitude): d is rounded to binary32 toward
+// odd (round to nearest, then, if inexact, the neighbour with an odd last bit), which
+// keeps the information a second rounding to binary16 needs (24 >= 11 + 2 bits), and
+// then to binary16; d minus the binary16 value is exact in binary64.
+__device__ __forceinline__ uint32_t take_f16_binary64(double &d) {
+  const float f = (float)d;
+  const double fd = (double)f;
+  uint32_t fb = __builtin_bit_cast(uint32_t, f);
+  if (fd != d && (fb & 1u) == 0u) fb = __builtin_fabs(fd) < __builtin_fabs(d) ? fb + 1u : fb - 1u;
+  const _Float16 h = (_Float16)__builtin_bit_cast(float, fb);
+  d -= (double)(float)h;
+  return __builtin_bit_cast(uint16_t, h);
+}
+
 // Epilogue of one wavefront's WTR x WTC tiles of 16 x 16 outputs (accumulator element
 // i of lane l is row 4 (l / 16) + i, column l % 16 of its tile, one int32 accumulator
 // per tile and shift class).  stage: 16-byte aligned LDS of at least 2560 bytes owned by
@@ -435,17 +450,43 @@ __device__ __forceinline__ void xm_epilogue(const XmArgs &g, const XLevels &lv, 
           }
           v[r][c][i] = (int64_t)vu;
         }
+    // When every |V| of the wavefront is below 2^53 (the usual case: V is the output in
+    // units of 2^-48), V * 2^-48 is exact in binary64 and the components are taken in
+    // binary64 arithmetic, a third of the integer path's instructions.
+    bool below53 = true;
+    double dv[WTR][WTC][4];
+#pragma unroll
+    for (int r = 0; r < WTR; ++r)
+#pragma unroll
+      for (int c = 0; c < WTC; ++c)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int64_t x = v[r][c][i];
+          below53 = below53 && (uint64_t)(x + (1ll << 53)) < (1ull << 54);
+          dv[r][c][i] = __builtin_fma((double)(int32_t)(x >> 32), 0x1p32, (double)(uint32_t)x) * 0x1p-48;
+        }
+    const bool f64path = __all(below53);
     constexpr int TR = 16 * WTR, TC = 16 * WTC, LD = TC + 8;
     static_assert(TR * LD * 2 <= 2560, "stage tile too small");
     const bool vec = g.cvec && col0 + TC <= g.N;
     for (int k = 0; k < g.nc; ++k) {
+      if (f64path) {
 #pragma unroll
-      for (int r = 0; r < WTR; ++r)
+        for (int r = 0; r < WTR; ++r)
 #pragma unroll
-        for (int c = 0; c < WTC; ++c)
+          for (int c = 0; c < WTC; ++c)
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
-            st[(16 * r + 4 * (lane / 16) + i) * LD + 16 * c + lane % 16] = (uint16_t)take_f16_fast(v[r][c][i]);
+            for (int i = 0; i < 4; ++i)
+              st[(16 * r + 4 * (lane / 16) + i) * LD + 16 * c + lane % 16] = (uint16_t)take_f16_binary64(dv[r][c][i]);
+      } else {
+#pragma unroll
+        for (int r = 0; r < WTR; ++r)
+#pragma unroll
+          for (int c = 0; c < WTC; ++c)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              st[(16 * r + 4 * (lane / 16) + i) * LD + 16 * c + lane % 16] = (uint16_t)take_f16_fast(v[r][c][i]);
+      }
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
