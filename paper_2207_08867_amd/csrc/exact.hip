@@ -401,34 +401,41 @@ __device__ __forceinline__ void xm_epilogue(const XmArgs &g, const XLevels &lv, 
   // sum fits; otherwise in 128-bit integers.
   const int shift0 = 8 * (lv.loA + lv.loB);
   bool fits = true;
+  // The test, term by term: a non-zero term with bit length b at shift h needs
+  // b + h + 4 <= 62, i.e. its magnitude below 2^(58 - h).  lim(h) is the largest
+  // magnitude allowed (uniform across the wavefront).
+  auto lim = [&](int h) -> uint64_t {
+    const int e = 58 - h;
+    return e <= 0 ? 0ull : (e >= 64 ? ~0ull : (1ull << e) - 1);
+  };
   // each lane's columns: their bias (units of 2^-24, added 24 bits up) joins the sum
   int64_t bu[WTC];
-  int bhb[WTC];
 #pragma unroll
   for (int c = 0; c < WTC; ++c) {
     const int64_t col = col0 + 16 * c + lane % 16;
     bool bb = false;
     bu[c] = col < g.N ? bias_units(g, col, bb) : 0;
-    fits = fits && !bb;
     const uint64_t ab = (uint64_t)(bu[c] < 0 ? -bu[c] : bu[c]);
-    bhb[c] = ab ? 64 - __builtin_clzll(ab) + 24 : 0;
+    fits = fits && !bb && ab <= lim(24 + shift0);
+  }
+  uint32_t lq[NCLS];
+#pragma unroll
+  for (int q = 0; q < NCLS; ++q) {
+    const uint64_t l = lim(8 * q + shift0);
+    lq[q] = l > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)l;
   }
 #pragma unroll
   for (int r = 0; r < WTR; ++r)
 #pragma unroll
     for (int c = 0; c < WTC; ++c)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        int hb = bhb[c];
+      for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int q = 0; q < NCLS; ++q) {
           const int32_t x = acc[q][r][c][i];
-          const uint32_t ax = (uint32_t)(x < 0 ? -(int64_t)x : (int64_t)x);
-          const int bl = ax ? 32 - __builtin_clz(ax) : 0;
-          hb = max(hb, bl ? bl + 8 * q : 0);
+          const uint32_t ux = (uint32_t)x, ax = x < 0 ? 0u - ux : ux;  // |x|, also for -2^31
+          fits = fits && ax <= lq[q];
         }
-        fits = fits && (hb == 0 || hb + 4 + shift0 <= 62);
-      }
   const bool fast = __all(fits) && !lv.anybad && S == 1;  // uniform across the wavefront
   const int64_t MN = g.M * g.N;
   if (fast) {
