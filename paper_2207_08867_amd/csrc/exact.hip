@@ -574,6 +574,13 @@ __device__ __forceinline__ void xm_tile(const XmArgs &g, const XLevels &lv, int6
     if (khalf) kb0 = mid;
     else kb1 = mid;
   }
+  // the k range is uniform across the wavefront: keep the loop control scalar, so that
+  // the loop is not run under an execution mask and the waits for the prefetched
+  // fragments are counted
+  kb0 = ((int64_t)__builtin_amdgcn_readfirstlane((int)(kb0 >> 32)) << 32) |
+        (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)kb0);
+  kb1 = ((int64_t)__builtin_amdgcn_readfirstlane((int)(kb1 >> 32)) << 32) |
+        (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)kb1);
 
   v4i acc[NCLS][WTR][WTC];
 #pragma unroll
@@ -583,53 +590,55 @@ __device__ __forceinline__ void xm_tile(const XmArgs &g, const XLevels &lv, int6
 #pragma unroll
       for (int c = 0; c < WTC; ++c) acc[q][r][c] = v4i{0, 0, 0, 0};
 
-  // fragment (level s, k block kb, row block rb) at ((s KB + kb) RB + rb) KiB
+  // fragment (level s, k block kb, row block rb) at ((s KB + kb) RB + rb) KiB.  Every
+  // level slot up to DM is loaded (a slot beyond the levels in use reads an existing
+  // level and is never multiplied), so that the loads of a k block form one straight
+  // block of code whose completion the compiler can wait for by count.
   const int64_t RBa = g.Mp / 16, RBb = g.Np / 16;
-  const int8_t *pa = g.DA + (((int64_t)lv.loA * KB) * RBa + row0 / 16) * 1024 + lane * 16;
-  const int8_t *pb = g.DB + (((int64_t)lv.loB * KB) * RBb + col0 / 16) * 1024 + lane * 16;
+  const int nA = __builtin_amdgcn_readfirstlane(lv.nA), nB = __builtin_amdgcn_readfirstlane(lv.nB);
+  const int loA = __builtin_amdgcn_readfirstlane(lv.loA), loB = __builtin_amdgcn_readfirstlane(lv.loB);
+  const int8_t *pa = g.DA + (row0 / 16) * 1024 + lane * 16;
+  const int8_t *pb = g.DB + (col0 / 16) * 1024 + lane * 16;
   const int64_t la = KB * RBa * 1024, lb = KB * RBb * 1024;  // level strides
-  const int64_t ka = RBa * 1024, kbs = RBb * 1024;           // k-block strides
+  const int64_t ka = RBa * 1024, kbs = RBb * 1024;          // k-block strides
 
-  v4i fa[DM][WTR], fb[DM][WTC];
   auto load = [&](int64_t kb, v4i (&xa)[DM][WTR], v4i (&xb)[DM][WTC]) {
 #pragma unroll
     for (int s = 0; s < DM; ++s) {
-      if (s < lv.nA) {
+      const int64_t oa = min(loA + s, XD - 1) * la + kb * ka, ob = min(loB + s, XD - 1) * lb + kb * kbs;
 #pragma unroll
-        for (int r = 0; r < WTR; ++r) xa[s][r] = *(const v4i *)(pa + s * la + kb * ka + r * 1024);
-      }
-      if (s < lv.nB) {
+      for (int r = 0; r < WTR; ++r) xa[s][r] = *(const v4i *)(pa + oa + r * 1024);
 #pragma unroll
-        for (int c = 0; c < WTC; ++c) xb[s][c] = *(const v4i *)(pb + s * lb + kb * kbs + c * 1024);
-      }
+      for (int c = 0; c < WTC; ++c) xb[s][c] = *(const v4i *)(pb + ob + c * 1024);
     }
   };
-  if (kb0 < kb1) load(kb0, fa, fb);
-  for (int64_t kb = kb0; kb < kb1; ++kb) {
-    v4i na[DM][WTR], nb[DM][WTC];
-    if (kb + 1 < kb1) load(kb + 1, na, nb);
+  auto mfmas = [&](const v4i (&xa)[DM][WTR], const v4i (&xb)[DM][WTC]) {
 #pragma unroll
     for (int s = 0; s < DM; ++s) {
-      if (s < lv.nA) {
+      if (s < nA) {
 #pragma unroll
         for (int t = 0; t < DM; ++t) {
-          if (t < lv.nB) {
+          if (t < nB) {
 #pragma unroll
             for (int r = 0; r < WTR; ++r)
 #pragma unroll
               for (int c = 0; c < WTC; ++c)
-                acc[s + t][r][c] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[s][r], fb[t][c], acc[s + t][r][c], 0, 0, 0);
+                acc[s + t][r][c] = __builtin_amdgcn_mfma_i32_16x16x64_i8(xa[s][r], xb[t][c], acc[s + t][r][c], 0, 0, 0);
           }
         }
       }
     }
-#pragma unroll
-    for (int s = 0; s < DM; ++s) {
-#pragma unroll
-      for (int r = 0; r < WTR; ++r) fa[s][r] = na[s][r];
-#pragma unroll
-      for (int c = 0; c < WTC; ++c) fb[s][c] = nb[s][c];
-    }
+  };
+  // two register sets in alternation (no copies between them): the loads of the next
+  // k block are issued before the current block's matrix-core instructions
+  v4i fa[DM][WTR], fb[DM][WTC], na[DM][WTR], nb[DM][WTC];
+  if (kb0 < kb1) load(kb0, fa, fb);
+  for (int64_t kb = kb0; kb < kb1; kb += 2) {
+    if (kb + 1 < kb1) load(kb + 1, na, nb);
+    mfmas(fa, fb);
+    if (kb + 1 >= kb1) break;
+    if (kb + 2 < kb1) load(kb + 2, fa, fb);
+    mfmas(na, nb);
   }
   if constexpr (KS == 2) {
     // The two wavefronts of a tile split its rows: the one with khalf = h completes tile
