@@ -172,6 +172,7 @@ struct Lane {
               if (__builtin_expect(sr_try<T, NCP, SPOL>(h, t, v == T(0)), 0)) compact_nz<T, NCP + 1, NCP>(h, t);
             }
             if constexpr (FIRST) {
+              nonfinite_tail<T, NCP>(t);
 #pragma unroll
               for (int c = 0; c < NCP; ++c) ac[c] = t[c];
 #pragma unroll
@@ -192,6 +193,18 @@ struct Lane {
   // term k = 0 initialises the accumulators
   template <bool TPS>
   __device__ __forceinline__ void first(const Ops &o) {
+    first_terms<TPS>(o);
+    if constexpr (!PRUNE) {  // (the pruned parts are patched in prune_step)
+#pragma unroll
+      for (int p = 0; p < NP; ++p)
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j) nonfinite_tail<T, NC>(acc[p][i][j]);
+    }
+  }
+  template <bool TPS>
+  __device__ __forceinline__ void first_terms(const Ops &o) {
     if constexpr (PRUNE) {
       prune_step<0, (1 << NP) - 1, TPS, true>(o);
     } else if constexpr (SPOL == SR_SUFFIX) {

@@ -330,6 +330,26 @@ __device__ __forceinline__ void kept_add(T (&a)[N], const T (&t)[N]) {
   for (int c = 0; c < N; ++c) a[c] = s[c];
 }
 
+// The steps above elide the first Two-Sum of ScalingN with the +0 carry, which is
+// exact for finite terms.  When a term is infinite or NaN that Two-Sum (and every one
+// after it) leaves a NaN carry, so every later component of the algorithm's result is
+// NaN; an Add-MCN that follows restores this by itself (its Two-Sums with a non-finite
+// term have NaN errors), but a ScalingN result that is stored as it is -- the product
+// of a single reduction step -- is patched here.
+__device__ __forceinline__ bool finite_(float x) { return __builtin_isfinite(x); }
+__device__ __forceinline__ bool finite_(double x) { return __builtin_isfinite(x); }
+__device__ __forceinline__ bool finite_(_Float16 x) { return __builtin_isfinite((float)x); }
+
+template <typename T, int N>
+__device__ __forceinline__ void nonfinite_tail(T (&t)[N]) {
+  bool nf = false;
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    if (i > 0) t[i] = nf ? T(__builtin_nanf("")) : t[i];
+    nf = nf | !finite_(t[i]);
+  }
+}
+
 // out = Add-MCN(x, y) for one value (the epilogue's combinations).
 template <typename T, int N, int POL>
 __device__ __forceinline__ void mm_add(const T (&x)[N], const T (&y)[N], T (&out)[N]) {

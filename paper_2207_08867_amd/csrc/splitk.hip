@@ -109,6 +109,7 @@ __device__ __forceinline__ void sk_term(T (&acc)[(AMC && BMC) ? NC : 1][NC], con
       scaling_terms<T, NC>(b, v, h);
     if constexpr (FIRST) {
       if (__builtin_expect(sr_try<T, NC, SPOL>(h, acc[p], v == T(0)), 0)) compact_nz<T, NC + 1, NC>(h, acc[p]);
+      nonfinite_tail<T, NC>(acc[p]);
     } else {
       T term[NC];
       if (__builtin_expect(sr_try<T, NC, SPOL>(h, term, v == T(0)), 0)) compact_nz<T, NC + 1, NC>(h, term);
