@@ -8,10 +8,13 @@
 //   e^x = 2^k 2^(j/64) e^r.
 // First stage, double-double: r from a three-part ln2/64 (the first part has 36
 // significant bits, so its product with |N| < 2^17 is exact), e^r = 1 + r + r^2/2 +
-// r^3/6 + ... with the terms below r^3 in binary64 Horner form (|r|^4/24 < 2^-34), the
-// table value 2^(j/64) as a double-double.  Its relative error is below 2^-75; the
-// result is final when every value within 2^-69 (relative) of it rounds to the same
-// binary64 number (to the same multiple of 2^-1074 for results below 2^-1021).
+// r^3 q(r) with r + r^2/2 kept exact as a double-double and q(r) = 1/3! + ... + r^6/9!
+// in binary64 Horner form (the terms beyond degree 9 are below 2^-96), the table value
+// 2^(j/64) as a double-double read from a copy in LDS.  Its relative error is below
+// 2^-75; the result is final when every value within 2^-69 (relative) of it rounds to
+// the same binary64 number (to the same multiple of 2^-1074 for results below 2^-1021).
+// Arguments below 2^-27 in magnitude (the low components of an expansion) take a
+// shorter first stage, 1 + x + x^2/2 + x^3/6, with the same test.
 // Otherwise -- about one argument in 2^16 -- the second stage evaluates e^x in 192-bit
 // fixed point (176 fraction bits: ln2/64 and 2^(j/64) to 176 bits, Taylor series of e^r
 // to degree 20, relative error below 2^-165) and rounds those bits to nearest.  e^x is
@@ -255,8 +258,14 @@ __device__ __forceinline__ U192 u_div_small(U192 a, uint32_t n) {
   return r;
 }
 
+// a.w[i] for 0 <= i < 3 (0 otherwise), by selection rather than an indexed access, so
+// nothing of a U192 lives in scratch memory.
+__device__ __forceinline__ uint64_t u_word(const U192 &a, int i) {
+  return i == 0 ? a.w[0] : i == 1 ? a.w[1] : i == 2 ? a.w[2] : 0ull;
+}
+
 __device__ __forceinline__ bool u_bit(const U192 &a, int pos) {
-  return (a.w[pos >> 6] >> (pos & 63)) & 1ull;
+  return (u_word(a, pos >> 6) >> (pos & 63)) & 1ull;
 }
 
 __device__ __forceinline__ bool u_any_below(const U192 &a, int pos) {  // a bit below position pos
@@ -271,8 +280,8 @@ __device__ __forceinline__ bool u_any_below(const U192 &a, int pos) {  // a bit 
 
 __device__ __forceinline__ uint64_t u_shr_low(const U192 &a, int s) {  // low 64 bits of a >> s
   const int i = s >> 6, b = s & 63;
-  uint64_t v = i < 3 ? a.w[i] >> b : 0;
-  if (b && i + 1 < 3) v |= a.w[i + 1] << (64 - b);
+  uint64_t v = u_word(a, i) >> b;
+  if (b) v |= u_word(a, i + 1) << (64 - b);
   return v;
 }
 
@@ -290,10 +299,12 @@ __device__ __noinline__ double exp64_fixed(double x, int N, int j, int k) {
   const uint64_t m = (uint64_t)__builtin_ldexp(f, 53);
   const int s = ex - 53 + 176;
   U192 X = {{0, 0, 0}};
-  if (s >= 0) {
+  if (s >= 0) {  // s < 192 - 53: the two words below stay inside X
     const int i = s >> 6, b = s & 63;
-    X.w[i] = m << b;
-    if (b && i + 1 < 3) X.w[i + 1] = m >> (64 - b);
+    const uint64_t lo = m << b, hi = b ? m >> (64 - b) : 0ull;
+    X.w[0] = i == 0 ? lo : 0ull;
+    X.w[1] = i == 1 ? lo : i == 0 ? hi : 0ull;
+    X.w[2] = i == 2 ? lo : i == 1 ? hi : 0ull;
   } else if (s > -64) {
     X.w[0] = m >> (-s);
   }
@@ -331,47 +342,79 @@ __device__ __noinline__ double exp64_fixed(double x, int N, int j, int k) {
   return __builtin_ldexp((double)n, -1074);
 }
 
-// Correctly rounded binary64 e^x.
-__device__ __forceinline__ double exp64_cr(double x) {
-  if (x != x) return x + x;
-  if (x > 710.0) return __builtin_inf();  // e^710 exceeds the largest binary64 number
-  if (x < -746.0) return 0.0;             // e^-746 is below half the smallest subnormal
-  const double Nd = __builtin_rint(x * EXP64_INV);
+// First stage of the correctly rounded binary64 e^x: returns true and sets y when the
+// double-double value decides the rounding (NaN, overflow and underflow included).
+// Special arguments are replaced by 0 for the arithmetic and their results selected at
+// the end, so the common path has no branch; |x| < 2^-27 and results below 2^-1021 take
+// their own branches.
+__device__ __forceinline__ bool exp64_first(double x, const double (*__restrict__ tdd)[2], double &y) {
+  const bool nan = x != x, over = x > 710.0, under = x < -746.0;
+  const bool special = nan || over || under;
+  // |x| < 2^-27 (the low components of an expansion): e^x = (1 + x) + x^2/2 + x^3/6 +
+  // O(2^-110), 1 + x split exactly into a double-double; the same margin test as below.
+  if (__builtin_fabs(x) < 0x1p-27) {
+    const DD a = dd_sum(1.0, x);
+    const double t = a.lo + (x * x) * (0.5 + x * INV_FACT[3]);
+    const double lo = a.hi + (t - 0x1p-69), hi = a.hi + (t + 0x1p-69);
+    y = x == 0.0 ? 1.0 : lo;
+    return x == 0.0 || lo == hi;
+  }
+  const double xs = special ? 0.0 : x;
+  const double Nd = __builtin_rint(xs * EXP64_INV);
   const int N = (int)Nd;
   const int j = N & 63;
   const int k = (N - j) / 64;
   // r = x - N ln2/64 as a double-double: N L1 is exact and so is x - N L1
-  const double t = x - Nd * EXP64_L1;
+  const double t = xs - Nd * EXP64_L1;
   const double p2 = Nd * EXP64_L2;
   const double e2 = __builtin_fma(Nd, EXP64_L2, -p2);
   DD r = dd_sum(t, -p2);
   r = dd_fast_sum(r.hi, (r.lo - e2) - Nd * EXP64_L3);
   const double rh = r.hi, rl = r.lo;
-  // e^r = 1 + r + r^2/2 + r^3/6 + r^4 q(r)
-  double q = INV_FACT[11];
-  for (int n = 10; n >= 4; --n) q = __builtin_fma(q, rh, INV_FACT[n]);
+  // e^r = 1 + r + r^2/2 + r^3 q(r), q = 1/3! + r/4! + ... + r^6/9! in binary64
+  double q = INV_FACT[9];
+  for (int n = 8; n >= 3; --n) q = __builtin_fma(q, rh, INV_FACT[n]);
   const double r2h = rh * rh;
   const double r2l = __builtin_fma(rh, rh, -r2h) + 2.0 * rh * rl;
-  const double c3 = r2h * rh * INV_FACT[3];
-  const double low = rl + 0.5 * r2l + (c3 + q * (r2h * r2h));
-  const DD a = dd_sum(1.0, rh);
-  const DD b = dd_sum(a.hi, 0.5 * r2h);
-  const DD P = dd_fast_sum(b.hi, (a.lo + b.lo) + low);
-  const DD Y = dd_mul(DD{EXP64_T_DD[j][0], EXP64_T_DD[j][1]}, P);
+  const double low = rl + 0.5 * r2l + q * (r2h * rh);
+  // P = 1 + (r + r^2/2) + low: r + r^2/2 split exactly, 1 + its high part exactly
+  const DD s2 = dd_sum(rh, 0.5 * r2h);
+  const DD o = dd_fast_sum(1.0, s2.hi);
+  const double pl = o.lo + (s2.lo + low);
+  // Y = 2^(j/64) P, left unnormalized (|Y.lo| < 2^-24 |Y.hi|): the margin test below
+  // takes it as it is; the rounding to a multiple of 2^-1074 normalizes it first
+  const double th = tdd[j][0], tl = tdd[j][1];
+  const double p = th * o.hi;
+  const DD Y = {p, __builtin_fma(th, o.hi, -p) + (th * pl + tl * o.hi)};
+  bool ok;
+  double v = 0.0;
   if (k >= -1021) {
     const double e = 0x1p-69 * Y.hi;
     const double lo = Y.hi + (Y.lo - e), hi = Y.hi + (Y.lo + e);
-    if (lo == hi) return __builtin_ldexp(lo, k);
+    v = __builtin_ldexp(lo, k);
+    ok = lo == hi;
   } else {  // results below 2^-1021: round to a multiple of 2^-1074
-    const double zh = __builtin_ldexp(Y.hi, k + 1074), zl = __builtin_ldexp(Y.lo, k + 1074);
+    const DD Z = dd_fast_sum(Y.hi, Y.lo);
+    const double zh = __builtin_ldexp(Z.hi, k + 1074), zl = __builtin_ldexp(Z.lo, k + 1074);
     const double i = __builtin_rint(zh);
     const double d = (zh - i) + zl;
     const double e = 0x1p-69 * zh;
-    if (d < 0.5 - e && d > -0.5 + e) return __builtin_ldexp(i, -1074);
-    if (d > 0.5 + e) return __builtin_ldexp(i + 1.0, -1074);
-    if (d < -0.5 - e) return __builtin_ldexp(i - 1.0, -1074);
+    ok = true;
+    if (d < 0.5 - e && d > -0.5 + e) v = i;
+    else if (d > 0.5 + e) v = i + 1.0;
+    else if (d < -0.5 - e) v = i - 1.0;
+    else ok = false;
+    v = __builtin_ldexp(v, -1074);
   }
-  return exp64_fixed(x, N, j, k);
+  y = nan ? x + x : over ? __builtin_inf() : under ? 0.0 : v;
+  return special || ok;
+}
+
+// Second stage for the arguments the first leaves undecided (about one in 2^16).
+__device__ __noinline__ double exp64_second(double x) {
+  const int N = (int)__builtin_rint(x * EXP64_INV);
+  const int j = N & 63;
+  return exp64_fixed(x, N, j, (N - j) / 64);
 }
 
 // Exp-MCN of one element: h = (e^x_0), then h = ScalingN(h, e^x_i) with expand.
@@ -392,16 +435,44 @@ constexpr int EXP64_THREADS = 256;
 template <int NC>
 __global__ __launch_bounds__(EXP64_THREADS) void exp64_kernel(const double *__restrict__ x,
                                                               double *__restrict__ out, int64_t n) {
+  __shared__ double tdd[64][2];
+  if (threadIdx.x < 128) tdd[threadIdx.x >> 1][threadIdx.x & 1] = EXP64_T_DD[threadIdx.x >> 1][threadIdx.x & 1];
+  __syncthreads();
   const int64_t stride = (int64_t)gridDim.x * EXP64_THREADS;
-  for (int64_t i = (int64_t)blockIdx.x * EXP64_THREADS + threadIdx.x; i < n; i += stride) {
-    double ex[NC];
+  int64_t i = (int64_t)blockIdx.x * EXP64_THREADS + threadIdx.x;
+  if (i >= n) return;
+  double cur[NC];
 #pragma unroll
-    for (int c = 0; c < NC; ++c) ex[c] = exp64_cr(x[c * n + i]);
+  for (int c = 0; c < NC; ++c) cur[c] = x[c * n + i];
+  while (true) {
+    // the next element's loads go out before this one's arithmetic (the last lane
+    // iteration re-reads its own element)
+    const int64_t nx = i + stride;
+    const bool more = nx < n;
+    const int64_t ni = more ? nx : i;
+    double nxt[NC];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) nxt[c] = x[c * n + ni];
+    double ex[NC];
+    bool ok = true;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) ok = exp64_first(cur[c], tdd, ex[c]) && ok;
+    if (!ok) {
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        double y;
+        if (!exp64_first(cur[c], tdd, y)) ex[c] = exp64_second(cur[c]);
+      }
+    }
     const double h0[1] = {ex[0]};
     double r[NC];
     exp64_chain<NC, 1>(h0, ex, r);
 #pragma unroll
     for (int c = 0; c < NC; ++c) out[c * n + i] = r[c];
+    if (!more) break;
+    i = nx;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) cur[c] = nxt[c];
   }
 }
 

@@ -22,7 +22,8 @@ typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
 enum ProbeOp {
   P_ADD_F32 = 0, P_MUL_F32, P_FMA_F32, P_ADD_F16, P_MUL_F16, P_FMA_F16, P_PK_ADD_F16, P_MIN3_F32, P_CVT_F16_F32,
   P_CVT_F32_F16, P_FMA_MIX_F32, P_FMA_MIXLO_F16, P_ADD_F64, P_FMA_F64, P_ADD_U32, P_AND_B32, P_ADD3_U32,
-  P_BFE_U32, P_LDEXP_F16, P_COUNT
+  P_BFE_U32, P_LDEXP_F16, P_MUL_F64, P_LDEXP_F64, P_RNDNE_F64, P_CVT_I32_F64, P_CMP_LT_F64, P_MOV_B64,
+  P_LSHL_ADD_U64, P_COUNT
 };
 
 template <int OP>
@@ -32,6 +33,8 @@ __global__ __launch_bounds__(256) void probe_kernel(float *out, uint64_t *clocks
   double d[CH];
   half2_t p[CH];
   unsigned u[CH];
+  uint64_t q[CH];
+  uint64_t sc[CH];
 #pragma unroll
   for (int c = 0; c < CH; ++c) {
     f[c] = seed + (float)c + (float)threadIdx.x;
@@ -39,12 +42,15 @@ __global__ __launch_bounds__(256) void probe_kernel(float *out, uint64_t *clocks
     d[c] = (double)seed + c;
     p[c] = half2_t{h[c], h[c]};
     u[c] = threadIdx.x + c;
+    q[c] = threadIdx.x + 7 * c;
+    sc[c] = 0;
   }
   const float g = seed * 0.5f;
   const _Float16 hg = (_Float16)g;
   const double dg = g;
   const half2_t pg = half2_t{hg, hg};
   const unsigned ug = 3u;
+  const uint64_t qg = 5u;
   const int ig = -1;
   const uint64_t t0 = clock64(), w0 = wall_clock64();
   for (int it = 0; it < iters; ++it) {
@@ -73,13 +79,20 @@ __global__ __launch_bounds__(256) void probe_kernel(float *out, uint64_t *clocks
         if constexpr (OP == P_ADD3_U32) asm volatile("v_add3_u32 %0, %0, %1, %1" : "+v"(u[c]) : "v"(ug));
         if constexpr (OP == P_BFE_U32) asm volatile("v_bfe_u32 %0, %0, %1, %1" : "+v"(u[c]) : "v"(ug));
         if constexpr (OP == P_LDEXP_F16) asm volatile("v_ldexp_f16 %0, %0, %1" : "+v"(h[c]) : "v"(ig));
+        if constexpr (OP == P_MUL_F64) asm volatile("v_mul_f64 %0, %0, %1" : "+v"(d[c]) : "v"(dg));
+        if constexpr (OP == P_LDEXP_F64) asm volatile("v_ldexp_f64 %0, %0, %1" : "+v"(d[c]) : "v"(ig));
+        if constexpr (OP == P_RNDNE_F64) asm volatile("v_rndne_f64 %0, %0" : "+v"(d[c]));
+        if constexpr (OP == P_CVT_I32_F64) asm volatile("v_cvt_i32_f64 %0, %1" : "=v"(u[c]) : "v"(d[c]));
+        if constexpr (OP == P_CMP_LT_F64) asm volatile("v_cmp_lt_f64_e64 %0, %1, %2" : "=s"(sc[c]) : "v"(d[c]), "v"(dg));
+        if constexpr (OP == P_MOV_B64) asm volatile("v_mov_b64 %0, %0" : "+v"(d[c]));
+        if constexpr (OP == P_LSHL_ADD_U64) asm volatile("v_lshl_add_u64 %0, %0, 1, %1" : "+v"(q[c]) : "v"(qg));
       }
     }
   }
   const uint64_t t1 = clock64(), w1 = wall_clock64();
   float s = 0.0f;
 #pragma unroll
-  for (int c = 0; c < CH; ++c) s += f[c] + (float)h[c] + (float)d[c] + (float)p[c].x + (float)u[c];
+  for (int c = 0; c < CH; ++c) s += f[c] + (float)h[c] + (float)d[c] + (float)p[c].x + (float)u[c] + (float)q[c] + (float)sc[c];
   if (s == 1234.5f) out[blockIdx.x * blockDim.x + threadIdx.x] = s;
   if (threadIdx.x == 0) {
     clocks[2 * blockIdx.x] = t1 - t0;
@@ -105,7 +118,8 @@ hipError_t launch_op(int op, int blocks, int iters, float *out, uint64_t *clocks
 const char *const NAMES[P_COUNT] = {
     "v_add_f32", "v_mul_f32", "v_fma_f32", "v_add_f16", "v_mul_f16", "v_fma_f16", "v_pk_add_f16", "v_min3_f32",
     "v_cvt_f16_f32", "v_cvt_f32_f16", "v_fma_mix_f32", "v_fma_mixlo_f16", "v_add_f64", "v_fma_f64", "v_add_u32",
-    "v_and_b32", "v_add3_u32", "v_bfe_u32", "v_ldexp_f16"};
+    "v_and_b32", "v_add3_u32", "v_bfe_u32", "v_ldexp_f16", "v_mul_f64", "v_ldexp_f64", "v_rndne_f64",
+    "v_cvt_i32_f64", "v_cmp_lt_f64", "v_mov_b64", "v_lshl_add_u64"};
 
 }  // namespace
 

@@ -1,6 +1,7 @@
 """Writes exp64_near_midpoints.txt: binary64 arguments x whose e^x lies within 2^-72
 (relative) of a binary64 rounding boundary, found by the oracle's binary128 search over
-seeded random arguments (whole range, and the range of subnormal results).  A
+seeded random arguments (whole range, the range of subnormal results, and |x| < 2^-27,
+where e^x is 1 + x + x^2/2 + ... to far beyond binary64).  A
 correctly rounded binary64 exponential that first evaluates e^x to a few bits beyond
 2^-70 must take its slow path on every one of them.  Run from the repository root:
     python tests/golden/make_exp64_near_midpoints.py
@@ -14,7 +15,8 @@ sys.path.insert(0, ROOT)
 import oracle  # noqa: E402
 
 REL = 2.0 ** -72
-runs = [(-745.0, 709.7, 1, 1 << 26), (-745.13, -708.4, 2, 1 << 24), (-0.5, 0.5, 3, 1 << 24)]
+runs = [(-745.0, 709.7, 1, 1 << 26), (-745.13, -708.4, 2, 1 << 24), (-0.5, 0.5, 3, 1 << 24),
+        (-2.0 ** -27, 2.0 ** -27, 4, 1 << 24)]
 xs = []
 for lo, hi, seed, tries in runs:
     xs.extend(float(v) for v in oracle.exp64_near_midpoints(lo, hi, seed, tries, REL, max_out=100000))

@@ -63,7 +63,7 @@ def _near_midpoints():
 def test_exp64_component_exponential(mcf, orc):
     """nc = 1 Exp-MCN is the correctly rounded binary64 e^x: 2^24 random arguments over
     the whole range (about 2^-15 of them take the 192-bit fixed-point stage), the range
-    of subnormal results, tiny arguments, boundaries, special values, and the 255
+    of subnormal results, tiny arguments, boundaries, special values, and the 311
     arguments whose e^x lies within 2^-72 of a rounding boundary (every one takes the
     fixed-point stage)."""
     g = np.random.default_rng(4100)
