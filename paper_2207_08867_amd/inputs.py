@@ -85,7 +85,7 @@ def matmul_uniform(M, N, K, nc, dtype, seed=0, lo=-1.0, hi=1.0):
 def matmul_normal(M, N, K, nc, dtype, seed=0):
     """A, B entries float64 ~ N(0, 1/K), split into nc components (A drawn first)."""
     g = rng(seed)
-    s = 1.0 / np.sqrt(K)
+    s = 1.0 / np.sqrt(K) if K > 0 else 1.0
     A = split(g.normal(0.0, s, (M, K)), nc, dtype)
     B = split(g.normal(0.0, s, (K, N)), nc, dtype)
     return A, B
@@ -94,7 +94,7 @@ def matmul_normal(M, N, K, nc, dtype, seed=0):
 def matmul_normal_scaled(M, N, K, nc, seed=0):
     """The same draws as matmul_normal, split into scaled binary16 components."""
     g = rng(seed)
-    s = 1.0 / np.sqrt(K)
+    s = 1.0 / np.sqrt(K) if K > 0 else 1.0
     A = split_scaled(g.normal(0.0, s, (M, K)), nc)
     B = split_scaled(g.normal(0.0, s, (K, N)), nc)
     return A, B
