@@ -92,8 +92,8 @@ struct SliceOp {
 };
 
 // Level statistics of a workgroup: wavefront maxima, then the workgroup maximum, then
-// an atomic only if it raises the stored word (a plain read first: every workgroup
-// would otherwise update the same two words, and same-address atomics serialise).
+// one atomic maximum per kind into the workgroup's slot (no value returned, so the
+// workgroup does not wait for it; the XSLOTS slots keep same-address atomics few).
 // Every lane of the workgroup must call this.
 __device__ __forceinline__ void x_stats(uint32_t *stats, int kind_hi, int kind_lo, uint32_t top, uint32_t low) {
   __shared__ uint32_t red[2][XS_THREADS / 64];
@@ -113,8 +113,8 @@ __device__ __forceinline__ void x_stats(uint32_t *stats, int kind_hi, int kind_l
     }
     const int slot = (int)(blockIdx.x % XSLOTS) * 64;
     uint32_t *hi = stats + (kind_hi * XSLOTS) * 64 + slot, *lo = stats + (kind_lo * XSLOTS) * 64 + slot;
-    if (bt > __atomic_load_n(hi, __ATOMIC_RELAXED)) atomicMax(hi, bt);
-    if (bl > __atomic_load_n(lo, __ATOMIC_RELAXED)) atomicMax(lo, bl);
+    if (bt) atomicMax(hi, bt);
+    if (bl) atomicMax(lo, bl);
   }
 }
 
