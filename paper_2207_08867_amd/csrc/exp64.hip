@@ -13,8 +13,8 @@
 // 2^(j/64) as a double-double read from a copy in LDS.  Its relative error is below
 // 2^-75; the result is final when every value within 2^-69 (relative) of it rounds to
 // the same binary64 number (to the same multiple of 2^-1074 for results below 2^-1021).
-// Arguments below 2^-27 in magnitude (the low components of an expansion) take a
-// shorter first stage, 1 + x + x^2/2 + x^3/6, with the same test.
+// When every argument of a wavefront is below 2^-27 in magnitude (the low components of
+// an expansion), a shorter first stage, 1 + x + x^2/2 + x^3/6, takes the same test.
 // Otherwise -- about one argument in 2^16 -- the second stage evaluates e^x in 192-bit
 // fixed point (176 fraction bits: ln2/64 and 2^(j/64) to 176 bits, Taylor series of e^r
 // to degree 20, relative error below 2^-165) and rounds those bits to nearest.  e^x is
@@ -342,23 +342,25 @@ __device__ __noinline__ double exp64_fixed(double x, int N, int j, int k) {
   return __builtin_ldexp((double)n, -1074);
 }
 
-// First stage of the correctly rounded binary64 e^x: returns true and sets y when the
-// double-double value decides the rounding (NaN, overflow and underflow included).
+// First stage for |x| < 2^-27 (the low components of an expansion): e^x = (1 + x) +
+// x^2/2 + x^3/6 + O(2^-110), 1 + x split exactly into a double-double; the same margin
+// test as the general first stage.  Returns true and sets y when it decides the rounding.
+__device__ __forceinline__ bool exp64_first_small(double x, double &y) {
+  const DD a = dd_sum(1.0, x);
+  const double t = a.lo + (x * x) * (0.5 + x * INV_FACT[3]);
+  const double lo = a.hi + (t - 0x1p-69), hi = a.hi + (t + 0x1p-69);
+  y = x == 0.0 ? 1.0 : lo;
+  return x == 0.0 || lo == hi;
+}
+
+// First stage of the correctly rounded binary64 e^x, any x: returns true and sets y when
+// the double-double value decides the rounding (NaN, overflow and underflow included).
 // Special arguments are replaced by 0 for the arithmetic and their results selected at
-// the end, so the common path has no branch; |x| < 2^-27 and results below 2^-1021 take
-// their own branches.
+// the end; results below 2^-1021 take a branch that is uniform across the wavefront, so
+// the common path runs without one.
 __device__ __forceinline__ bool exp64_first(double x, const double (*__restrict__ tdd)[2], double &y) {
   const bool nan = x != x, over = x > 710.0, under = x < -746.0;
   const bool special = nan || over || under;
-  // |x| < 2^-27 (the low components of an expansion): e^x = (1 + x) + x^2/2 + x^3/6 +
-  // O(2^-110), 1 + x split exactly into a double-double; the same margin test as below.
-  if (__builtin_fabs(x) < 0x1p-27) {
-    const DD a = dd_sum(1.0, x);
-    const double t = a.lo + (x * x) * (0.5 + x * INV_FACT[3]);
-    const double lo = a.hi + (t - 0x1p-69), hi = a.hi + (t + 0x1p-69);
-    y = x == 0.0 ? 1.0 : lo;
-    return x == 0.0 || lo == hi;
-  }
   const double xs = special ? 0.0 : x;
   const double Nd = __builtin_rint(xs * EXP64_INV);
   const int N = (int)Nd;
@@ -386,27 +388,29 @@ __device__ __forceinline__ bool exp64_first(double x, const double (*__restrict_
   const double th = tdd[j][0], tl = tdd[j][1];
   const double p = th * o.hi;
   const DD Y = {p, __builtin_fma(th, o.hi, -p) + (th * pl + tl * o.hi)};
-  bool ok;
-  double v = 0.0;
-  if (k >= -1021) {
-    const double e = 0x1p-69 * Y.hi;
-    const double lo = Y.hi + (Y.lo - e), hi = Y.hi + (Y.lo + e);
-    v = __builtin_ldexp(lo, k);
-    ok = lo == hi;
-  } else {  // results below 2^-1021: round to a multiple of 2^-1074
-    const DD Z = dd_fast_sum(Y.hi, Y.lo);
-    const double zh = __builtin_ldexp(Z.hi, k + 1074), zl = __builtin_ldexp(Z.lo, k + 1074);
-    const double i = __builtin_rint(zh);
-    const double d = (zh - i) + zl;
-    const double e = 0x1p-69 * zh;
-    ok = true;
-    if (d < 0.5 - e && d > -0.5 + e) v = i;
-    else if (d > 0.5 + e) v = i + 1.0;
-    else if (d < -0.5 - e) v = i - 1.0;
-    else ok = false;
-    v = __builtin_ldexp(v, -1074);
+  const double e = 0x1p-69 * Y.hi;
+  const double lo = Y.hi + (Y.lo - e), hi = Y.hi + (Y.lo + e);
+  double v = __builtin_ldexp(lo, k);
+  bool ok = lo == hi;
+  const bool sub = k < -1021;
+  if (__builtin_expect(__any(sub), 0)) {
+    if (sub) {  // results below 2^-1021: round to a multiple of 2^-1074
+      const DD Z = dd_fast_sum(Y.hi, Y.lo);
+      const double zh = __builtin_ldexp(Z.hi, k + 1074), zl = __builtin_ldexp(Z.lo, k + 1074);
+      const double i = __builtin_rint(zh);
+      const double d = (zh - i) + zl;
+      const double ez = 0x1p-69 * zh;
+      ok = true;
+      double w = 0.0;
+      if (d < 0.5 - ez && d > -0.5 + ez) w = i;
+      else if (d > 0.5 + ez) w = i + 1.0;
+      else if (d < -0.5 - ez) w = i - 1.0;
+      else ok = false;
+      v = __builtin_ldexp(w, -1074);
+    }
   }
-  y = nan ? x + x : over ? __builtin_inf() : under ? 0.0 : v;
+  const double sv = nan ? x + x : (over ? __builtin_inf() : 0.0);
+  y = special ? sv : v;
   return special || ok;
 }
 
@@ -453,16 +457,24 @@ __global__ __launch_bounds__(EXP64_THREADS) void exp64_kernel(const double *__re
     double nxt[NC];
 #pragma unroll
     for (int c = 0; c < NC; ++c) nxt[c] = x[c * n + ni];
+    // the short first stage when every lane's argument is small (the general one is
+    // valid for small arguments too), then the second stage where a lane needs it
     double ex[NC];
+    bool okc[NC];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      if (__all(__builtin_fabs(cur[c]) < 0x1p-27))
+        okc[c] = exp64_first_small(cur[c], ex[c]);
+      else
+        okc[c] = exp64_first(cur[c], tdd, ex[c]);
+    }
     bool ok = true;
 #pragma unroll
-    for (int c = 0; c < NC; ++c) ok = exp64_first(cur[c], tdd, ex[c]) && ok;
-    if (!ok) {
+    for (int c = 0; c < NC; ++c) ok = ok && okc[c];
+    if (__builtin_expect(__any(!ok), 0)) {
 #pragma unroll
-      for (int c = 0; c < NC; ++c) {
-        double y;
-        if (!exp64_first(cur[c], tdd, y)) ex[c] = exp64_second(cur[c]);
-      }
+      for (int c = 0; c < NC; ++c)
+        if (!okc[c]) ex[c] = exp64_second(cur[c]);
     }
     const double h0[1] = {ex[0]};
     double r[NC];

@@ -77,6 +77,25 @@ def test_exp64_component_exponential(mcf, orc):
     assert_bits(got, orc.fl_exp64(xs), "binary64 e^x")
 
 
+def test_exp64_small_arguments(mcf, orc):
+    """Arguments below 2^-27 in magnitude fill whole wavefronts (the short first stage
+    runs only then): random ones of every scale, the near-boundary ones of the fixture
+    (each of which must reach the fixed-point stage), as nc = 1 values and as the low
+    component of nc = 2 values."""
+    nm = _near_midpoints()
+    small = nm[np.abs(nm) < 2.0 ** -27]
+    assert small.size >= 40
+    g = np.random.default_rng(4101)
+    rnd = g.uniform(-1, 1, 1 << 16) * np.exp2(g.integers(-1074 + 60, -27, 1 << 16).astype(np.float64))
+    xs = np.concatenate([np.tile(small, 64), rnd, [0.0, -0.0, 5e-324, -5e-324]])
+    got = to_host(mcf.mc_exp(to_dev(xs[None]), nc=1))[0]
+    assert_bits(got, orc.fl_exp64(xs), "binary64 e^x, small arguments")
+    x2 = np.zeros((2, xs.size))
+    x2[0] = g.uniform(-5, 5, xs.size)
+    x2[1] = xs
+    assert_bits(to_host(mcf.mc_exp(to_dev(x2), nc=2)), orc.exp(x2, nc=2), "Exp-MCN f64 small low components")
+
+
 @pytest.mark.parametrize("nc", [2, 3, 4])
 def test_exp_mcn_f64(mcf, orc, nc):
     """Exp-MCN over binary64 expansions (components from a draw of e^x-sized
