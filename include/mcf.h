@@ -217,8 +217,7 @@ int mc_addmm(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, 
  *   slices <= 0 selects mc_matmul_splitk_slices(M, N, K).
  * workspace: device memory of at least mc_matmul_splitk_workspace(...) bytes (the
  *   partial tree roots: G = ceil(S / 256) entries of planes x nc x M x N components
- *   when S > 256, plus ceil(G / 256) more when G > 256; planes = nc for MC x MC, else
- *   1), owned
+ *   when S > 256; planes = nc for MC x MC, else 1), owned
  *   by the caller, not overlapping A, B or C; may be NULL when that size is 0.  Its
  *   contents on entry do not matter; calls sharing a workspace must not overlap
  *   in time.  Too small: MCF_E_ARG; NULL when needed: MCF_E_NULL.
@@ -235,7 +234,7 @@ int mc_matmul_splitk(int dtype, int nc, int64_t M, int64_t N, int64_t K, const v
  * caller workspace; the call allocates nothing.
  * Limit: calls whose mc_matmul_splitk_workspace(...) exceeds 8 MiB (8388608 bytes)
  *   return MCF_E_SCRATCH and launch nothing.  With the default slice count the roots
- *   take at most 0.25 MiB (binary64, nc = 4, MC x MC), so the limit binds only for
+ *   take at most 1 MiB (binary64, nc = 4, MC x MC), so the limit binds only for
  *   large explicit slice counts on many outputs.
  * Sharing: every call on a device uses that device's one scratch array, so calls on
  *   one device that overlap in time (different streams, or different host threads)
@@ -247,8 +246,8 @@ int mc_matmul_splitk_noalloc(int dtype, int nc, int64_t M, int64_t N, int64_t K,
                              const void *B, int b_mc, int64_t slices, void *C, void *stream);
 
 /* Default slice count of mc_matmul_splitk, a function of the shape only: enough
- * slices for about 2^18 lanes in total (ceil(2^18 / (M N))), at most K / 8 (so a
- * slice holds at least 8 terms when K allows), at most 2^20, at least 1.
+ * slices for about 2^20 lanes in total (ceil(2^20 / (M N))), at most K / 64 (so a
+ * slice holds at least 64 terms when K allows), at most 2^20, at least 1.
  * Negative sizes: MCF_E_SHAPE. */
 int64_t mc_matmul_splitk_slices(int64_t M, int64_t N, int64_t K);
 

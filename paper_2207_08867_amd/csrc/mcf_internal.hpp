@@ -54,14 +54,16 @@ hipError_t launch_matmul(int dtype, int nc, int64_t M, int64_t N, int64_t K, con
                          const void *B, int b_mc, int b_trans, const void *bias, void *C, hipStream_t stream);
 
 // K-split product (splitk.hip).  S slices (1 <= S <= min(K, SPLITK_MAX_SLICES)); W is
-// a workspace of splitk_workspace_elems(...) components when S exceeds one
-// workgroup's slice group, else unused.
-constexpr int64_t SPLITK_TARGET_LANES = (int64_t)1 << 18;
+// a workspace of splitk_roots(S) entries when S exceeds one workgroup's slice group,
+// else unused.  The default slice count aims at SPLITK_TARGET_LANES lanes in all
+// and keeps at least SPLITK_MIN_STEPS reduction steps per slice.
+constexpr int64_t SPLITK_TARGET_LANES = (int64_t)1 << 20;
+constexpr int64_t SPLITK_MIN_STEPS = 64;
 constexpr int64_t SPLITK_MAX_SLICES = (int64_t)1 << 20;
 int64_t splitk_default_slices(int64_t M, int64_t N, int64_t K);
 void splitk_shape(int64_t S, int *KS, int *G);
 // Workspace entries (each NP x nc components per output) for S slices: the G slice
-// group roots and, when G exceeds one workgroup's 256, the roots of their groups of 256.
+// group roots when G > 1, else none.
 int64_t splitk_roots(int64_t S);
 hipError_t launch_matmul_splitk(int dtype, int nc, int64_t M, int64_t N, int64_t K, const void *A, int a_mc,
                                 const void *B, int b_mc, int64_t S, void *W, void *C, hipStream_t stream);

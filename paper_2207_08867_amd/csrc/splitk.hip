@@ -16,11 +16,12 @@
 // so the lanes of a slice group read consecutive k.  The first log2(KS) tree levels
 // run inside the workgroup (strides < 64 by lane exchange inside a wavefront, 64 and
 // 128 through LDS); when S > KS the G = ceil(S/KS) group results go to a workspace
-// and a second kernel runs the next levels the same way over aligned groups of up to
-// 256 roots (a third launch combines the ceil(G/256) roots of the second when G >
-// 256).  Because every group is an aligned block of the level below, the split
-// between launches never pairs entries across groups: the result equals the tree's
-// definition for every launch shape.
+// and a second kernel runs all further levels in one launch: each of its lanes takes an
+// aligned block of R consecutive roots (R = 1, 4 or 16, the smallest with G <= 256 R)
+// and runs the first log2(R) of those levels in registers, and the lanes then run the
+// last levels as in the first kernel.  Because every group and block is an aligned
+// block of the level below, a pair of the tree never straddles two of them: the
+// result equals the tree's definition for every launch shape.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -190,36 +191,79 @@ __global__ __launch_bounds__(SK_THREADS) void sk_kernel(const T *__restrict__ A,
   }
 }
 
-// Phase 2: the next tree levels over the G entries of each output in W, in aligned
-// groups of up to 256 (block y of the grid takes entries 256 y .. 256 y + 255), GW
-// lanes per output (GW = the group size rounded up to a power of two).  With one
-// group (G <= 256) the root is the result and goes to C; otherwise group y's root goes
-// to entry y of Wn [ceil(G/256)][NP][NC][M*N].
-template <typename T, int NC, int NP, int APOL>
-__global__ __launch_bounds__(SK_THREADS) void sk_reduce_kernel(const T *__restrict__ W, T *__restrict__ Wn,
-                                                               T *__restrict__ C, int64_t MN, int G, int GW) {
+// Phase 2: the tree levels above the G group roots of each output in W, in one launch.
+// Lane q of an output's GW-lane group takes roots q R .. q R + R - 1 (those below G)
+// and folds them in tree order in registers: entry j is pushed after one Add-MCN with
+// each completed left neighbour (one per trailing one bit of j), and what is left
+// when fewer than R are present combines lowest level first -- an unpaired right
+// entry moves up until it meets its left partner, as the tree's rule has it.  The
+// lanes then run the last levels as a group tree over ceil(G / R) entries.
+template <int R>
+struct log2_of {
+  static constexpr int value = R <= 1 ? 0 : 1 + log2_of<R / 2>::value;
+};
+template <>
+struct log2_of<1> {
+  static constexpr int value = 0;
+};
+
+template <typename T, int NC, int NP, int APOL, int R>
+__global__ __launch_bounds__(SK_THREADS) void sk_reduce_kernel(const T *__restrict__ W, T *__restrict__ C, int64_t MN,
+                                                               int G, int GW) {
+  constexpr int L = log2_of<R>::value;
   __shared__ T lds[SK_THREADS][NP * NC];
   const int q = threadIdx.x & (GW - 1);
   const int64_t o = (int64_t)blockIdx.x * (SK_THREADS / GW) + threadIdx.x / GW;
-  const int base = (int)blockIdx.y * SK_THREADS;
-  const int count = G - base < SK_THREADS ? G - base : SK_THREADS;
+  const int first = q * R;
+  const int n = (o < MN && first < G) ? (G - first < R ? G - first : R) : 0;
+  // Loads stay in bounds for absent entries (the last root of the last output) so that
+  // they can all be issued before the arithmetic; absent entries are never used.
+  const int64_t ol = o < MN ? o : MN - 1;
+  T stk[L + 1][NP][NC];
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    const int64_t e = first + j < G ? first + j : G - 1;
+    T v[NP][NC];
+#pragma unroll
+    for (int p = 0; p < NP; ++p)
+#pragma unroll
+      for (int c = 0; c < NC; ++c) v[p][c] = W[((e * NP + p) * NC + c) * MN + ol];
+    if (j < n) {
+      int l = 0;
+#pragma unroll
+      for (; l < L && ((j >> l) & 1); ++l) {
+#pragma unroll
+        for (int p = 0; p < NP; ++p) mm_add<T, NC, APOL>(stk[l][p], v[p], v[p]);
+      }
+#pragma unroll
+      for (int p = 0; p < NP; ++p)
+#pragma unroll
+        for (int c = 0; c < NC; ++c) stk[l][p][c] = v[p][c];
+    }
+  }
   T acc[NP][NC];
 #pragma unroll
   for (int p = 0; p < NP; ++p)
 #pragma unroll
-    for (int c = 0; c < NC; ++c)
-      acc[p][c] = (o < MN && q < count) ? W[(((int64_t)(base + q) * NP + p) * NC + c) * MN + o] : T(0);
-  group_tree<T, NC, NP, APOL>(acc, q, GW, count, lds);
-  if (q == 0 && o < MN) {
-    if (G <= SK_THREADS) {
-      sk_store<T, NC, NP, APOL>(acc, C, MN, o);
-    } else {
+    for (int c = 0; c < NC; ++c) acc[p][c] = T(0);
+  bool have = false;
 #pragma unroll
-      for (int p = 0; p < NP; ++p)
+  for (int l = 0; l <= L; ++l) {
+    if ((n >> l) & 1) {
 #pragma unroll
-        for (int c = 0; c < NC; ++c) Wn[(((int64_t)blockIdx.y * NP + p) * NC + c) * MN + o] = acc[p][c];
+      for (int p = 0; p < NP; ++p) {
+        if (have) {
+          mm_add<T, NC, APOL>(stk[l][p], acc[p], acc[p]);
+        } else {
+#pragma unroll
+          for (int c = 0; c < NC; ++c) acc[p][c] = stk[l][p][c];
+        }
+      }
+      have = true;
     }
   }
+  group_tree<T, NC, NP, APOL>(acc, q, GW, (G + R - 1) / R, lds);
+  if (q == 0 && o < MN) sk_store<T, NC, NP, APOL>(acc, C, MN, o);
 }
 
 static int pow2_at_least(int64_t v) {
@@ -232,7 +276,7 @@ int64_t splitk_default_slices(int64_t M, int64_t N, int64_t K) {
   const int64_t MN = M * N;
   if (MN <= 0 || K <= 0) return 1;
   int64_t s = ((int64_t)SPLITK_TARGET_LANES + MN - 1) / MN;
-  const int64_t by_k = K / 8 > 1 ? K / 8 : 1;
+  const int64_t by_k = K / SPLITK_MIN_STEPS > 1 ? K / SPLITK_MIN_STEPS : 1;
   if (s > by_k) s = by_k;
   if (s > SPLITK_MAX_SLICES) s = SPLITK_MAX_SLICES;
   return s < 1 ? 1 : s;
@@ -247,8 +291,15 @@ void splitk_shape(int64_t S, int *KS, int *G) {
 int64_t splitk_roots(int64_t S) {
   int KS, G;
   splitk_shape(S, &KS, &G);
-  if (G == 1) return 0;
-  return G + (G > SK_THREADS ? (G + SK_THREADS - 1) / SK_THREADS : 0);
+  return G == 1 ? 0 : G;
+}
+
+template <typename T, int NC, int NP, int APOL, int R>
+static void sk_reduce_launch(const T *W, T *C, int64_t MN, int G, hipStream_t s) {
+  const int lanes = (G + R - 1) / R;
+  const int GW = pow2_at_least(lanes);
+  dim3 grid((unsigned)((MN + (SK_THREADS / GW) - 1) / (SK_THREADS / GW)));
+  hipLaunchKernelGGL((sk_reduce_kernel<T, NC, NP, APOL, R>), grid, dim3(SK_THREADS), 0, s, W, C, MN, G, GW);
 }
 
 template <typename T, int NC, bool AMC, bool BMC>
@@ -261,27 +312,21 @@ static hipError_t sk_launch(int64_t M, int64_t N, int64_t K, const void *A, cons
   const int64_t MN = M * N;
   int KS, G;
   splitk_shape(S, &KS, &G);
+  // S <= SPLITK_MAX_SLICES = 2^20 gives G <= 4096 = 16 x 256 group roots.
+  if (G > 16 * SK_THREADS) return hipErrorInvalidValue;
   dim3 grid((unsigned)((MN + (SK_THREADS / KS) - 1) / (SK_THREADS / KS)), (unsigned)G);
   hipLaunchKernelGGL((sk_kernel<T, NC, AMC, BMC, SPOL, APOL>), grid, dim3(SK_THREADS), 0, s, (const T *)A,
                      (const T *)B, (T *)C, (T *)W, M, N, K, S, KS, G);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || G == 1) return e;
-  // W: [G] group roots, then [ceil(G/256)] roots of their groups of 256 (G > 256).
-  // S <= SPLITK_MAX_SLICES = 2^20 gives G <= 4096, so the second level has at most
-  // 16 entries and a third launch finishes.
-  T *lvl = (T *)W, *next = (T *)W + (int64_t)G * NP * NC * MN;
-  for (int g = G;;) {
-    const int GW = pow2_at_least(g < SK_THREADS ? g : SK_THREADS);
-    const int groups = (g + SK_THREADS - 1) / SK_THREADS;
-    dim3 grid2((unsigned)((MN + (SK_THREADS / GW) - 1) / (SK_THREADS / GW)), (unsigned)groups);
-    hipLaunchKernelGGL((sk_reduce_kernel<T, NC, NP, APOL>), grid2, dim3(SK_THREADS), 0, s, (const T *)lvl, next,
-                       (T *)C, MN, g, GW);
-    e = hipGetLastError();
-    if (e != hipSuccess || groups == 1) return e;
-    if (groups > SK_THREADS) return hipErrorInvalidValue;  // beyond SPLITK_MAX_SLICES
-    lvl = next;
-    g = groups;
-  }
+  // W: the G group roots.
+  if (G <= SK_THREADS)
+    sk_reduce_launch<T, NC, NP, APOL, 1>((const T *)W, (T *)C, MN, G, s);
+  else if (G <= 4 * SK_THREADS)
+    sk_reduce_launch<T, NC, NP, APOL, 4>((const T *)W, (T *)C, MN, G, s);
+  else
+    sk_reduce_launch<T, NC, NP, APOL, 16>((const T *)W, (T *)C, MN, G, s);
+  return hipGetLastError();
 }
 
 template <typename T, int NC>

@@ -101,12 +101,14 @@ def test_validation_splitk(L):
     sl = L.mc_matmul_splitk_slices
     sl.restype = ctypes.c_int64
     sl.argtypes = [ctypes.c_int64] * 3
-    # default slice count: about 2^18 lanes, at most K / 8, at most 2^20, at least 1
-    assert sl(64, 64, 64) == 8
+    # default slice count: about 2^20 lanes, at most K / 64, at most 2^20, at least 1
+    assert sl(64, 64, 64) == 1
     assert sl(4096, 1, 4096) == 64
+    assert sl(8192, 1, 8192) == 128
     assert sl(1, 1, 1 << 24) == 1 << 18
-    assert sl(1, 1, 1 << 30) == 1 << 18  # the 2^20 cap binds explicit slice counts only
-    assert sl(1, 1, 100) == 12
+    assert sl(1, 1, 1 << 30) == 1 << 20
+    assert sl(1, 1, 6400) == 100
+    assert sl(1, 1, 100) == 1
     assert sl(1024, 1024, 1024) == 1
     assert sl(1, 1, 3) == 1
     assert sl(-1, 1, 3) == MCF_E_SHAPE
@@ -115,8 +117,8 @@ def test_validation_splitk(L):
     assert ws(1, 3, 4, 4, 4096, 1, 0, 257) == 2 * 1 * 3 * 16 * 4
     assert ws(0, 2, 4, 4, 4096, 1, 1, 1024) == 4 * 2 * 2 * 16 * 2
     assert ws(1, 3, 4, 4, 4096, 1, 0, (1 << 20) + 1) == MCF_E_ARG
-    # G = 274 group roots and 2 roots of their groups of 256
-    assert ws(1, 3, 4, 4, 1 << 20, 1, 0, 70000) == (274 + 2) * 1 * 3 * 16 * 4
+    # G = 274 group roots, and no further level in the workspace
+    assert ws(1, 3, 4, 4, 1 << 20, 1, 0, 70000) == 274 * 1 * 3 * 16 * 4
     assert ws(1, 3, 4, 4, 100, 1, 0, 1000) == 0  # capped at K = 100 slices
     assert f(1, 3, 4, 4, 4096, a, 0, b, 0, 16, None, 0, c, None) == MCF_E_ARG
     assert f(1, 7, 4, 4, 4096, a, 1, b, 0, 16, None, 0, c, None) == MCF_E_NC
@@ -152,13 +154,13 @@ def test_validation_splitk_noalloc(L):
     assert f(1, 3, 0, 4, 4096, None, 1, None, 0, 16, None, None) == MCF_OK
     assert f(1, 3, 4, 4, 4096, None, 1, b, 0, 16, c, None) == MCF_E_NULL
     assert f(1, 3, 4, 4, 4096, a, 1, b, 0, 16, P(0x100000 + 8), None) == MCF_E_ALIAS
-    # 4 x 4096 outputs at 2^20 slices: 4112 roots of 3 x 16384 binary32 components
+    # 4 x 4096 outputs at 2^20 slices: 4096 roots of 3 x 16384 binary32 components
     need = ws(1, 3, 4, 4096, 1 << 20, 1, 0, 1 << 20)
-    assert need == 4112 * 3 * 16384 * 4 > 8 << 20
+    assert need == 4096 * 3 * 16384 * 4 > 8 << 20
     far = [P(k << 40) for k in (1, 2, 3)]  # operands of several GiB must not overlap
     assert f(1, 3, 4, 4096, 1 << 20, far[0], 1, far[1], 0, 1 << 20, far[2], None) == MCF_E_SCRATCH
     # the largest roots the default slice count asks for fit with room to spare
-    assert ws(2, 4, 1, 1023, 1 << 30, 1, 1, 0) == 261888 < 8 << 20
+    assert ws(2, 4, 1, 4095, 1 << 30, 1, 1, 0) == 2 * 16 * 4095 * 8 == 1048320 < 8 << 20
     assert L.mc_status_str(MCF_E_SCRATCH).decode().startswith("MCF_E_SCRATCH")
 
 

@@ -54,11 +54,11 @@ def test_one_slice_equals_mc_matmul(mcf):
 
 @pytest.mark.parametrize("dt,nc", [(np.float32, 2), (np.float32, 3), (np.float16, 3)])
 def test_dot(mcf, orc, dt, nc):
-    """Dot-MCN (M = N = 1), K = 200003, default slice count (25000: 98 workgroups)."""
+    """Dot-MCN (M = N = 1), K = 200003, default slice count (3125: 13 workgroups)."""
     K = 200003
     A, B = inputs.matmul_normal(1, 1, K, nc, dt, seed=96)
     S = mcf.mc_matmul_splitk_slices(1, 1, K)
-    assert S == K // 8
+    assert S == K // 64
     got = to_host(mcf.mc_matmul_splitk(to_dev(A), to_dev(B[:1]), nc=nc, b_mc=False))
     want = orc.matmul_splitk(A, B[:1], nc=nc, b_mc=False, slices=S)
     assert_bits(got, want, f"dot {dt.__name__} nc={nc}")
@@ -75,12 +75,14 @@ def test_dot_max_slices(mcf, orc):
     check_bound(orc, A, B, got, 2, K, np.float32)
 
 
-@pytest.mark.parametrize("S", [70000, 1 << 20])
-def test_dot_three_levels(mcf, orc, S):
-    """More than 256 slice groups: the second tree level runs over aligned groups of
-    256 roots and a third combines their roots.  S = 70000: 274 groups (the last
-    partial), 2 second-level roots; S = 2^20 (the maximum): 4096 groups, 16 roots;
-    K = 2^21 + 3, so the largest S has two or three steps per slice."""
+@pytest.mark.parametrize("S", [70000, 1 << 18, 300000, 1 << 20])
+def test_dot_many_groups(mcf, orc, S):
+    """More than 256 slice groups: the second launch folds aligned blocks of 4 or 16
+    group roots per lane before its lane tree.  S = 70000: 274 groups, blocks of 4,
+    the last one partial; S = 2^18 (the default Dot slice count): 1024 groups, 256 full
+    blocks of 4; S = 300000: 1172 groups, blocks of 16, the last of 4 roots; S = 2^20
+    (the maximum): 4096 groups, 256 full blocks of 16.  K = 2^21 + 3, so the largest S
+    has two or three steps per slice."""
     K = (1 << 21) + 3
     A, B = inputs.matmul_normal(1, 1, K, 2, np.float32, seed=98)
     got = to_host(mcf.mc_matmul_splitk(to_dev(A), to_dev(B), nc=2, slices=S))
@@ -90,9 +92,10 @@ def test_dot_three_levels(mcf, orc, S):
 
 
 @pytest.mark.parametrize("dt", [np.float16, np.float32])
-def test_small_outputs_three_levels(mcf, orc, dt):
-    """Several outputs (3 x 2, MC x MC, nc = 3) with 70000 slices: second-level
-    groups of 256 roots per output in a two-dimensional grid, then a third level."""
+def test_small_outputs_many_groups(mcf, orc, dt):
+    """Several outputs (3 x 2, MC x MC, nc = 3) with 70000 slices: 274 group roots per
+    output, folded in blocks of 4 by a 128-lane group per output in the second
+    launch."""
     M, N, K, nc = 3, 2, 150_001, 3
     A, B = inputs.matmul_normal(M, N, K, nc, dt, seed=99)
     got = to_host(mcf.mc_matmul_splitk(to_dev(A), to_dev(B), nc=nc, slices=70000))
@@ -112,14 +115,16 @@ def test_mv(mcf, orc, dt):
     check_bound(orc, A, B[:1], got, nc, K, dt)
 
 
-def test_config_64_fp32_nc2(mcf, orc):
+@pytest.mark.parametrize("slices", [0, 8])
+def test_config_64_fp32_nc2(mcf, orc, slices):
     """The 64^3 binary32 nc = 2 workload (uniform [-1, 1], seed 0) through the K-split
-    product with its default 8 slices: bitwise against the oracle's K-split product,
-    and within 2^-40 relative of the exact product."""
+    product, with its default slice count (1 at this size, where a slice keeps at least
+    64 steps) and with 8 slices: bitwise against the oracle's K-split product, and
+    within 2^-40 relative of the exact product."""
     A, B = inputs.matmul_uniform(64, 64, 64, 2, np.float32, seed=0)
-    S = mcf.mc_matmul_splitk_slices(64, 64, 64)
-    got = to_host(mcf.mc_matmul_splitk(to_dev(A), to_dev(B), nc=2))
-    assert_bits(got, orc.matmul_splitk(A, B, nc=2, slices=S), "64^3 split")
+    S = slices or mcf.mc_matmul_splitk_slices(64, 64, 64)
+    got = to_host(mcf.mc_matmul_splitk(to_dev(A), to_dev(B), nc=2, slices=slices))
+    assert_bits(got, orc.matmul_splitk(A, B, nc=2, slices=S), f"64^3 split S={S}")
     assert check_bound(orc, A, B, got, 2, 64, np.float32) < 2.0 ** -40
 
 
@@ -147,16 +152,17 @@ def test_workspace_reuse_and_degenerate(mcf, orc):
 
 def test_bench_shapes(mcf, orc):
     """The K-split launch configurations the benchmark times (default slice counts):
-    Dot of two binary32 nc = 2 MC vectors at 2^18 slices (1024 workgroups of 256
-    slices, a second tree level over groups of 256 roots and a third over the 4
-    roots of those) with K = 2^22 + 5 (the benchmark's 2^24 takes the same launch;
-    the one-output oracle is sequential),
-    bitwise and within the bound; MV of an 8192 x 8192 binary32 nc = 3 MC matrix by a
-    plain vector, in full on the GPU, on 48 sampled rows."""
+    Dot of two binary32 nc = 2 MC vectors at the 2^18 slices of a 2^24 Dot (1024
+    workgroups of 256 slices, then one launch that folds the 1024 group roots in
+    blocks of 4 per lane and runs a 256-lane tree over them) with K = 2^22 + 5 (the
+    same launch; the one-output oracle is sequential), bitwise and within the bound;
+    MV of an 8192 x 8192 binary32 nc = 3 MC matrix by a plain vector (128 slices), in
+    full on the GPU, on 48 sampled rows."""
     K = (1 << 22) + 5
+    S = mcf.mc_matmul_splitk_slices(1, 1, 1 << 24)
+    assert S == 1 << 18
     A, B = inputs.matmul_normal(1, 1, K, 2, np.float32, seed=0)
-    got = to_host(mcf.mc_matmul_splitk(to_dev(A), to_dev(B), nc=2))
-    S = mcf.mc_matmul_splitk_slices(1, 1, K)
+    got = to_host(mcf.mc_matmul_splitk(to_dev(A), to_dev(B), nc=2, slices=S))
     assert_bits(got, orc.matmul_splitk(A, B, nc=2, slices=S), "dot 2^24")
     check_bound(orc, A, B, got, 2, K, np.float32)
     n = 8192

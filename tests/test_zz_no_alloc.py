@@ -45,7 +45,7 @@ def noalloc(mcf, A, B, nc, a_mc, b_mc, S):
 
 
 CASES = [
-    # (format, nc, M, N, K, a_mc, b_mc, slices): scratch bytes 7 372 800, 16 448, 720
+    # (format, nc, M, N, K, a_mc, b_mc, slices): scratch bytes 7 372 800, 16 384, 720
     (np.float32, 3, 32, 64, 30000, True, True, 25600),
     (np.float32, 2, 1, 1, (1 << 20) + 3, True, True, 1 << 18),
     (np.float16, 3, 3, 2, 100003, True, False, 5000),
