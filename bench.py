@@ -184,13 +184,33 @@ class Timer:
         return [s.elapsed_time(e) for s, e in self.pairs]
 
 
-def bench_matmul(torch, mcf, A, B, nc, steps, warmup, a_mc=True, b_mc=True):
+def warm(torch, fn, seconds=0.2, min_calls=3):
+    """Untimed calls of fn for at least `seconds` of wall time (and min_calls calls):
+    the timed calls that follow then run at the clocks the workload holds once the GPU
+    is busy, not during the ramp after the host-side work before it (input generation,
+    error checks), which costs the first calls of a 1 ms product up to 10%."""
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    n = 0
+    while n < min_calls or time.perf_counter() - t0 < seconds:
+        fn()
+        n += 1
+        if n % 4 == 0:
+            torch.cuda.synchronize()
+    torch.cuda.synchronize()
+
+
+def bench_matmul(torch, mcf, A, B, nc, steps, warmup, a_mc=True, b_mc=True, warm_s=0.0):
+    """warmup untimed calls (warm_s > 0: untimed calls for warm_s seconds instead),
+    then `steps` timed ones."""
     tA = torch.from_numpy(A).cuda()
     tB = torch.from_numpy(B).cuda()
     M, K = A.shape[1:]
     N = B.shape[2]
     C = torch.empty((nc, M, N), dtype=tA.dtype, device="cuda")
-    for _ in range(warmup):
+    if warm_s > 0:
+        warm(torch, lambda: mcf.mc_matmul(tA, tB, nc=nc, a_mc=a_mc, b_mc=b_mc, out=C), warm_s, warmup)
+    for _ in range(0 if warm_s > 0 else warmup):
         mcf.mc_matmul(tA, tB, nc=nc, a_mc=a_mc, b_mc=b_mc, out=C)
     torch.cuda.synchronize()
     tm = Timer(torch)
@@ -339,8 +359,7 @@ def bench_elementwise(torch, mcf, inputs, steps=10):
     ops["exp_mcn_f32"] = (lambda: mcf.mc_exp(e32, nc=nc, out=out32), 24)
     res = {}
     for name, (fn, bpe) in ops.items():
-        for _ in range(2):
-            fn()
+        warm(torch, fn)
         tm = Timer(torch)
         for _ in range(steps):
             tm.run(fn)
@@ -374,8 +393,7 @@ def bench_splitk(torch, mcf, inputs, steps=20):
         wb = mcf.mc_matmul_splitk_workspace(1, nc, M, N, K, a_mc, b_mc, S)
         ws = torch.empty(max(wb, 1), dtype=torch.uint8, device="cuda")
         fn = lambda: mcf.mc_matmul_splitk(tA, tB, nc=nc, a_mc=a_mc, b_mc=b_mc, out=out, workspace=ws)
-        for _ in range(3):
-            fn()
+        warm(torch, fn)
         tm = Timer(torch)
         for _ in range(steps):
             tm.run(fn)
@@ -414,8 +432,7 @@ def bench_batched(torch, mcf, inputs, steps=20):
         cases.append(("addmm", lambda: mcf.mc_addmm(tA2, tB2, tY2, nc=nc, alpha=1.0, beta=1.0, out=out2),
                       500 * 200 * 100))
         for name, fn, macs in cases:
-            for _ in range(3):
-                fn()
+            warm(torch, fn)
             tm = Timer(torch)
             for _ in range(steps):
                 tm.run(fn)
@@ -445,8 +462,7 @@ def bench_linear(torch, mcf, oracle, inputs, layers=100):
             host[l] = (np.ascontiguousarray(W.transpose(0, 2, 1)), b)
     tx = torch.from_numpy(x).cuda()
     y = torch.empty((nc, T, O), dtype=torch.float16, device="cuda")
-    mcf.mc_linear_fwd(tx, Ws[0], bs[0], out=y)
-    torch.cuda.synchronize()
+    warm(torch, lambda: mcf.mc_linear_fwd(tx, Ws[0], bs[0], out=y))
     tm = Timer(torch)
     t0 = time.perf_counter()
     for W, b in zip(Ws, bs):
@@ -467,7 +483,7 @@ def bench_linear(torch, mcf, oracle, inputs, layers=100):
     ws = torch.empty(mcf.mc_linear_bwd_workspace(0, nc, T, I, O), dtype=torch.uint8, device="cuda")
     for kind, dY, mc in (("plain_dY", dYmc[0].contiguous(), False), ("mc_dY", dYmc, True)):
         run = lambda: mcf.mc_linear_bwd(tx, Ws[0], dY, dy_mc=mc, workspace=ws)
-        run()
+        warm(torch, run)
         tb = Timer(torch)
         for _ in range(3):
             tb.run(run)
@@ -517,9 +533,7 @@ def bench_exact(torch, mcf, oracle, inputs, steps=20):
             run = lambda: mcf.mc_linear_fwd_exact(tA[0], tB, tb, out=C, workspace=ws)
         else:
             run = lambda: mcf.mc_matmul_exact(tA, tB, nc=nc, out=C, workspace=ws)
-        for _ in range(3):
-            run()
-        torch.cuda.synchronize()
+        warm(torch, run)
         tm = Timer(torch)
         for _ in range(steps):
             tm.run(run)
@@ -549,8 +563,7 @@ def bench_scaled(torch, mcf, oracle, inputs, steps=5):
         tA, tB = torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda()
         C = torch.empty((nc, 1024, 1024), dtype=torch.float16, device="cuda")
         run = lambda: mcf.mc_matmul(tA, tB, nc=nc, out=C, scaled=True)
-        for _ in range(2):
-            run()
+        warm(torch, run)
         tm = Timer(torch)
         for _ in range(steps):
             tm.run(run)
@@ -574,8 +587,7 @@ def bench_scaled(torch, mcf, oracle, inputs, steps=5):
     tx, tW, tb = (torch.from_numpy(v).cuda() for v in (x, W, b))
     y = torch.empty((3, 4096, 1024), dtype=torch.float16, device="cuda")
     run = lambda: mcf.mc_linear_fwd(tx, tW, tb, out=y, scaled=True)
-    for _ in range(2):
-        run()
+    warm(torch, run)
     tm = Timer(torch)
     for _ in range(steps):
         tm.run(run)
@@ -616,8 +628,7 @@ def bench_f64(torch, mcf, oracle, inputs, steps=10):
            "exp_mcn": (lambda: mcf.mc_exp(a, nc=nc, out=out), 32)}
     res = {}
     for name, (fn, bpe) in ops.items():
-        for _ in range(2):
-            fn()
+        warm(torch, fn)
         tm = Timer(torch)
         for _ in range(steps):
             tm.run(fn)
@@ -631,7 +642,7 @@ def bench_f64(torch, mcf, oracle, inputs, steps=10):
     del a, b, d, v, out
     A = inputs.expansion(g, (1024, 1024), nc, np.float64, 1 / 32)
     B = inputs.expansion(g, (1024, 1024), nc, np.float64, 1 / 32)
-    C, _, kms = bench_matmul(torch, mcf, A, B, nc, 5, 2)
+    C, _, kms = bench_matmul(torch, mcf, A, B, nc, 10, 3, warm_s=0.2)
     macs = 1024 ** 3
     res["matmul_1024_nc2"] = {
         "ms": round(kms, 3), "MC-GFLOP/s": round(2 * macs / (kms * 1e-3) / 1e9, 1),
@@ -849,13 +860,13 @@ def main():
         del Cph
     if not args.no_extra and want("small"):
         A1, B1 = inputs.matmul_uniform(64, 64, 64, 2, np.float32, seed=0)
-        C1, ms1, k1 = bench_matmul(torch, mcf, A1, B1, 2, 20, 3)
+        C1, ms1, k1 = bench_matmul(torch, mcf, A1, B1, 2, 20, 3, warm_s=0.2)
         extra["matmul_64_f32_nc2"] = {"us": round(k1 * 1e3, 1),
                                       "error": exact_error(oracle, A1, B1, C1.cpu().numpy(), 2, 64, np.float32,
                                                            count=4096)}
         for nc3 in (2, 3):
             A3, B3 = inputs.matmul_normal(1024, 1024, 1024, nc3, np.float16, seed=0)
-            C3, ms3, k3 = bench_matmul(torch, mcf, A3, B3, nc3, 5, 2)
+            C3, ms3, k3 = bench_matmul(torch, mcf, A3, B3, nc3, 10, 3, warm_s=0.2)
             macs = 1024 ** 3
             extra[f"matmul_1024_f16_nc{nc3}"] = {
                 "ms": round(k3, 3), "MC-GFLOP/s": round(2 * macs / (k3 * 1e-3) / 1e9, 1),
