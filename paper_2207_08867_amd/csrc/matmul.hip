@@ -136,15 +136,20 @@ struct Lane {
 
   // ScalingN of term (x, v) in kept-terms form; lanes failing the test run the
   // general step.  HEAD / TAIL: the products' errors are known to be zero (see mm_kernel).
+  // With several outputs per lane (the MC-Linear shape) the tests are wavefront masks
+  // and a failing lane sends its wavefront through the general step (3.26 -> 3.20 ms
+  // per 4096 x 1024 x 1024 layer); with one output per lane the per-lane branch
+  // measured 1% faster.
+  static constexpr bool KEPT_MASK = TM * TN > 1;
   template <bool HEAD, bool TAIL>
   __device__ __forceinline__ void scale_kept(const T (&x)[NC], T v, T (&t)[NC]) {
-    kept_scale<T, NC, HEAD, TAIL>(x, v, t);
+    kept_scale<T, NC, HEAD, TAIL, KEPT_MASK>(x, v, t);
   }
 
   // a = Add-MCN(a, t) in kept-terms form (TINY: the add_tiny form)
   template <bool TINY>
   __device__ __forceinline__ void add_kept_into(T (&a)[NC], const T (&t)[NC]) {
-    kept_add<T, NC, TINY>(a, t);
+    kept_add<T, NC, TINY, KEPT_MASK>(a, t);
   }
 
   // Pruned MC x MC product: component P of B multiplies the first NC - P components
@@ -227,9 +232,10 @@ struct Lane {
   }
 
   // S consecutive reduction steps kk .. kk+S-1 in kept-terms form, all terms of all
-  // S steps behind one test: a lane whose test fails anywhere restores its
-  // accumulators and redoes the S steps with the general steps (full terms and the
-  // compaction network), so a wavefront takes one rarely-taken branch per S steps.
+  // S steps behind one test: when a lane's test fails anywhere, the wavefront restores
+  // its accumulators and redoes the S steps with the general steps (full terms and the
+  // compaction network; a lane whose kept terms were valid gets the same values), so a
+  // wavefront takes one rarely-taken uniform branch per S steps.
   template <int PMASK, bool TPS, int S>
   __device__ __forceinline__ void group_kept(const T (*As)[KT][BM], const T (*Bs)[KT][BN], int kk, int tx, int ty) {
     T saved[NP][TM][TN][NC];
@@ -241,7 +247,7 @@ struct Lane {
         for (int j = 0; j < TN; ++j)
 #pragma unroll
           for (int c = 0; c < NC; ++c) saved[p][i][j][c] = acc[p][i][j][c];
-    bool bad = false;
+    uint64_t bad = 0;  // lanes failing a test, as a wavefront mask
 #pragma unroll
     for (int st = 0; st < S; ++st) {
       Ops o;
@@ -256,26 +262,26 @@ struct Lane {
             T t[NC], sum[NC], last;
             if constexpr (!AMC) {
               scaling_kept<T, NC, false, TPS>(o.b[j], o.a[i][0], t, last);
-              bad |= kept_invalid<T, NC, TPS, true>(t, last);
+              bad |= kept_invalid_mask<T, NC, TPS, true>(t, last);
             } else if (TPS && p > 0) {
               scaling_kept<T, NC, true, true>(o.a[i], o.b[j][p], t, last);
-              bad |= kept_invalid<T, NC, true, true>(t, last);
+              bad |= kept_invalid_mask<T, NC, true, true>(t, last);
             } else {
               scaling_kept<T, NC, false, TPS>(o.a[i], o.b[j][p], t, last);
-              bad |= kept_invalid<T, NC, TPS, true>(t, last);
+              bad |= kept_invalid_mask<T, NC, TPS, true>(t, last);
             }
             if (AMC && BMC && TPS && p > 0) {
-              bad |= add_tiny<T, NC>(acc[p][i][j], t, sum);
+              bad |= add_tiny_mask<T, NC>(acc[p][i][j], t, sum);
             } else {
               add_kept<T, NC>(acc[p][i][j], t, sum, last);
-              bad |= kept_invalid<T, NC, false>(sum, last);
+              bad |= kept_invalid_mask<T, NC, false>(sum, last);
             }
 #pragma unroll
             for (int c = 0; c < NC; ++c) acc[p][i][j][c] = sum[c];
           }
       }
     }
-    if (__builtin_expect(bad, 0)) {
+    if (__builtin_expect(bad != 0, 0)) {
 #pragma unroll
       for (int p = 0; p < NP; ++p)
 #pragma unroll
@@ -329,8 +335,20 @@ struct Lane {
       // nc = 2: the tests of two steps share one branch.  (For nc >= 3 grouping keeps
       // more temporaries live, lowers the wavefronts per SIMD and was measured
       // slower; there each step tests and branches on its own, below.)
+      // Two groups per iteration: each group keeps its input accumulators live for the
+      // redo, so with one group per iteration the new accumulators were copied back
+      // into the old registers at the back edge (4 of 54 VALU instructions per two
+      // steps); with two the registers alternate.  Together with the mask tests:
+      // 1024^3 nc = 2 0.733 -> 0.699 ms.
       int kk = kk0;
-      for (; kk + 1 < kt; kk += 2) group_kept<PMASK, TPS, 2>(As, Bs, kk, tx, ty);
+      for (; kk + 3 < kt; kk += 4) {
+        group_kept<PMASK, TPS, 2>(As, Bs, kk, tx, ty);
+        group_kept<PMASK, TPS, 2>(As, Bs, kk + 2, tx, ty);
+      }
+      if (kk + 1 < kt) {
+        group_kept<PMASK, TPS, 2>(As, Bs, kk, tx, ty);
+        kk += 2;
+      }
       if (kk < kt) group_kept<PMASK, TPS, 1>(As, Bs, kk, tx, ty);
       return;
     }

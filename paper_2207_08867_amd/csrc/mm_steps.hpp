@@ -297,29 +297,70 @@ __device__ __forceinline__ bool kept_invalid(const T (&h)[N], T last) {
   }
 }
 
+// The same tests as wavefront lane masks (bit l for active lane l): the flags stay
+// masks in scalar registers, combined there (a flag and the negation of another take
+// one scalar and-not instead of a second compare), and the step that follows can
+// branch once for the wavefront.  A lane whose kept terms are valid gets the same
+// terms from the general step, so a wavefront may run the general step for all its
+// lanes whenever one of them fails.
+__device__ __forceinline__ uint64_t lane_mask(bool b) { return __builtin_amdgcn_ballot_w64(b); }
+
+template <typename T, int N, bool LAST_EXACT, bool ORDERED = false>
+__device__ __forceinline__ uint64_t kept_invalid_mask(const T (&h)[N], T last) {
+  if constexpr (N == 1) {
+    return 0;
+  } else {
+    uint64_t z[N];
+#pragma unroll
+    for (int i = 0; i < N; ++i) z[i] = lane_mask(h[i] == T(0));
+    uint64_t bad = 0;
+#pragma unroll
+    for (int i = 0; i + 1 < N; ++i) bad |= ORDERED ? lane_mask(out_of_order(h[i], h[i + 1])) : (z[i] & ~z[i + 1]);
+    if constexpr (LAST_EXACT) return bad;
+    return bad | (z[N - 1] & lane_mask(!abs_below(last, (T)exact_limit<T>())));
+  }
+}
+
+template <typename T, int N>
+__device__ __forceinline__ uint64_t add_tiny_mask(const T (&x)[N], const T (&y)[N], T (&h)[N]) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) h[i] = x[i] + y[i];
+  uint64_t bad = lane_mask(!abs_below(h[0], (T)exact_limit<T>()));
+#pragma unroll
+  for (int i = 0; i + 1 < N; ++i) bad |= lane_mask(out_of_order(h[i], h[i + 1]));
+  return bad;
+}
+
 // ScalingN of (x, v) in kept-terms form into t; lanes failing the test run the
-// general step.  HEAD / TAIL: the products' errors are known to be zero.
-template <typename T, int N, bool HEAD, bool TAIL>
+// general step (MASK: the whole wavefront runs it when one lane fails, see
+// kept_invalid_mask).  HEAD / TAIL: the products' errors are known to be zero.
+template <typename T, int N, bool HEAD, bool TAIL, bool MASK = false>
 __device__ __forceinline__ void kept_scale(const T (&x)[N], T v, T (&t)[N]) {
   T last;
   scaling_kept<T, N, HEAD, TAIL>(x, v, t, last);
-  if (__builtin_expect(kept_invalid<T, N, TAIL, true>(t, last), 0)) {
+  bool bad;
+  if constexpr (MASK)
+    bad = kept_invalid_mask<T, N, TAIL, true>(t, last) != 0;
+  else
+    bad = kept_invalid<T, N, TAIL, true>(t, last);
+  if (__builtin_expect(bad, 0)) {
     T h[N + 1];
     scaling_terms<T, N>(x, v, h);
     compact_nz<T, N + 1, N>(h, t);
   }
 }
 
-// a = Add-MCN(a, t) in kept-terms form (TINY: the add_tiny form).
-template <typename T, int N, bool TINY>
+// a = Add-MCN(a, t) in kept-terms form (TINY: the add_tiny form; MASK as in
+// kept_scale).
+template <typename T, int N, bool TINY, bool MASK = false>
 __device__ __forceinline__ void kept_add(T (&a)[N], const T (&t)[N]) {
   T s[N], last;
   bool bad;
   if constexpr (TINY) {
-    bad = add_tiny<T, N>(a, t, s);
+    bad = MASK ? add_tiny_mask<T, N>(a, t, s) != 0 : add_tiny<T, N>(a, t, s);
   } else {
     add_kept<T, N>(a, t, s, last);
-    bad = kept_invalid<T, N, false>(s, last);
+    bad = MASK ? kept_invalid_mask<T, N, false>(s, last) != 0 : kept_invalid<T, N, false>(s, last);
   }
   if (__builtin_expect(bad, 0)) {
     T h[N + 1];
