@@ -152,6 +152,21 @@ struct Lane {
     kept_add<T, NC, TINY, KEPT_MASK>(a, t);
   }
 
+  // ScalingN of (x, v) when every product x_i v is exact and |x_0| >= |x_1| >= ...
+  // (tile flags TPS and ORD): the terms are the products themselves, in magnitude
+  // order, so the kept-terms test cannot fail and is not run.
+  __device__ __forceinline__ void scale_exact(const T (&x)[NC], T v, T (&t)[NC]) {
+    T last;
+    scaling_kept<T, NC, true, true>(x, v, t, last);
+  }
+  template <bool ORD>
+  __device__ __forceinline__ void scale_low(const T (&x)[NC], T v, T (&t)[NC]) {
+    if constexpr (ORD)
+      scale_exact(x, v, t);
+    else
+      scale_kept<true, true>(x, v, t);
+  }
+
   // Pruned MC x MC product: component P of B multiplies the first NC - P components
   // of A in MM-MCN order with NC - P components; the accumulator of P keeps zeros in
   // its other components, so the epilogue's Add-MCN combination pads it with zeros.
@@ -196,9 +211,9 @@ struct Lane {
   }
 
   // term k = 0 initialises the accumulators
-  template <bool TPS>
+  template <bool TPS, bool ORD>
   __device__ __forceinline__ void first(const Ops &o) {
-    first_terms<TPS>(o);
+    first_terms<TPS, ORD>(o);
     if constexpr (!PRUNE) {  // (the pruned parts are patched in prune_step)
 #pragma unroll
       for (int p = 0; p < NP; ++p)
@@ -208,7 +223,7 @@ struct Lane {
           for (int j = 0; j < TN; ++j) nonfinite_tail<T, NC>(acc[p][i][j]);
     }
   }
-  template <bool TPS>
+  template <bool TPS, bool ORD>
   __device__ __forceinline__ void first_terms(const Ops &o) {
     if constexpr (PRUNE) {
       prune_step<0, (1 << NP) - 1, TPS, true>(o);
@@ -222,7 +237,7 @@ struct Lane {
             if constexpr (!AMC)
               scale_kept<false, TPS>(o.b[j], o.a[i][0], acc[p][i][j]);
             else if (TPS && p > 0)
-              scale_kept<true, true>(o.a[i], o.b[j][p], acc[p][i][j]);
+              scale_low<ORD>(o.a[i], o.b[j][p], acc[p][i][j]);
             else
               scale_kept<false, TPS>(o.a[i], o.b[j][p], acc[p][i][j]);
           }
@@ -236,7 +251,7 @@ struct Lane {
   // its accumulators and redoes the S steps with the general steps (full terms and the
   // compaction network; a lane whose kept terms were valid gets the same values), so a
   // wavefront takes one rarely-taken uniform branch per S steps.
-  template <int PMASK, bool TPS, int S>
+  template <int PMASK, bool TPS, int S, bool ORD>
   __device__ __forceinline__ void group_kept(const T (*As)[KT][BM], const T (*Bs)[KT][BN], int kk, int tx, int ty) {
     T saved[NP][TM][TN][NC];
 #pragma unroll
@@ -265,7 +280,7 @@ struct Lane {
               bad |= kept_invalid_mask<T, NC, TPS, true>(t, last);
             } else if (TPS && p > 0) {
               scaling_kept<T, NC, true, true>(o.a[i], o.b[j][p], t, last);
-              bad |= kept_invalid_mask<T, NC, true, true>(t, last);
+              if constexpr (!ORD) bad |= kept_invalid_mask<T, NC, true, true>(t, last);
             } else {
               scaling_kept<T, NC, false, TPS>(o.a[i], o.b[j][p], t, last);
               bad |= kept_invalid_mask<T, NC, TPS, true>(t, last);
@@ -317,7 +332,7 @@ struct Lane {
 
   // steps kk0 .. kt-1 of a tile.  GROUP = false: each term's ScalingN and Add-MCN run
   // back to back, so only one term is live at a time.
-  template <int PMASK, bool TPS>
+  template <int PMASK, bool TPS, bool ORD>
   __device__ __forceinline__ void run(const T (*As)[KT][BM], const T (*Bs)[KT][BN], int kk0, int kt, int tx,
                                       int ty) {
     // two steps per loop iteration, so the accumulators keep their registers across
@@ -342,14 +357,14 @@ struct Lane {
       // 1024^3 nc = 2 0.733 -> 0.699 ms.
       int kk = kk0;
       for (; kk + 3 < kt; kk += 4) {
-        group_kept<PMASK, TPS, 2>(As, Bs, kk, tx, ty);
-        group_kept<PMASK, TPS, 2>(As, Bs, kk + 2, tx, ty);
+        group_kept<PMASK, TPS, 2, ORD>(As, Bs, kk, tx, ty);
+        group_kept<PMASK, TPS, 2, ORD>(As, Bs, kk + 2, tx, ty);
       }
       if (kk + 1 < kt) {
-        group_kept<PMASK, TPS, 2>(As, Bs, kk, tx, ty);
+        group_kept<PMASK, TPS, 2, ORD>(As, Bs, kk, tx, ty);
         kk += 2;
       }
-      if (kk < kt) group_kept<PMASK, TPS, 1>(As, Bs, kk, tx, ty);
+      if (kk < kt) group_kept<PMASK, TPS, 1, ORD>(As, Bs, kk, tx, ty);
       return;
     }
 #pragma unroll 2
@@ -369,7 +384,7 @@ struct Lane {
                 scale_kept<false, TPS>(o.b[j], o.a[i][0], term);
                 add_kept_into<false>(acc[p][i][j], term);
               } else if (BMC && TPS && p > 0) {
-                scale_kept<true, true>(o.a[i], o.b[j][p], term);
+                scale_low<ORD>(o.a[i], o.b[j][p], term);
                 add_kept_into<true>(acc[p][i][j], term);
               } else {
                 scale_kept<false, TPS>(o.a[i], o.b[j][p], term);
@@ -533,11 +548,17 @@ mm_kernel(const T *__restrict__ A, const T *__restrict__ B,
   // c + p >= 1 (x the MC operand, v_p the other operand's components), is below
   // exact_limit, so that its Two-Prod error is zero (a product's error is at most half
   // the spacing of the format at the product, which below exact_limit is half the
-  // smallest subnormal, and that rounds to zero).
+  // smallest subnormal, and that rounds to zero).  For MC x MC one more slot notes
+  // whether some value of A in the tile has components out of magnitude order
+  // (|a_c| < |a_{c+1}|, or a NaN); when none has and the products are exact, the
+  // ScalingN terms of B's low components are exact products in magnitude order and
+  // need no kept-terms test (ORD).
   constexpr bool TRACK = SPOL == SR_SUFFIX && NC > 1;
-  __shared__ uint32_t mx[2][NA + NB];
+  constexpr bool ORD_OK = TRACK && AMC && BMC && !PRUNE;
+  constexpr int NSLOT = NA + NB + (ORD_OK ? 1 : 0);
+  __shared__ uint32_t mx[2][NSLOT];
   if constexpr (TRACK) {
-    if (threadIdx.x < 2 * (NA + NB)) (&mx[0][0])[threadIdx.x] = 0;
+    if (threadIdx.x < 2 * NSLOT) (&mx[0][0])[threadIdx.x] = 0;
     __syncthreads();
   }
 
@@ -547,9 +568,9 @@ mm_kernel(const T *__restrict__ A, const T *__restrict__ B,
     const int kt = (int)((K - k0) < KT ? (K - k0) : KT);
     // registers -> LDS: A transposed to [k][m]; note which planes of B hold a non-zero
     int nonzero_planes = 0;
-    uint32_t lmax[NA + NB];
+    uint32_t lmax[NSLOT];
 #pragma unroll
-    for (int c = 0; c < NA + NB; ++c) lmax[c] = 0;
+    for (int c = 0; c < NSLOT; ++c) lmax[c] = 0;
 #pragma unroll
     for (int t = 0; t < A_PER; ++t) {
       const int idx = threadIdx.x + t * MM_THREADS;
@@ -558,6 +579,8 @@ mm_kernel(const T *__restrict__ A, const T *__restrict__ B,
         for (int c = 0; c < NA; ++c) {
           As[c][idx % KT][idx / KT] = ra[t][c];
           if constexpr (TRACK) lmax[c] = max(lmax[c], __float_as_uint(__builtin_fabsf((float)ra[t][c])));
+          if constexpr (ORD_OK)
+            if (c + 1 < NA && out_of_order(ra[t][c], ra[t][c + 1 < NA ? c + 1 : c])) lmax[NA + NB] = 1;
         }
       }
     }
@@ -577,7 +600,7 @@ mm_kernel(const T *__restrict__ A, const T *__restrict__ B,
     if constexpr (TRACK) {
       // wavefront maximum (DPP), then one LDS atomic per wavefront and plane
 #pragma unroll
-      for (int c = 0; c < NA + NB; ++c) {
+      for (int c = 0; c < NSLOT; ++c) {
         const uint32_t w = __ockl_wfred_max_u32(lmax[c]);
         if (threadIdx.x % warpSize == 0) atomicMax(&mx[tile & 1][c], w);
       }
@@ -589,7 +612,7 @@ mm_kernel(const T *__restrict__ A, const T *__restrict__ B,
     } else {
       __syncthreads();
     }
-    bool tps = false;
+    bool tps = false, ord = false;
     if constexpr (TRACK) {
       // X: the MC operand's planes, V: the other operand's planes
       constexpr int X0 = AMC ? 0 : NA, NX = AMC ? NA : NB;
@@ -602,29 +625,34 @@ mm_kernel(const T *__restrict__ A, const T *__restrict__ B,
           if (c + p >= 1)
             tps = tps && __uint_as_float(mx[tile & 1][X0 + c]) * __uint_as_float(mx[tile & 1][V0 + p]) <
                              exact_limit<T>();
+      if constexpr (ORD_OK) ord = mx[tile & 1][NA + NB] == 0;
       // the other slot set was last read during the previous tile, before its final
       // barrier, and is next written by the next tile, after this tile's final barrier
-      if (threadIdx.x < NA + NB) mx[(tile & 1) ^ 1][threadIdx.x] = 0;
+      if (threadIdx.x < NSLOT) mx[(tile & 1) ^ 1][threadIdx.x] = 0;
     }
     if (k0 + KT < K) fetch(k0 + KT);  // next tile, in flight during this one
-    auto steps = [&](auto tps_c) {
+    auto steps = [&](auto tps_c, auto ord_c) {
       constexpr bool TPS = decltype(tps_c)::value;
+      constexpr bool ORD = decltype(ord_c)::value;
       int kk0 = 0;
       if (k0 == 0) {  // term k = 0 initialises the accumulators
         typename decltype(lane)::Ops o;
         o.load(As, Bs, 0, tx, ty);
-        lane.template first<TPS>(o);
+        lane.template first<TPS, ORD>(o);
         kk0 = 1;
       }
       if (NP > 1 && pmask != ALL)
-        lane.template run<(ALL >> 1), TPS>(As, Bs, kk0, kt, tx, ty);
+        lane.template run<(ALL >> 1), TPS, ORD>(As, Bs, kk0, kt, tx, ty);
       else
-        lane.template run<ALL, TPS>(As, Bs, kk0, kt, tx, ty);
+        lane.template run<ALL, TPS, ORD>(As, Bs, kk0, kt, tx, ty);
     };
-    if (TRACK && tps)
-      steps(std::integral_constant<bool, TRACK>{});
+    using no = std::integral_constant<bool, false>;
+    if (TRACK && tps && ord)
+      steps(std::integral_constant<bool, TRACK>{}, std::integral_constant<bool, ORD_OK>{});
+    else if (TRACK && tps)
+      steps(std::integral_constant<bool, TRACK>{}, no{});
     else
-      steps(std::integral_constant<bool, false>{});
+      steps(no{}, no{});
     __syncthreads();
   }
 

@@ -5,7 +5,8 @@ The binary16 product computes only the terms Simple-Renorm keeps and proves per
 lane that the dropped final carry is zero (zeros form a trailing run and the last
 operation is exact, |result| < 2^-13); per tile it decides from the largest
 magnitude of each component plane whether the products of low components are
-exact.  These inputs make each of those decisions go both ways:
+exact, and whether A's components are in magnitude order.  These inputs make each of
+those decisions go both ways:
   * per-row and per-column scales spread over 2^-14 .. 2^2, so some tiles have
     exact low products and others do not, and the last-term test fails for some
     lanes and passes for others;
@@ -13,7 +14,8 @@ exact.  These inputs make each of those decisions go both ways:
     (not normalized MC values; the algorithms are defined for any component
     tuple), so zero terms appear before non-zero ones;
   * products straddling 2^-13 exactly;
-  * pairs of reduction steps that cancel exactly, so accumulators return to zero.
+  * pairs of reduction steps that cancel exactly, so accumulators return to zero;
+  * zero leading components of A in some tiles only.
 """
 import numpy as np
 import pytest
@@ -163,6 +165,26 @@ def test_growing_low_accumulators(mcf, orc, nc):
     B = inputs.split(2.0 ** -5 * (1.0 + g.uniform(0.0, 1.0, (K, N))), nc, np.float16)
     got = to_host(mcf.mc_matmul(to_dev(A), to_dev(B), nc=nc))
     assert_bits(got, orc.matmul(A, B, nc=nc), f"growing nc={nc}")
+
+
+@pytest.mark.parametrize("nc", [2, 3])
+def test_component_order_flag(mcf, orc, nc):
+    """MC x MC with every low-component product below 2^-13 (N(0, 1/K) splits): per
+    32-step tile the product skips the kept-terms test of B's low components when every
+    value of A in the tile has its components in magnitude order.  Here some values of
+    A in the k ranges 32..63 and 160..191 (and in a few rows only) get a zero leading
+    component (a low component then exceeds the leading one), so those tiles run the
+    test and its failing lanes take the general step, while the other tiles skip it."""
+    M, N, K = 80, 48, 256
+    g = np.random.default_rng(1150 + nc)
+    A, B = inputs.matmul_normal(M, N, K, nc, np.float16, seed=1160 + nc)
+    rows = g.choice(M, 12, replace=False)
+    for k0 in (32, 160):
+        ks = k0 + g.integers(0, 32, 12)
+        A[0, rows, ks] = np.where(g.random(12) < 0.5, np.float16(0.0), np.float16(-0.0))
+    assert (np.abs(A[1]) > np.abs(A[0])).any()
+    got = to_host(mcf.mc_matmul(to_dev(A), to_dev(B), nc=nc))
+    assert_bits(got, orc.matmul(A, B, nc=nc), f"order flag nc={nc}")
 
 
 def unordered(g, shape, nc, nonfinite=0):
