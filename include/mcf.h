@@ -325,7 +325,9 @@ int mc_linear_fwd(int dtype, int nc, int64_t batch, int64_t in, int64_t out, con
  * dX: [nc][batch][in], dW: [nc][out][in], db: [nc][out] -- each may be NULL (not
  * computed); outputs must not overlap the inputs, each other or the workspace.
  * workspace: device memory of at least mc_linear_bwd_workspace(...) bytes when dW or
- *   db is requested (dY^T staged in nc planes and a column of ones), owned by the
+ *   db is requested (dY^T staged in nc planes; then a column of ones, or, when both dW
+ *   and db are requested, x with a column of ones appended and the [dW | db] product,
+ *   which gives both in one pass), owned by the
  *   caller, not overlapping the inputs; contents on entry do not matter; calls sharing
  *   it must not overlap in time.  Too small: MCF_E_ARG; NULL when needed: MCF_E_NULL.
  * dtype: MCF_F16, MCF_F32, MCF_F64.  Sizes: batch, out <= 2^20, in <= 2^30 (and the

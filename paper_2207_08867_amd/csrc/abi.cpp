@@ -447,7 +447,7 @@ int mc_linear_fwd_exact(int dtype, int nc, int64_t batch, int64_t in, int64_t ou
 int64_t mc_linear_bwd_workspace(int dtype, int nc, int64_t batch, int64_t in, int64_t out) {
   const int st = linear_bwd_check(dtype, nc, batch, in, out);
   if (st != MCF_OK) return st;
-  return mcf::linear_bwd_workspace_bytes(dtype, nc, batch, out);
+  return mcf::linear_bwd_workspace_bytes(dtype, nc, batch, in, out);
 }
 
 int mc_linear_bwd(int dtype, int nc, int64_t batch, int64_t in, int64_t out, const void *x, const void *W,
@@ -467,7 +467,7 @@ int mc_linear_bwd(int dtype, int nc, int64_t batch, int64_t in, int64_t out, con
   if ((dX || dW) && in > 0 && batch > 0 && (!x || !W)) return MCF_E_NULL;
   if (batch > 0 && out > 0 && !dY) return MCF_E_NULL;
   const bool staged = dW || db;
-  const int64_t wb = staged ? mcf::linear_bwd_workspace_bytes(dtype, nc, batch, out) : 0;
+  const int64_t wb = staged ? mcf::linear_bwd_workspace_bytes(dtype, nc, batch, in, out) : 0;
   if (staged) {
     if (!workspace) return MCF_E_NULL;
     if (workspace_bytes < wb) return MCF_E_ARG;

@@ -91,8 +91,9 @@ hipError_t launch_scaled_matmul(int nc, int64_t M, int64_t N, int64_t K, const v
 
 // MC-Linear backward (linear_bwd.hip): dX = dY W, dW = dY^T x, db = column sums of dY
 // (each output optional); dY is [nc or 1][batch][out] (dy_mc).  ws holds
-// linear_bwd_workspace_bytes(...) bytes (dY^T promoted to nc planes, a column of ones).
-int64_t linear_bwd_workspace_bytes(int dtype, int nc, int64_t batch, int64_t out);
+// linear_bwd_workspace_bytes(...) bytes (dY^T promoted to nc planes; then a column of
+// ones, or x with a column of ones appended and the [dW | db] product).
+int64_t linear_bwd_workspace_bytes(int dtype, int nc, int64_t batch, int64_t in, int64_t out);
 hipError_t launch_linear_bwd(int dtype, int nc, int64_t batch, int64_t in, int64_t out, const void *x, const void *W,
                              const void *dY, int dy_mc, void *dX, void *dW, void *db, void *ws, hipStream_t stream);
 
