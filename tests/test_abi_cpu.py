@@ -187,3 +187,18 @@ def test_scaled_format_rejections(L):
     assert L.mc_matmul_pruned(3, 3, 4, 4, 4, x, y, o, None) == MCF_E_DTYPE
     assert L.mc_matmul(4, 3, 4, 4, 4, x, 1, y, 1, o, None) == MCF_E_DTYPE
     assert L.mc_matmul(3, 3, 4, 4, 4, x, 1, y, 1, P(0x100000 + 8), None) == MCF_E_ALIAS
+
+
+def test_linear_bwd_workspace(L):
+    """The backward's workspace: dY^T in nc planes, then the larger of a column of ones
+    (db alone) and x with a column of ones appended plus the [dW | db] product (both)."""
+    f = L.mc_linear_bwd_workspace
+    f.restype = ctypes.c_int64
+    f.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64]
+    a = lambda n: (n + 255) // 256 * 256
+    # binary16 nc = 3, batch 4096, in 1024, out 1024 (the benchmark's layer)
+    assert f(0, 3, 4096, 1024, 1024) == a(3 * 1024 * 4096 * 2) + a(4096 * 1025 * 2) + a(3 * 1024 * 1025 * 2)
+    # binary32 nc = 2, batch 10, in 0: [x | 1] is the column of ones itself
+    assert f(1, 2, 10, 0, 5) == a(2 * 5 * 10 * 4) + a(10 * 4) + a(2 * 5 * 4)
+    assert f(0, 3, -1, 4, 4) == MCF_E_SHAPE
+    assert f(7, 3, 4, 4, 4) == MCF_E_DTYPE
