@@ -466,13 +466,20 @@ struct MmArgs {
 // Occupancy: with nc <= 3, binary32 kernels run at least 5 wavefronts per SIMD (at most
 // 96 VGPRs); they sit just under that bound (the 8192^3 one spills one 8-byte value
 // outside its loop) and one register more would drop them to 4.  The binary16 kernels
-// (but the pruned ones) run 8, the most a SIMD holds: at 64 VGPRs the few values that
-// no longer fit are per-tile addresses, reloaded once per tile, and the 1024^3
-// products run 4-6% faster than at 5 or 6 wavefronts.  nc = 4 needs more registers.
+// (but the pruned ones) run 7 or 8.  MC-Linear (BT) and nc = 1 run 8, the most a SIMD
+// holds: at 64 VGPRs the few values that no longer fit are per-tile addresses,
+// reloaded once per tile.  The other nc = 2 and 3 products run 7 (72 VGPRs: fewer
+// spills around the tile loop): 1024^3 nc = 2 0.70 -> 0.67 ms, nc = 3 1.30 -> 1.26 ms
+// (6 wavefronts: 0.67 / 1.29, 5: 0.72 ms); MC-Linear is 1% slower at 7.  nc = 4 needs
+// more registers.
+template <int NC, bool BT>
+constexpr int f16_waves() {
+  return NC >= 2 && !BT ? 7 : 8;
+}
 template <typename T, int NC, bool AMC, bool BMC, bool BT, int TM, int TN, int KT, int SPOL, int APOL,
           bool GROUP, bool ADDMM, bool PRUNE>
 __global__ __attribute__((amdgpu_flat_work_group_size(1, MM_THREADS),
-                          amdgpu_waves_per_eu(sizeof(T) == 2 && NC <= 3 && !PRUNE ? 8
+                          amdgpu_waves_per_eu(sizeof(T) == 2 && NC <= 3 && !PRUNE ? f16_waves<NC, BT>()
                                               : (NC <= 3 && sizeof(T) <= 4 ? 5 : 1)))) void
 mm_kernel(const T *__restrict__ A, const T *__restrict__ B,
                                                         T *__restrict__ C, const MmArgs<T> g) {
