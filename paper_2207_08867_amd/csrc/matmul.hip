@@ -332,7 +332,7 @@ struct Lane {
 
   // steps kk0 .. kt-1 of a tile.  GROUP = false: each term's ScalingN and Add-MCN run
   // back to back, so only one term is live at a time.
-  template <int PMASK, bool TPS, bool ORD>
+  template <int PMASK, bool TPS, bool ORD, int DEPTH = 1>
   __device__ __forceinline__ void run(const T (*As)[KT][BM], const T (*Bs)[KT][BN], int kk0, int kt, int tx,
                                       int ty) {
     // two steps per loop iteration, so the accumulators keep their registers across
@@ -367,6 +367,24 @@ struct Lane {
       if (kk < kt) group_kept<PMASK, TPS, 1, ORD>(As, Bs, kk, tx, ty);
       return;
     }
+    if constexpr (DEPTH > 1 && SPOL != SR_SUFFIX && !GROUP) {
+      // Grids of few wavefronts, where nothing hides a step's LDS latency: the operands
+      // of DEPTH steps are read first, then the steps run on them in k order.
+      int kk = kk0;
+      for (; kk + DEPTH <= kt; kk += DEPTH) {
+        Ops os[DEPTH];
+#pragma unroll
+        for (int u = 0; u < DEPTH; ++u) os[u].load(As, Bs, kk + u, tx, ty);
+#pragma unroll
+        for (int u = 0; u < DEPTH; ++u) full_step<PMASK>(os[u]);
+      }
+      for (; kk < kt; ++kk) {
+        Ops o;
+        o.load(As, Bs, kk, tx, ty);
+        full_step<PMASK>(o);
+      }
+      return;
+    }
 #pragma unroll 2
     for (int kk = kk0; kk < kt; ++kk) {
       Ops o;
@@ -397,25 +415,33 @@ struct Lane {
         scale<PMASK>(o, term);
         add<PMASK>(term);
       } else {
-#pragma unroll
-        for (int p = 0; p < NP; ++p) {
-          if (!((PMASK >> p) & 1)) continue;
-#pragma unroll
-          for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int j = 0; j < TN; ++j) {
-              const T v = AMC ? o.b[j][p] : o.a[i][0];
-              T h[NC + 1], term[NC];
-              if constexpr (AMC)
-                scaling_terms<T, NC>(o.a[i], v, h);
-              else
-                scaling_terms<T, NC>(o.b[j], v, h);
-              if (__builtin_expect(sr_try<T, NC, SPOL>(h, term, v == T(0)), 0)) compact_nz<T, NC + 1, NC>(h, term);
-              add_terms<T, NC>(acc[p][i][j], term, h);
-              if (__builtin_expect(sr_try<T, NC, APOL>(h, acc[p][i][j]), 0)) compact_nz<T, NC + 1, NC>(h, acc[p][i][j]);
-            }
-        }
+        full_step<PMASK>(o);
       }
+    }
+  }
+
+  // One reduction step in the general form: each term's ScalingN and Add-MCN back to
+  // back, with Simple-Renorm's fast path (SPOL / APOL) and the compaction network for
+  // lanes that fail its test.
+  template <int PMASK>
+  __device__ __forceinline__ void full_step(const Ops &o) {
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      if (!((PMASK >> p) & 1)) continue;
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const T v = AMC ? o.b[j][p] : o.a[i][0];
+          T h[NC + 1], term[NC];
+          if constexpr (AMC)
+            scaling_terms<T, NC>(o.a[i], v, h);
+          else
+            scaling_terms<T, NC>(o.b[j], v, h);
+          if (__builtin_expect(sr_try<T, NC, SPOL>(h, term, v == T(0)), 0)) compact_nz<T, NC + 1, NC>(h, term);
+          add_terms<T, NC>(acc[p][i][j], term, h);
+          if (__builtin_expect(sr_try<T, NC, APOL>(h, acc[p][i][j]), 0)) compact_nz<T, NC + 1, NC>(h, acc[p][i][j]);
+        }
     }
   }
 };
@@ -477,7 +503,7 @@ constexpr int f16_waves() {
   return NC >= 2 && !BT ? 7 : 8;
 }
 template <typename T, int NC, bool AMC, bool BMC, bool BT, int TM, int TN, int KT, int SPOL, int APOL,
-          bool GROUP, bool ADDMM, bool PRUNE>
+          bool GROUP, bool ADDMM, bool PRUNE, int DEPTH = 1>
 __global__ __attribute__((amdgpu_flat_work_group_size(1, MM_THREADS),
                           amdgpu_waves_per_eu(sizeof(T) == 2 && NC <= 3 && !PRUNE ? f16_waves<NC, BT>()
                                               : (NC <= 3 && sizeof(T) <= 4 ? 5 : 1)))) void
@@ -649,9 +675,9 @@ mm_kernel(const T *__restrict__ A, const T *__restrict__ B,
         kk0 = 1;
       }
       if (NP > 1 && pmask != ALL)
-        lane.template run<(ALL >> 1), TPS, ORD>(As, Bs, kk0, kt, tx, ty);
+        lane.template run<(ALL >> 1), TPS, ORD, DEPTH>(As, Bs, kk0, kt, tx, ty);
       else
-        lane.template run<ALL, TPS, ORD>(As, Bs, kk0, kt, tx, ty);
+        lane.template run<ALL, TPS, ORD, DEPTH>(As, Bs, kk0, kt, tx, ty);
     };
     using no = std::integral_constant<bool, false>;
     if (TRACK && tps && ord)
@@ -702,7 +728,7 @@ mm_kernel(const T *__restrict__ A, const T *__restrict__ B,
 constexpr int64_t MM_MAX_GRID_Y = 65535;
 
 template <typename T, int NC, bool AMC, bool BMC, bool BT, int TM, int TN, int SPOL, int APOL, int KT = 16,
-          bool PRUNE = false>
+          bool PRUNE = false, int DEPTH = 1>
 static hipError_t mm_launch_tile(MmArgs<T> g, int64_t batches, const void *A, const void *B, void *C,
                                  hipStream_t s) {
   constexpr int BM = 16 * TM, BN = 16 * TN;
@@ -711,10 +737,10 @@ static hipError_t mm_launch_tile(MmArgs<T> g, int64_t batches, const void *A, co
     g.bb0 = b0;
     const int64_t nb = (batches - b0) < MM_MAX_GRID_Y ? (batches - b0) : MM_MAX_GRID_Y;
     if (g.mode == 2)  // the AddMM epilogue is a separate instantiation: it needs more registers
-      hipLaunchKernelGGL((mm_kernel<T, NC, AMC, BMC, BT, TM, TN, KT, SPOL, APOL, false, true, PRUNE>),
+      hipLaunchKernelGGL((mm_kernel<T, NC, AMC, BMC, BT, TM, TN, KT, SPOL, APOL, false, true, PRUNE, DEPTH>),
                          dim3(gx, (unsigned)nb), dim3(MM_THREADS), 0, s, (const T *)A, (const T *)B, (T *)C, g);
     else
-      hipLaunchKernelGGL((mm_kernel<T, NC, AMC, BMC, BT, TM, TN, KT, SPOL, APOL, false, false, PRUNE>),
+      hipLaunchKernelGGL((mm_kernel<T, NC, AMC, BMC, BT, TM, TN, KT, SPOL, APOL, false, false, PRUNE, DEPTH>),
                          dim3(gx, (unsigned)nb), dim3(MM_THREADS), 0, s, (const T *)A, (const T *)B, (T *)C, g);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -737,6 +763,11 @@ static hipError_t mm_launch(const MmArgs<T> &g, int64_t batches, const void *A, 
   } else if constexpr (sizeof(T) == 4) {
     if (g.M * g.N >= ((int64_t)1 << 25))
       return mm_launch_tile<T, NC, AMC, BMC, BT, 1, 2, SR_FULL, SR_FULL, 16, PRUNE>(g, batches, A, B, C, s);
+    // up to 2^20 outputs in all (at most 4 wavefronts per SIMD): the operands of 8 steps
+    // are read from LDS before the steps run
+    if constexpr (!PRUNE)
+      if (g.M * g.N <= ((int64_t)1 << 20) / (batches > 0 ? batches : 1))
+        return mm_launch_tile<T, NC, AMC, BMC, BT, 1, 1, SR_FULL, SR_FULL, 16, PRUNE, 8>(g, batches, A, B, C, s);
     return mm_launch_tile<T, NC, AMC, BMC, BT, 1, 1, SR_FULL, SR_FULL, 16, PRUNE>(g, batches, A, B, C, s);
   } else {
     if constexpr (BT)  // MC-Linear: two rows of x per lane share each weight value; 32-step tiles (2.5% faster)
