@@ -367,21 +367,30 @@ struct Lane {
       if (kk < kt) group_kept<PMASK, TPS, 1, ORD>(As, Bs, kk, tx, ty);
       return;
     }
-    if constexpr (DEPTH > 1 && SPOL != SR_SUFFIX && !GROUP) {
-      // Grids of few wavefronts, where nothing hides a step's LDS latency: the operands
-      // of DEPTH steps are read first, then the steps run on them in k order.
+    if constexpr (DEPTH > 1 && !GROUP) {
+      // The operands of DEPTH steps are read from LDS first, then the steps run on them
+      // in k order: for binary32 grids of few wavefronts, where nothing hides a step's
+      // LDS latency, and for the binary16 MC-Linear kernel.
       int kk = kk0;
       for (; kk + DEPTH <= kt; kk += DEPTH) {
         Ops os[DEPTH];
 #pragma unroll
         for (int u = 0; u < DEPTH; ++u) os[u].load(As, Bs, kk + u, tx, ty);
 #pragma unroll
-        for (int u = 0; u < DEPTH; ++u) full_step<PMASK>(os[u]);
+        for (int u = 0; u < DEPTH; ++u) {
+          if constexpr (SPOL == SR_SUFFIX)
+            kept_step<PMASK, TPS, ORD>(os[u]);
+          else
+            full_step<PMASK>(os[u]);
+        }
       }
       for (; kk < kt; ++kk) {
         Ops o;
         o.load(As, Bs, kk, tx, ty);
-        full_step<PMASK>(o);
+        if constexpr (SPOL == SR_SUFFIX)
+          kept_step<PMASK, TPS, ORD>(o);
+        else
+          full_step<PMASK>(o);
       }
       return;
     }
@@ -390,26 +399,7 @@ struct Lane {
       Ops o;
       o.load(As, Bs, kk, tx, ty);
       if constexpr (SPOL == SR_SUFFIX) {
-#pragma unroll
-        for (int p = 0; p < NP; ++p) {
-          if (!((PMASK >> p) & 1)) continue;
-#pragma unroll
-          for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int j = 0; j < TN; ++j) {
-              T term[NC];
-              if constexpr (!AMC) {
-                scale_kept<false, TPS>(o.b[j], o.a[i][0], term);
-                add_kept_into<false>(acc[p][i][j], term);
-              } else if (BMC && TPS && p > 0) {
-                scale_low<ORD>(o.a[i], o.b[j][p], term);
-                add_kept_into<true>(acc[p][i][j], term);
-              } else {
-                scale_kept<false, TPS>(o.a[i], o.b[j][p], term);
-                add_kept_into<false>(acc[p][i][j], term);
-              }
-            }
-        }
+        kept_step<PMASK, TPS, ORD>(o);
       } else if constexpr (GROUP) {
         T term[NP][TM][TN][NC];
         scale<PMASK>(o, term);
@@ -417,6 +407,31 @@ struct Lane {
       } else {
         full_step<PMASK>(o);
       }
+    }
+  }
+
+  // One reduction step in kept-terms form, term by term.
+  template <int PMASK, bool TPS, bool ORD>
+  __device__ __forceinline__ void kept_step(const Ops &o) {
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      if (!((PMASK >> p) & 1)) continue;
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          T term[NC];
+          if constexpr (!AMC) {
+            scale_kept<false, TPS>(o.b[j], o.a[i][0], term);
+            add_kept_into<false>(acc[p][i][j], term);
+          } else if (BMC && TPS && p > 0) {
+            scale_low<ORD>(o.a[i], o.b[j][p], term);
+            add_kept_into<true>(acc[p][i][j], term);
+          } else {
+            scale_kept<false, TPS>(o.a[i], o.b[j][p], term);
+            add_kept_into<false>(acc[p][i][j], term);
+          }
+        }
     }
   }
 
@@ -770,7 +785,13 @@ static hipError_t mm_launch(const MmArgs<T> &g, int64_t batches, const void *A, 
         return mm_launch_tile<T, NC, AMC, BMC, BT, 1, 1, SR_FULL, SR_FULL, 16, PRUNE, 8>(g, batches, A, B, C, s);
     return mm_launch_tile<T, NC, AMC, BMC, BT, 1, 1, SR_FULL, SR_FULL, 16, PRUNE>(g, batches, A, B, C, s);
   } else {
-    if constexpr (BT)  // MC-Linear: two rows of x per lane share each weight value; 32-step tiles (2.5% faster)
+    // MC-Linear: two rows of x per lane share each weight value; 32-step tiles (2.5%
+    // faster); at nc = 3 the operands of two steps are read before they run (3.18 ->
+    // 3.05 ms per 4096 x 1024 x 1024 layer; the same for the 1024^3 MC x MC product was
+    // slower: 1.26 -> 1.31 ms)
+    if constexpr (BT && NC == 3)
+      return mm_launch_tile<T, NC, AMC, BMC, BT, 2, 1, SR_SUFFIX, SR_SUFFIX, 32, false, 2>(g, batches, A, B, C, s);
+    if constexpr (BT)
       return mm_launch_tile<T, NC, AMC, BMC, BT, 2, 1, SR_SUFFIX, SR_SUFFIX, NC <= 3 ? 32 : 16>(g, batches, A, B, C, s);
     // 32-step LDS tiles halve the per-tile staging and barriers (1024^3: nc = 2 8%
     // faster than 16 steps, nc = 3 4% at eight wavefronts per SIMD; 64 steps slower)
